@@ -1,0 +1,373 @@
+"""Pins of the fp64 oracle against facts fixed outside it: the paper's
+definitions and printed data, closed forms, special cases, brute force and
+torch's reference decoder layer.  CPU only."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import evo_oracle as O
+from paper_2607_20293_amd import inputs as I
+from tests.conftest import load_printed_schedules, printed_unit_lattice
+
+TINY = I.TINY
+
+
+def _tiny_inputs(variant="perturbed", batch=2, seed=0):
+    w = I.make_weights(TINY, seed, variant)
+    P = O.prepare_params(I.split_weights(TINY, w), "fp32")
+    obs = I.make_obs(TINY, batch, seed)
+    noise = I.make_noise(TINY, batch, seed)
+    return P, obs, noise
+
+
+# ---------------------------------------------------------------- elementary
+def test_layer_norm_matches_torch():
+    rng = np.random.default_rng(1)
+    v = rng.standard_normal((5, 64)) * 3 + 0.7
+    g = rng.standard_normal(64)
+    b = rng.standard_normal(64)
+    ref = torch.nn.functional.layer_norm(torch.tensor(v), (64,), torch.tensor(g), torch.tensor(b), eps=1e-5)
+    np.testing.assert_allclose(O.layer_norm(v, g, b), ref.numpy(), rtol=0, atol=1e-13)
+
+
+def test_gelu_matches_torch_exact_erf():
+    v = np.linspace(-8, 8, 1001)
+    ref = torch.nn.functional.gelu(torch.tensor(v), approximate="none").numpy()
+    np.testing.assert_allclose(O.gelu(v), ref, rtol=1e-14, atol=1e-15)
+
+
+def test_sinusoid_special_values():
+    d = 64
+    s0 = O.sinusoid(0, d)
+    assert np.array_equal(s0, np.concatenate([np.zeros(32), np.ones(32)]))
+    k = 37
+    s = O.sinusoid(k, d)
+    # first frequency is 1, last is 1e-4
+    assert s[0] == pytest.approx(math.sin(k), abs=1e-15)
+    assert s[31] == pytest.approx(math.sin(k * 1e-4), abs=1e-15)
+    assert s[32] == pytest.approx(math.cos(k), abs=1e-15)
+    np.testing.assert_allclose(s[:32] ** 2 + s[32:] ** 2, 1.0, atol=1e-15)
+
+
+def test_bf16_rounding_matches_torch():
+    rng = np.random.default_rng(2)
+    a = np.concatenate([rng.standard_normal(4096).astype(np.float32) * 0.02,
+                        np.array([1.0, -1.0, 0.0, 3.0e38, 1.00390625, 1.01171875, 65504.0], np.float32)])
+    ref = torch.tensor(a).to(torch.bfloat16).to(torch.float64).numpy()
+    assert np.array_equal(O.to_bf16(a), ref)
+
+
+# -------------------------------------------------------------- attention
+def test_attention_two_token_brute_force():
+    rng = np.random.default_rng(3)
+    dh = 8
+    q = rng.standard_normal((2, dh))
+    k = rng.standard_normal((2, dh))
+    v = rng.standard_normal((2, dh))
+    o = O.attention(q, k, v, 1, causal=True)
+    # row 0 can only see key 0: output is exactly v0
+    assert np.array_equal(o[0], v[0])
+    s10, s11 = q[1] @ k[0] / math.sqrt(dh), q[1] @ k[1] / math.sqrt(dh)
+    w0 = 1.0 / (1.0 + math.exp(-(s10 - s11)))
+    np.testing.assert_allclose(o[1], w0 * v[0] + (1 - w0) * v[1], rtol=1e-14, atol=1e-15)
+    # unmasked, two memory tokens: same logistic form for every query
+    oc = O.attention(q, k, v, 1, causal=False)
+    for i in range(2):
+        a, b = q[i] @ k[0] / math.sqrt(dh), q[i] @ k[1] / math.sqrt(dh)
+        w = 1.0 / (1.0 + math.exp(-(a - b)))
+        np.testing.assert_allclose(oc[i], w * v[0] + (1 - w) * v[1], rtol=1e-14, atol=1e-15)
+
+
+@pytest.mark.parametrize("causal", [True, False])
+def test_attention_matches_sdpa(causal):
+    rng = np.random.default_rng(4)
+    H, S, d, nh = 16, 16 if causal else 5, 64, 4
+    q = rng.standard_normal((3, H, d))
+    k = rng.standard_normal((3, S, d))
+    v = rng.standard_normal((3, S, d))
+    o = O.attention(q, k, v, nh, causal)
+    split = lambda x: torch.tensor(x).reshape(x.shape[0], x.shape[1], nh, d // nh).transpose(1, 2)
+    ref = torch.nn.functional.scaled_dot_product_attention(split(q), split(k), split(v), is_causal=causal)
+    ref = ref.transpose(1, 2).reshape(3, H, d).numpy()
+    np.testing.assert_allclose(o, ref, rtol=0, atol=1e-13)
+
+
+# ----------------------------------------------------------- decoder layer
+@pytest.mark.parametrize("shape", [TINY, I.PUSHT])
+def test_units_equal_torch_decoder_layer(shape):
+    """h + SA + CA + FFN of one layer == torch's pre-norm decoder layer with
+    the same weights (exact-erf GELU, causal target mask)."""
+    w = I.make_weights(shape, 5, "perturbed")
+    P = O.prepare_params(I.split_weights(shape, w), "fp32")
+    d, nh = shape.d_model, shape.n_heads
+    rng = np.random.default_rng(6)
+    h = rng.standard_normal((2, shape.horizon, d))
+    mem = rng.standard_normal((2, shape.n_mem, d))
+    l = shape.n_layers - 1
+    r1 = O.unit_residual(3 * l + 0, h, mem, P, nh)
+    h1 = h + r1
+    r2 = O.unit_residual(3 * l + 1, h1, mem, P, nh)
+    h2 = h1 + r2
+    ours = h2 + O.unit_residual(3 * l + 2, h2, mem, P, nh)
+
+    layer = torch.nn.TransformerDecoderLayer(d, nh, shape.d_ff, dropout=0.0, activation="gelu",
+                                             batch_first=True, norm_first=True, layer_norm_eps=1e-5)
+    layer = layer.double().eval()
+    p = f"l{l}."
+    with torch.no_grad():
+        t = lambda a: torch.tensor(np.asarray(a, np.float64))
+        layer.norm1.weight.copy_(t(P[p + "ln1_g"])); layer.norm1.bias.copy_(t(P[p + "ln1_b"]))
+        layer.self_attn.in_proj_weight.copy_(t(P[p + "W_qkv"])); layer.self_attn.in_proj_bias.copy_(t(P[p + "b_qkv"]))
+        layer.self_attn.out_proj.weight.copy_(t(P[p + "W_o"])); layer.self_attn.out_proj.bias.copy_(t(P[p + "b_o"]))
+        layer.norm2.weight.copy_(t(P[p + "ln2_g"])); layer.norm2.bias.copy_(t(P[p + "ln2_b"]))
+        layer.multihead_attn.in_proj_weight.copy_(t(np.concatenate([P[p + "W_q"], P[p + "W_kv"]])))
+        layer.multihead_attn.in_proj_bias.copy_(t(np.concatenate([P[p + "b_q"], P[p + "b_kv"]])))
+        layer.multihead_attn.out_proj.weight.copy_(t(P[p + "W_o2"])); layer.multihead_attn.out_proj.bias.copy_(t(P[p + "b_o2"]))
+        layer.norm3.weight.copy_(t(P[p + "ln3_g"])); layer.norm3.bias.copy_(t(P[p + "ln3_b"]))
+        layer.linear1.weight.copy_(t(P[p + "W_1"])); layer.linear1.bias.copy_(t(P[p + "b_1"]))
+        layer.linear2.weight.copy_(t(P[p + "W_2"])); layer.linear2.bias.copy_(t(P[p + "b_2"]))
+        mask = torch.nn.Transformer.generate_square_subsequent_mask(shape.horizon, dtype=torch.float64)
+        ref = layer(t(h), t(mem), tgt_mask=mask).numpy()
+    np.testing.assert_allclose(ours, ref, rtol=0, atol=1e-12)
+
+
+# ------------------------------------------------------------------ sampler
+@pytest.mark.parametrize("T", [10, 100])
+def test_betas_closed_form(T):
+    tab = O.ddpm_table(T)
+    s = 0.008
+    f = lambda u: math.cos((u + s) / (1 + s) * math.pi / 2) ** 2
+    # telescoping product while the cap is inactive
+    for k in range(T - 1):
+        assert tab["abar"][k] == pytest.approx(f((k + 1) / T) / f(0.0), rel=1e-12)
+    # the 0.999 cap is active exactly at the last timestep
+    assert tab["beta"][T - 1] == 0.999
+    assert np.all(tab["beta"][: T - 1] < 0.999)
+    assert np.all(np.diff(tab["abar"]) < 0)
+
+
+@pytest.mark.parametrize("T", [10, 100])
+def test_posterior_consistency(T):
+    """The posterior of x_{k-1} given x_k = sqrt(abar_k) x0 + sqrt(1-abar_k) e
+    and x0 must have marginal mean sqrt(abar_{k-1}) x0 and marginal variance
+    1 - abar_{k-1} (forward-process marginals)."""
+    tab = O.ddpm_table(T)
+    for k in range(1, T):
+        c0, ct, sg = tab["c0"][k], tab["ct"][k], tab["sigma"][k]
+        ab, abp = tab["abar"][k], tab["abar_prev"][k]
+        assert c0 + ct * math.sqrt(ab) == pytest.approx(math.sqrt(abp), rel=1e-12)
+        assert ct ** 2 * (1 - ab) + sg ** 2 == pytest.approx(1 - abp, rel=1e-12)
+
+
+def test_step_recovers_x0_and_eps_route():
+    tab = O.ddpm_table(100)
+    rng = np.random.default_rng(7)
+    x0 = rng.uniform(-0.9, 0.9, (16, 2))
+    e = rng.standard_normal((16, 2))
+    for k in (0, 1, 50, 98):
+        ab = tab["abar"][k]
+        xk = math.sqrt(ab) * x0 + math.sqrt(1 - ab) * e
+        # true eps: clipped x0 estimate equals x0, so the step is the posterior mean
+        got = O.ddpm_step(xk, e, k, np.zeros_like(xk), tab, clip=True)
+        want = tab["c0"][k] * x0 + tab["ct"][k] * xk
+        np.testing.assert_allclose(got, want, rtol=1e-9, atol=1e-9)
+        # unclipped x0 route == epsilon route (x - beta/sqrt(1-abar) eps)/sqrt(alpha)
+        eps = rng.standard_normal((16, 2))
+        got = O.ddpm_step(xk, eps, k, np.zeros_like(xk), tab, clip=False)
+        b, a = tab["beta"][k], tab["alpha"][k]
+        want = (xk - b / math.sqrt(1 - ab) * eps) / math.sqrt(a)
+        np.testing.assert_allclose(got, want, rtol=1e-10, atol=1e-10)
+    # no noise is added at the last step (k = 0)
+    z = rng.standard_normal((16, 2))
+    a = O.ddpm_step(x0, e, 0, z, tab)
+    b = O.ddpm_step(x0, e, 0, None, tab)
+    assert np.array_equal(a, b)
+
+
+# ------------------------------------------------------- cached execution
+def test_all_refresh_equals_uncached():
+    P, obs, noise = _tiny_inputs()
+    eff = np.ones((3 * TINY.n_layers, TINY.n_steps), bool)
+    a = O.denoise_group(TINY, P, obs, noise, eff, cache=True)
+    b = O.denoise_group(TINY, P, obs, noise, eff, cache=False)
+    assert np.array_equal(a, b)
+
+
+def test_step0_only_reuses_step0_residuals():
+    """Refreshing only step 0: every later step reuses r_{b,0}, so the model
+    output is the head applied to emb(x_t) + sum_b r_{b,0}."""
+    P, obs, noise = _tiny_inputs()
+    U, T = 3 * TINY.n_layers, TINY.n_steps
+    eff = np.zeros((U, T), bool)
+    eff[:, 0] = True
+    tr = {}
+    out = O.denoise_group(TINY, P, obs, noise, eff, trace=tr)
+    assert tr["computed"][0].all() and not tr["computed"][1:].any()
+    for t in range(1, T):
+        assert np.array_equal(tr["r"][t], tr["r"][0])
+    # closed form: eps_t depends on x_t only through the embedding
+    C = tr["r"][0].sum(axis=0)
+    tab = O.ddpm_table(T)
+    x = noise[0].astype(np.float64)
+    for t in range(T):
+        k = T - 1 - t
+        h = x @ P["W_in"].T + P["b_in"] + P["P_act"] + C
+        eps = O.layer_norm(h, P["lnf_g"], P["lnf_b"]) @ P["W_out"].T + P["b_out"]
+        np.testing.assert_allclose(eps, tr["eps"][t], rtol=0, atol=1e-12)
+        x = O.ddpm_step(x, eps, k, noise[t + 1] if k > 0 else None, tab)
+    np.testing.assert_allclose(out, x, rtol=0, atol=1e-12)
+
+
+def test_most_recent_refresh_is_reused():
+    """One unit refreshed at steps {0, 2, 6}: steps 1 reuse r_0, 3..5 reuse
+    r_2, 7..9 reuse r_6 (brute-force check of 'most recently cached')."""
+    P, obs, noise = _tiny_inputs()
+    U, T = 3 * TINY.n_layers, TINY.n_steps
+    eff = np.ones((U, T), bool)
+    b = 4                                    # layer 1, CA
+    eff[b] = False
+    eff[b, [0, 2, 6]] = True
+    tr = {}
+    O.denoise_group(TINY, P, obs, noise, eff, trace=tr)
+    last = -1
+    for t in range(T):
+        if eff[b, t]:
+            last = t
+            assert tr["computed"][t, b]
+        else:
+            assert not tr["computed"][t, b]
+            assert np.array_equal(tr["r"][t, b], tr["r"][last, b])
+    assert not np.allclose(tr["r"][2, b], tr["r"][0, b])
+    # every other unit was recomputed at every step
+    assert tr["computed"][:, [u for u in range(U) if u != b]].all()
+
+
+def test_cold_policies():
+    """COLD_ZERO: a unit never refreshed contributes zero; COLD_COMPUTE
+    refreshes step 0 (S' = S u B x {0})."""
+    U, T = 3 * TINY.n_layers, TINY.n_steps
+    lat = np.zeros((U, T), np.uint8)
+    lat[:, 3] = 1
+    e0 = O.effective_lattice(O.expand_lattice(lat, O.GRAN_UNIT, 2), O.COLD_COMPUTE)
+    assert e0[:, 0].all() and e0[:, 3].all() and e0.sum() == 2 * U
+    e1 = O.effective_lattice(O.expand_lattice(lat, O.GRAN_UNIT, 2), O.COLD_ZERO)
+    assert e1.sum() == U
+    P, obs, noise = _tiny_inputs()
+    tr = {}
+    O.denoise_group(TINY, P, obs, noise, e1, trace=tr)
+    assert not tr["r"][:3].any()
+    assert np.array_equal(tr["r"][9], tr["r"][3])
+
+
+def test_layer_lattice_equals_unit_expansion():
+    P, obs, noise = _tiny_inputs()
+    rng = np.random.default_rng(8)
+    lat = I.lattice_bernoulli(TINY.n_layers, TINY.n_steps, 0.4, rng)
+    ids = np.array([0, 0], np.int32)
+    a, sa = O.denoise(TINY, I.split_weights(TINY, I.make_weights(TINY, 0, "perturbed")), obs, noise,
+                      [lat], ids, granularity=O.GRAN_LAYER)
+    ulat = np.repeat(lat, 3, axis=0)
+    b, sb = O.denoise(TINY, I.split_weights(TINY, I.make_weights(TINY, 0, "perturbed")), obs, noise,
+                      [ulat], ids, granularity=O.GRAN_UNIT)
+    assert np.array_equal(a, b)
+    assert sa == sb
+
+
+def test_samples_are_independent():
+    """A sample's chunk does not depend on the other samples in the call."""
+    P, obs, noise = _tiny_inputs(batch=3)
+    eff = O.effective_lattice(O.expand_lattice(
+        I.lattice_bernoulli(2, 10, 0.5, np.random.default_rng(9)), O.GRAN_LAYER, 2), O.COLD_COMPUTE)
+    full = O.denoise_group(TINY, P, obs, noise, eff)
+    one = O.denoise_group(TINY, P, obs[1:2], noise[:, 1:2], eff)
+    assert np.array_equal(full[1:2], one)
+
+
+def test_pairs_encoding():
+    lat = O.pairs_to_lattice([(0, 0), (5, 3), (2, 9)], 6, 10)
+    assert lat.sum() == 3 and lat[5, 3] == 1
+    with pytest.raises(ValueError):
+        O.pairs_to_lattice([(0, 0), (0, 0)], 6, 10)
+    with pytest.raises(ValueError):
+        O.pairs_to_lattice([(6, 0)], 6, 10)
+
+
+# -------------------------------------------------------------- bookkeeping
+def test_flops_match_torch_counter_and_density_identity():
+    """Projection FLOPs of one layer from torch's FLOP counter (pre-norm
+    decoder layer) plus dense attention products from the counter on explicit
+    batched products; then flops_cacheable == |S'| x per-layer FLOPs."""
+    from torch.utils.flop_counter import FlopCounterMode
+    s = I.PUSHT
+    d, nh, H, S = s.d_model, s.n_heads, s.horizon, s.n_mem
+    layer = torch.nn.TransformerDecoderLayer(d, nh, s.d_ff, dropout=0.0, activation="gelu",
+                                             batch_first=True, norm_first=True).double().eval()
+    x = torch.zeros(1, H, d, dtype=torch.float64)
+    m = torch.zeros(1, S, d, dtype=torch.float64)
+    mask = torch.nn.Transformer.generate_square_subsequent_mask(H, dtype=torch.float64)
+    with FlopCounterMode(display=False) as fc:
+        with torch.no_grad():
+            layer(x, m, tgt_mask=mask)   # masked path: projections go through counted addmm
+        dh = d // nh
+        torch.matmul(torch.zeros(1, nh, H, dh), torch.zeros(1, nh, dh, H))      # SA scores
+        torch.matmul(torch.zeros(1, nh, H, H), torch.zeros(1, nh, H, dh))       # SA values
+        torch.matmul(torch.zeros(1, nh, H, dh), torch.zeros(1, nh, dh, S))      # CA scores
+        torch.matmul(torch.zeros(1, nh, H, S), torch.zeros(1, nh, S, dh))       # CA values
+    F = O.unit_flops(s)
+    assert F["SA"] + F["CA"] + F["FFN"] == fc.get_total_flops()
+    counts = fc.get_flop_counts()
+    ffn = sum(counts["TransformerDecoderLayer.linear1"].values()) + \
+        sum(counts["TransformerDecoderLayer.linear2"].values())
+    assert F["FFN"] == ffn
+    # the values quoted for this shape
+    assert (F["SA"], F["CA"], F["FFN"]) == (8650752, 5029888, 16777216)
+    # density identity for a layer-granular lattice
+    lat = I.make_lattice("dirichlet", 8, 100, 0.25, 0)
+    st = O.bookkeeping(s, [lat], np.zeros(1, np.int32))
+    F_layer = F["SA"] + F["CA"] + F["FFN"]
+    assert st["flops_cacheable"] == int(lat.sum()) * F_layer
+    assert st["refreshes_effective"] == 3 * int(lat.sum()) == 600
+    full_cacheable = st["flops_full"] - st["flops_always"]
+    assert st["flops_cacheable"] * 4 == full_cacheable       # 25% density exactly
+
+
+def test_bookkeeping_matches_trace_counts():
+    """Refresh counts from the lattice arithmetic agree with the positions
+    the loop actually evaluated."""
+    P, obs, noise = _tiny_inputs(batch=1)
+    lat = I.lattice_bernoulli(6, 10, 0.3, np.random.default_rng(10))
+    lat[:, 0] = 0
+    lat[1, 0] = 1
+    for cold in (O.COLD_COMPUTE, O.COLD_ZERO):
+        eff = O.effective_lattice(O.expand_lattice(lat, O.GRAN_UNIT, 2), cold)
+        tr = {}
+        O.denoise_group(TINY, P, obs, noise, eff, trace=tr)
+        st = O.bookkeeping(TINY, [lat], np.zeros(1, np.int32), O.GRAN_UNIT, cold)
+        assert st["refreshes_effective"] == int(tr["computed"].sum())
+        assert st["refreshes_requested"] == int(lat.sum())
+        F = O.unit_flops(TINY)
+        per = [F["SA"], F["CA"], F["FFN"]]
+        assert st["flops_cacheable"] == sum(per[b % 3] for t, b in zip(*np.nonzero(tr["computed"])))
+
+
+# ------------------------------------------------------ printed schedules
+@pytest.mark.parametrize("tag,bac_k", [("pusht", 288), ("kitchen", 333), ("lift_ph", 329)])
+def test_printed_schedules(tag, bac_k):
+    """Appendix tables: 24 units x 100 steps; every EVO schedule has K = 240
+    (M = 10 refreshes per module on average, Sec. 4.1: K = 24 M); BAC rows
+    all refresh step 0."""
+    sch = load_printed_schedules(tag)
+    for method in ("BAC", "EVO"):
+        assert len(sch[method]) == 24
+        for steps in sch[method].values():
+            assert steps == sorted(set(steps)) and all(0 <= t < 100 for t in steps)
+    assert sum(len(v) for v in sch["EVO"].values()) == 240 == 24 * 10
+    assert sum(len(v) for v in sch["BAC"].values()) == bac_k
+    assert all(v[0] == 0 for v in sch["BAC"].values())
+    lat = printed_unit_lattice(tag, "EVO")
+    pairs = list(zip(*np.nonzero(lat)))
+    assert np.array_equal(O.pairs_to_lattice(pairs, 24, 100), lat)
+    # most EVO rows leave step 0 out: the cold-cache reading matters here
+    assert int((lat[:, 0] == 0).sum()) >= 20
