@@ -1,0 +1,195 @@
+/*
+ * evo.h -- C ABI of the schedule-driven cached denoising loop (EVO,
+ * arXiv 2607.20293) on AMD Instinct MI355X (gfx950).
+ *
+ * The method (Sec. 3.1, Eq. 1): a pretrained transformer diffusion policy
+ * runs T reverse denoising steps; the self-attention, cross-attention and
+ * feed-forward residual branches of its L decoder layers are B = 3L
+ * cacheable units.  A schedule S, a subset of the unit x step lattice with
+ * |S| = K (Eq. 2, Eq. 3), decides where a unit's residual branch is
+ * evaluated (and its cache refreshed); everywhere else the unit adds the
+ * residual cached at its most recent refresh.  Caches are reset at the
+ * start of every action query (Sec. 3.1, Sec. 3.4).  Weights, sampler and
+ * action interface are those of the unchanged policy.
+ *
+ * Conventions for every call:
+ *  - Return value: EVO_OK (0) or a negative EVO_E_* code; evo_last_error()
+ *    then returns a thread-local message.  Every argument is validated
+ *    before any device work is enqueued; on error nothing is enqueued and
+ *    the policy is unchanged.
+ *  - "host" pointers are ordinary CPU memory, read during the call only
+ *    (copied; the caller may free them on return).  "device" pointers are
+ *    HIP device memory on the policy's device; they stay owned by the
+ *    caller and must stay valid until the enqueued work completes.
+ *  - A policy is bound to the HIP device that was current at creation.
+ *    Calls on one policy are not thread-safe.
+ */
+#ifndef EVO_H
+#define EVO_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+  EVO_OK = 0,
+  EVO_E_INVALID = -1,     /* bad argument (shape, value, NULL pointer, id) */
+  EVO_E_STATE = -2,       /* call not valid in the current state (e.g. unknown schedule) */
+  EVO_E_NOMEM = -3,       /* device or pinned host allocation failed */
+  EVO_E_HIP = -4,         /* HIP runtime error (message has the HIP error string) */
+  EVO_E_UNSUPPORTED = -5  /* valid request outside the compiled shape set */
+};
+
+enum { EVO_FP32 = 0, EVO_BF16 = 1 };          /* matmul operand precision */
+enum { EVO_GRAN_LAYER = 0, EVO_GRAN_UNIT = 1 };/* lattice rows = L layers or 3L units */
+enum { EVO_COLD_COMPUTE = 0, EVO_COLD_ZERO = 1 };
+
+/* Policy shape and options.
+ *   n_layers L, d_model d, n_heads h (d % h == 0), d_ff, horizon H (action
+ *   tokens), action_dim A, n_obs_tokens, obs_dim, n_steps T.
+ *   dtype: EVO_BF16 multiplies the projection matrices (obs projection,
+ *     QKV, attention outputs, cross-attention Q and KV, MLP) in bfloat16
+ *     (weights rounded to nearest even at creation) with fp32 accumulation;
+ *     EVO_FP32 keeps them fp32.  The residual stream, LayerNorm statistics,
+ *     softmax, GELU, embeddings, head and sampler are fp32 in both modes.
+ *   cold_policy: what a unit does at a step where it is not scheduled but
+ *     has never been refreshed in this query.  Eq. 1 leaves it open (the
+ *     caches are reset per query).  EVO_COLD_COMPUTE evaluates every unit at
+ *     step 0 (S' = S u B x {0}); EVO_COLD_ZERO adds a zero residual.
+ *   clip_sample: nonzero clips the sampler's x0 estimate to [-1, 1].
+ *   max_batch: largest batch evo_denoise accepts (sizes the caches).
+ *   max_schedules: number of schedule ids (0 .. max_schedules-1). */
+typedef struct {
+  int32_t n_layers, d_model, n_heads, d_ff, horizon, action_dim;
+  int32_t n_obs_tokens, obs_dim, n_steps;
+  int32_t dtype, cold_policy, clip_sample;
+  int32_t max_batch, max_schedules;
+} evo_policy_desc;
+
+/* Bookkeeping of the last evo_denoise call, summed over the batch.
+ * Refreshes count unit positions (b, t) of the effective schedule.  FLOPs
+ * count 2 per multiply-add of the matrix products (attention score and
+ * value products dense) following Tables 1-3's "FLOPs for action
+ * generation":
+ *   per sample and evaluation  F_SA  = 2(4 H d^2 + 2 H^2 d)
+ *                              F_CA  = 2(2 H d^2 + 2 S d^2 + 2 H S d)
+ *                              F_FFN = 4 H d d_ff          (S = 1 + n_obs)
+ *   always-on per step 4 H A d, per query 2 n_obs obs_dim d.
+ * flops_kernel is what this implementation multiplies: the cross-attention
+ * key/value products of the observation tokens are done once per query and
+ * those of the time token once per policy, so they are not repeated at
+ * each refresh.  The byte counters are this implementation's algorithmic
+ * traffic: cache reads/writes of reused/refreshed residuals, and weight
+ * bytes of evaluated units summed over workgroups. */
+typedef struct {
+  uint64_t refreshes_requested;
+  uint64_t refreshes_effective;
+  uint64_t flops_cacheable;
+  uint64_t flops_always;
+  uint64_t flops_full;
+  uint64_t flops_kernel;
+  uint64_t cache_bytes_read;
+  uint64_t cache_bytes_written;
+  uint64_t weight_bytes;
+  uint64_t n_tiles;
+} evo_stats;
+
+typedef struct evo_policy evo_policy;
+
+/* Number of floats of the flat weight vector for `desc`, or a negative
+ * EVO_E_* code.  Host-only; no device needed.
+ * Flat order (Linear layers [out][in]):
+ *   W_in[d][A] b_in[d] P_act[H][d] W_obs[d][obs_dim] b_obs[d] P_mem[1+n_obs][d]
+ *   per layer l: ln1_g[d] ln1_b[d] W_qkv[3d][d] b_qkv[3d] W_o[d][d] b_o[d]
+ *                ln2_g ln2_b W_q[d][d] b_q[d] W_kv[2d][d] b_kv[2d] W_o2[d][d] b_o2[d]
+ *                ln3_g ln3_b W_1[d_ff][d] b_1[d_ff] W_2[d][d_ff] b_2[d]
+ *   lnf_g[d] lnf_b[d] W_out[A][d] b_out[A]
+ * Model (pre-norm decoder layers, LayerNorm eps 1e-5, exact-erf GELU):
+ *   memory tokens mem = [sinusoid(k); obs W_obs^T + b_obs] + P_mem, k = T-1-t
+ *   h = x W_in^T + b_in + P_act
+ *   SA  = W_o . causal multi-head attention(LN1(h))     (scale 1/sqrt(d/h))
+ *   CA  = W_o2 . attention(LN2(h) W_q^T, mem W_kv^T)   (unmasked)
+ *   FFN = W_2 . GELU(W_1 . LN3(h) + b_1) + b_2
+ *   eps = LN_f(h) W_out^T + b_out; DDPM step with squared-cosine betas
+ *   (s = 0.008, cap 0.999), fixed-small variance, k-th step adds noise
+ *   unless k == 0. */
+int64_t evo_weight_count(const evo_policy_desc* desc);
+
+/* Validate a descriptor without creating anything (host-only).  Returns
+ * EVO_OK, EVO_E_INVALID or EVO_E_UNSUPPORTED (shape not compiled). */
+int evo_check_desc(const evo_policy_desc* desc);
+
+/* Create a policy on the current HIP device.
+ *   host_weights: host float[n_floats] in the order above, n_floats ==
+ *   evo_weight_count(desc).  Copied and re-laid-out on the device; the call
+ *   returns after the device copies are complete.
+ *   out: receives the policy handle (unchanged on error). */
+int evo_create_policy(const evo_policy_desc* desc, const float* host_weights,
+                      size_t n_floats, evo_policy** out);
+
+/* Register (or replace) schedule `schedule_id` (Eq. 2): host uint8
+ * lattice[rows][n_steps], row-major, entries 0 or 1 (1 = evaluate the unit
+ * and refresh its cache at that step).  rows == L with EVO_GRAN_LAYER (a row
+ * applies to the SA, CA and FFN units of its layer; the three residuals are
+ * then cached as one sum) or 3L with EVO_GRAN_UNIT (row 3l+u, u = 0 SA,
+ * 1 CA, 2 FFN).  n_steps must equal T; row index t is the t-th reverse
+ * step, t = 0 the first (noisiest).  Host-only state; takes effect for
+ * later evo_denoise calls. */
+int evo_set_schedule(evo_policy* p, int32_t schedule_id, const uint8_t* lattice,
+                     int32_t rows, int32_t n_steps, int32_t granularity);
+
+/* Eq. 3 form of evo_set_schedule: K unique (row, step) pairs, host
+ * int32 pairs[K][2].  Duplicates or out-of-range pairs -> EVO_E_INVALID. */
+int evo_set_schedule_pairs(evo_policy* p, int32_t schedule_id, const int32_t* pairs,
+                           int32_t K, int32_t granularity);
+
+/* One action query per sample: run T cached denoising steps for `batch`
+ * independent samples and write the final chunk x_0.
+ *   obs_cond:  device float[batch][n_obs][obs_dim]
+ *   noise:     device float[T][batch][H][A]; slice 0 is x_T, slice t+1 the
+ *              standard-normal noise added after step t
+ *   schedule_ids: host int32[batch] (NULL = all 0); each id must be
+ *              registered.  Samples may carry different schedules.
+ *   actions_out: device float[batch][H][A]
+ *   hip_stream: hipStream_t to enqueue on (NULL = default stream).
+ * Caches are reset for every call.  Asynchronous: returns after enqueueing;
+ * the statistics of the call are available immediately (host computed). */
+int evo_denoise(evo_policy* p, int32_t batch, const float* obs_cond, const float* noise,
+                const int32_t* schedule_ids, float* actions_out, void* hip_stream);
+
+/* Statistics of the last evo_denoise call (host struct). */
+int evo_get_stats(const evo_policy* p, evo_stats* out);
+
+/* Host-only bookkeeping for lattices without a policy: n_lat lattices
+ * (host uint8[n_lat][rows][T]) of one granularity, per-sample ids (host
+ * int32[batch]).  Fills refreshes and the FLOP fields of `out` as
+ * evo_denoise would; byte and tile fields are zero. */
+int evo_schedule_stats(const evo_policy_desc* desc, const uint8_t* lattices, int32_t n_lat,
+                       int32_t rows, int32_t granularity, const int32_t* ids, int32_t batch,
+                       evo_stats* out);
+
+/* Host-only: per-(unit, step) execution codes of one lattice, host
+ * uint8 out[3L][T].  Bit 0: evaluate; bit 1: store the cache after it;
+ * bit 2: add the cached residual; bit 3: layer-merged cache.  For tests. */
+int evo_schedule_codes(const evo_policy_desc* desc, const uint8_t* lattice, int32_t rows,
+                       int32_t granularity, uint8_t* out);
+
+/* Test hook: synchronise the policy's device and copy the cached residual
+ * of `unit` for `sample` of the last evo_denoise into host float[H][d]
+ * (for a layer-granular schedule, unit 3l+2 holds the layer's merged sum). */
+int evo_debug_read_cache(evo_policy* p, int32_t unit, int32_t sample, float* host_dst);
+
+/* Release all device and host resources (NULL is a no-op).  Synchronises
+ * the policy's device first. */
+void evo_destroy_policy(evo_policy* p);
+
+/* Thread-local message of the last failed call on this thread. */
+const char* evo_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* EVO_H */

@@ -1,0 +1,467 @@
+// C ABI of the cached denoising library (see include/evo.h).
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "evo_host.hpp"
+#include "evo_kernels.hpp"
+
+namespace evo {
+const char* last_error();
+}
+
+using namespace evo;
+
+namespace {
+
+// Makes the policy's device current for the duration of a call.
+struct DeviceGuard {
+  int prev = -1, want = -1;
+  explicit DeviceGuard(int dev) : want(dev) {
+    if (hipGetDevice(&prev) != hipSuccess) prev = -1;
+    if (prev != want) (void)hipSetDevice(want);
+  }
+  ~DeviceGuard() {
+    if (prev >= 0 && prev != want) (void)hipSetDevice(prev);
+  }
+};
+
+#define HIP_TRY(expr)                                                                        \
+  do {                                                                                       \
+    hipError_t e_ = (expr);                                                                  \
+    if (e_ != hipSuccess) return fail(EVO_E_HIP, "%s failed: %s", #expr, hipGetErrorString(e_)); \
+  } while (0)
+
+int spt_options(int horizon, int out[2]) {
+  // samples per tile: tiles are whole samples and multiples of 16 rows
+  if (horizon == 8) { out[0] = 2; return 1; }
+  if (horizon == 16) { out[0] = 1; out[1] = 2; return 2; }
+  if (horizon == 32) { out[0] = 1; return 1; }
+  return 0;
+}
+
+int check_supported(const Shape& s) {
+  int opts[2];
+  const int n = spt_options(s.H, opts);
+  bool any = false;
+  for (int i = 0; i < n; ++i) {
+    KernelKey k{s.d, s.dh(), s.H, s.dff, s.dtype, opts[i]};
+    int th;
+    if (!kernel_available(k, &th)) continue;
+    if (s.A > kernel_max_action_dim()) return fail(EVO_E_UNSUPPORTED, "action_dim %d > %d", s.A, kernel_max_action_dim());
+    if (s.n_obs > kernel_max_obs_tokens_for(k))
+      return fail(EVO_E_UNSUPPORTED, "n_obs_tokens %d > %d for this shape", s.n_obs, kernel_max_obs_tokens_for(k));
+    any = true;
+  }
+  if (!any)
+    return fail(EVO_E_UNSUPPORTED,
+                "no kernel compiled for d_model=%d head_dim=%d horizon=%d d_ff=%d dtype=%d "
+                "(compiled: d 64/hd 32/H 8/ff 256, d 256/hd 64/H 16/ff 1024, d 768/hd 64/H 32/ff 3072 bf16)",
+                s.d, s.dh(), s.H, s.dff, s.dtype);
+  return EVO_OK;
+}
+
+}  // namespace
+
+struct evo_policy {
+  Shape s;
+  int device = 0;
+  int n_cu = 256;
+  WeightOffsets wo;
+  std::vector<LayerOff> loff_h;
+  std::vector<PackOff> poff_h;
+  uint64_t pk_obs = 0;
+  int obs_pad = 0;
+  float* d_raw = nullptr;
+  uint4* d_pk = nullptr;
+  LayerOff* d_loff = nullptr;
+  PackOff* d_poff = nullptr;
+  float* d_tkv = nullptr;
+  float* d_ddpm = nullptr;
+  float* d_cache = nullptr;
+  size_t cache_floats = 0;
+  float* d_okv = nullptr;
+  uint8_t* d_plan = nullptr;
+  size_t plan_bytes = 0, tiles_cap = 0, codes_cap = 0;
+  uint8_t* h_stage[2] = {nullptr, nullptr};
+  hipEvent_t ev[2] = {nullptr, nullptr};
+  int stage = 0;
+  std::vector<Schedule> reg;
+  evo_stats last{};
+  bool has_last = false;
+  Plan last_plan;
+  int last_threads = 0;
+};
+
+static void release(evo_policy* p) {
+  if (!p) return;
+  (void)hipDeviceSynchronize();
+  hipFree(p->d_raw);
+  hipFree(p->d_pk);
+  hipFree(p->d_loff);
+  hipFree(p->d_poff);
+  hipFree(p->d_tkv);
+  hipFree(p->d_ddpm);
+  hipFree(p->d_cache);
+  hipFree(p->d_okv);
+  hipFree(p->d_plan);
+  for (int i = 0; i < 2; ++i) {
+    if (p->h_stage[i]) (void)hipHostFree(p->h_stage[i]);
+    if (p->ev[i]) (void)hipEventDestroy(p->ev[i]);
+  }
+  delete p;
+}
+
+extern "C" {
+
+const char* evo_last_error(void) { return evo::last_error(); }
+
+int64_t evo_weight_count(const evo_policy_desc* desc) {
+  Shape s;
+  const int rc = shape_from_desc(desc, &s);
+  if (rc) return rc;
+  return (int64_t)weight_offsets(s).total;
+}
+
+int evo_check_desc(const evo_policy_desc* desc) {
+  Shape s;
+  int rc = shape_from_desc(desc, &s);
+  if (rc) return rc;
+  return check_supported(s);
+}
+
+int evo_create_policy(const evo_policy_desc* desc, const float* host_weights, size_t n_floats, evo_policy** out) {
+  clear_error();
+  Shape s;
+  int rc = shape_from_desc(desc, &s);
+  if (rc) return rc;
+  if ((rc = check_supported(s))) return rc;
+  if (!host_weights) return fail(EVO_E_INVALID, "host_weights is NULL");
+  if (!out) return fail(EVO_E_INVALID, "out is NULL");
+  const WeightOffsets wo = weight_offsets(s);
+  if (n_floats != wo.total)
+    return fail(EVO_E_INVALID, "n_floats is %zu, this shape needs %zu", n_floats, wo.total);
+  if (wo.total >= (1ull << 32)) return fail(EVO_E_UNSUPPORTED, "more than 2^32 parameters");
+
+  evo_policy* p = new (std::nothrow) evo_policy();
+  if (!p) return fail(EVO_E_NOMEM, "host allocation failed");
+  p->s = s;
+  p->wo = wo;
+  if (hipGetDevice(&p->device) != hipSuccess) {
+    delete p;
+    return fail(EVO_E_HIP, "no current HIP device");
+  }
+  hipDeviceProp_t prop;
+  if (hipGetDeviceProperties(&prop, p->device) == hipSuccess) p->n_cu = prop.multiProcessorCount;
+
+#define CREATE_TRY(expr)                                                                        \
+  do {                                                                                          \
+    hipError_t e_ = (expr);                                                                     \
+    if (e_ != hipSuccess) {                                                                     \
+      int code_ = (e_ == hipErrorOutOfMemory) ? EVO_E_NOMEM : EVO_E_HIP;                        \
+      fail(code_, "%s failed: %s", #expr, hipGetErrorString(e_));                               \
+      release(p);                                                                               \
+      return code_;                                                                             \
+    }                                                                                           \
+  } while (0)
+
+  const int L = s.L, d = s.d, T = s.T, U = s.U();
+  const int KF = s.dtype == EVO_BF16 ? 32 : 16;
+  // fp32 parameter copy (biases, norms, embeddings, head, and the source of the packed matrices)
+  CREATE_TRY(hipMalloc(&p->d_raw, wo.total * sizeof(float)));
+  CREATE_TRY(hipMemcpy(p->d_raw, host_weights, wo.total * sizeof(float), hipMemcpyHostToDevice));
+
+  // packed projection matrices
+  auto frag16 = [&](int N, int Kpad) { return (uint64_t)(N / 16) * (Kpad / KF) * 64; };
+  p->obs_pad = (s.obs_dim + 63) / 64 * 64;
+  uint64_t off = 0;
+  p->pk_obs = off;
+  off += frag16(d, p->obs_pad);
+  p->poff_h.resize(L);
+  for (int l = 0; l < L; ++l) {
+    PackOff& po = p->poff_h[l];
+    po.qkv = off; off += frag16(3 * d, d);
+    po.o = off; off += frag16(d, d);
+    po.q = off; off += frag16(d, d);
+    po.kv = off; off += frag16(2 * d, d);
+    po.o2 = off; off += frag16(d, d);
+    po.w1 = off; off += frag16(s.dff, d);
+    po.w2 = off; off += frag16(d, s.dff);
+    po.pad_ = 0;
+  }
+  CREATE_TRY(hipMalloc(&p->d_pk, off * sizeof(uint4)));
+  CREATE_TRY(launch_pack(p->d_raw, wo.W_obs, d, s.obs_dim, p->obs_pad, s.dtype, p->d_pk + p->pk_obs, 0));
+  for (int l = 0; l < L; ++l) {
+    const auto& y = wo.layer[l];
+    const PackOff& po = p->poff_h[l];
+    CREATE_TRY(launch_pack(p->d_raw, y.W_qkv, 3 * d, d, d, s.dtype, p->d_pk + po.qkv, 0));
+    CREATE_TRY(launch_pack(p->d_raw, y.W_o, d, d, d, s.dtype, p->d_pk + po.o, 0));
+    CREATE_TRY(launch_pack(p->d_raw, y.W_q, d, d, d, s.dtype, p->d_pk + po.q, 0));
+    CREATE_TRY(launch_pack(p->d_raw, y.W_kv, 2 * d, d, d, s.dtype, p->d_pk + po.kv, 0));
+    CREATE_TRY(launch_pack(p->d_raw, y.W_o2, d, d, d, s.dtype, p->d_pk + po.o2, 0));
+    CREATE_TRY(launch_pack(p->d_raw, y.W_1, s.dff, d, d, s.dtype, p->d_pk + po.w1, 0));
+    CREATE_TRY(launch_pack(p->d_raw, y.W_2, d, s.dff, s.dff, s.dtype, p->d_pk + po.w2, 0));
+  }
+  // per-layer offsets of the small tensors
+  p->loff_h.resize(L);
+  std::vector<uint32_t> wkv(L), bkv(L);
+  for (int l = 0; l < L; ++l) {
+    const auto& y = wo.layer[l];
+    LayerOff& lo = p->loff_h[l];
+    lo.ln1_g = (uint32_t)y.ln1_g; lo.ln1_b = (uint32_t)y.ln1_b; lo.b_qkv = (uint32_t)y.b_qkv;
+    lo.b_o = (uint32_t)y.b_o; lo.ln2_g = (uint32_t)y.ln2_g; lo.ln2_b = (uint32_t)y.ln2_b;
+    lo.b_q = (uint32_t)y.b_q; lo.b_kv = (uint32_t)y.b_kv; lo.b_o2 = (uint32_t)y.b_o2;
+    lo.ln3_g = (uint32_t)y.ln3_g; lo.ln3_b = (uint32_t)y.ln3_b; lo.b_1 = (uint32_t)y.b_1;
+    lo.b_2 = (uint32_t)y.b_2;
+    lo.pad_[0] = lo.pad_[1] = lo.pad_[2] = 0;
+    wkv[l] = (uint32_t)y.W_kv;
+    bkv[l] = (uint32_t)y.b_kv;
+  }
+  CREATE_TRY(hipMalloc(&p->d_loff, L * sizeof(LayerOff)));
+  CREATE_TRY(hipMemcpy(p->d_loff, p->loff_h.data(), L * sizeof(LayerOff), hipMemcpyHostToDevice));
+  CREATE_TRY(hipMalloc(&p->d_poff, L * sizeof(PackOff)));
+  CREATE_TRY(hipMemcpy(p->d_poff, p->poff_h.data(), L * sizeof(PackOff), hipMemcpyHostToDevice));
+
+  // time-token keys/values for every timestep and layer; sampler constants
+  {
+    uint32_t *d_wkv = nullptr, *d_bkv = nullptr;
+    float* rows = nullptr;
+    CREATE_TRY(hipMalloc(&p->d_tkv, (size_t)T * L * 2 * d * sizeof(float)));
+    CREATE_TRY(hipMalloc(&d_wkv, L * sizeof(uint32_t)));
+    hipError_t e = hipMalloc(&d_bkv, L * sizeof(uint32_t));
+    if (e == hipSuccess) e = hipMalloc(&rows, (size_t)T * d * sizeof(float));
+    if (e == hipSuccess) e = hipMemcpy(d_wkv, wkv.data(), L * sizeof(uint32_t), hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = hipMemcpy(d_bkv, bkv.data(), L * sizeof(uint32_t), hipMemcpyHostToDevice);
+    if (e == hipSuccess)
+      e = launch_time_kv(p->d_raw, (uint32_t)wo.P_mem, d_wkv, d_bkv, T, L, d, s.dtype, rows, p->d_tkv, 0);
+    if (e == hipSuccess) e = hipDeviceSynchronize();
+    hipFree(d_wkv);
+    hipFree(d_bkv);
+    hipFree(rows);
+    CREATE_TRY(e);
+  }
+  CREATE_TRY(hipMalloc(&p->d_ddpm, (size_t)T * 8 * sizeof(float)));
+  CREATE_TRY(launch_ddpm_table(T, p->d_ddpm, 0));
+
+  // caches, observation keys/values, per-call plan buffers
+  {
+    int opts[2];
+    const int n = spt_options(s.H, opts);
+    size_t rows = 0, tiles = 0;
+    int spt_max = 1;
+    for (int i = 0; i < n; ++i) {
+      const size_t t = (size_t)(s.max_batch + opts[i] - 1) / opts[i];
+      rows = std::max(rows, t * opts[i] * s.H);
+      tiles = std::max(tiles, t);
+      spt_max = std::max(spt_max, opts[i]);
+    }
+    p->cache_floats = (size_t)U * rows * d;
+    CREATE_TRY(hipMalloc(&p->d_cache, p->cache_floats * sizeof(float)));
+    CREATE_TRY(hipMalloc(&p->d_okv, (size_t)s.max_batch * L * s.n_obs * 2 * d * sizeof(float)));
+    p->tiles_cap = tiles * spt_max;
+    p->codes_cap = (size_t)std::min(s.max_sched, s.max_batch) * U * T;
+    p->plan_bytes = (2 * p->tiles_cap * sizeof(int32_t) + 255) / 256 * 256 + p->codes_cap;
+    CREATE_TRY(hipMalloc(&p->d_plan, p->plan_bytes));
+    for (int i = 0; i < 2; ++i) {
+      CREATE_TRY(hipHostMalloc((void**)&p->h_stage[i], p->plan_bytes, hipHostMallocDefault));
+      CREATE_TRY(hipEventCreateWithFlags(&p->ev[i], hipEventDisableTiming));
+    }
+  }
+  CREATE_TRY(hipDeviceSynchronize());
+#undef CREATE_TRY
+  p->reg.assign(s.max_sched, Schedule());
+  *out = p;
+  return EVO_OK;
+}
+
+int evo_set_schedule(evo_policy* p, int32_t schedule_id, const uint8_t* lattice, int32_t rows, int32_t n_steps,
+                     int32_t granularity) {
+  clear_error();
+  if (!p) return fail(EVO_E_INVALID, "policy is NULL");
+  if (schedule_id < 0 || schedule_id >= p->s.max_sched)
+    return fail(EVO_E_INVALID, "schedule_id %d outside [0, %d)", schedule_id, p->s.max_sched);
+  if (n_steps != p->s.T) return fail(EVO_E_INVALID, "n_steps is %d, the policy has %d", n_steps, p->s.T);
+  Schedule sc;
+  const int rc = build_schedule(p->s, lattice, rows, granularity, &sc);
+  if (rc) return rc;
+  p->reg[schedule_id] = std::move(sc);
+  return EVO_OK;
+}
+
+int evo_set_schedule_pairs(evo_policy* p, int32_t schedule_id, const int32_t* pairs, int32_t K,
+                           int32_t granularity) {
+  clear_error();
+  if (!p) return fail(EVO_E_INVALID, "policy is NULL");
+  if (K < 0 || (K > 0 && !pairs)) return fail(EVO_E_INVALID, "bad pairs / K");
+  if (granularity != EVO_GRAN_LAYER && granularity != EVO_GRAN_UNIT)
+    return fail(EVO_E_INVALID, "bad granularity");
+  const int rows = granularity == EVO_GRAN_LAYER ? p->s.L : p->s.U();
+  const int T = p->s.T;
+  std::vector<uint8_t> lat((size_t)rows * T, 0);
+  for (int i = 0; i < K; ++i) {
+    const int b = pairs[2 * i], t = pairs[2 * i + 1];
+    if (b < 0 || b >= rows || t < 0 || t >= T) return fail(EVO_E_INVALID, "pair %d = (%d, %d) out of range", i, b, t);
+    if (lat[(size_t)b * T + t]) return fail(EVO_E_INVALID, "pair %d = (%d, %d) is a duplicate", i, b, t);
+    lat[(size_t)b * T + t] = 1;
+  }
+  return evo_set_schedule(p, schedule_id, lat.data(), rows, T, granularity);
+}
+
+int evo_denoise(evo_policy* p, int32_t batch, const float* obs_cond, const float* noise, const int32_t* schedule_ids,
+                float* actions_out, void* hip_stream) {
+  clear_error();
+  if (!p) return fail(EVO_E_INVALID, "policy is NULL");
+  const Shape& s = p->s;
+  if (batch < 1 || batch > s.max_batch) return fail(EVO_E_INVALID, "batch %d outside [1, %d]", batch, s.max_batch);
+  if (!obs_cond || !noise || !actions_out) return fail(EVO_E_INVALID, "NULL device pointer");
+  for (int n = 0; n < batch; ++n) {
+    const int id = schedule_ids ? schedule_ids[n] : 0;
+    if (id < 0 || id >= s.max_sched) return fail(EVO_E_INVALID, "schedule id %d of sample %d out of range", id, n);
+    if (!p->reg[id].valid) return fail(EVO_E_STATE, "schedule id %d of sample %d is not registered", id, n);
+  }
+  DeviceGuard guard(p->device);
+  hipStream_t stream = (hipStream_t)hip_stream;
+  // samples per tile: two when a single-sample tiling would oversubscribe the CUs
+  int opts[2];
+  const int nopt = spt_options(s.H, opts);
+  int spt = 0, threads = 0;
+  for (int i = 0; i < nopt; ++i) {
+    KernelKey k{s.d, s.dh(), s.H, s.dff, s.dtype, opts[i]};
+    int th;
+    if (!kernel_available(k, &th)) continue;
+    if (spt == 0 || (opts[i] > spt && batch > p->n_cu)) {
+      spt = opts[i];
+      threads = th;
+    }
+  }
+  if (!spt) return fail(EVO_E_UNSUPPORTED, "no kernel for this shape");
+  Plan plan;
+  int rc = build_plan(s, p->reg, schedule_ids, batch, spt, 8, &plan);
+  if (rc) return rc;
+  const size_t ntile_ent = (size_t)plan.n_tiles * spt;
+  const size_t codes_off = (2 * p->tiles_cap * sizeof(int32_t) + 255) / 256 * 256;
+  const size_t ucodes = (size_t)s.U() * s.T;
+  if (ntile_ent > p->tiles_cap || plan.used.size() * ucodes > p->codes_cap)
+    return fail(EVO_E_STATE, "plan exceeds the policy's buffers");
+  // stage the plan in pinned memory; the buffer is reused only after its
+  // previous copy has completed
+  const int st = p->stage;
+  if (hipEventSynchronize(p->ev[st]) != hipSuccess) return fail(EVO_E_HIP, "event synchronize failed");
+  uint8_t* hs = p->h_stage[st];
+  int32_t* ts = reinterpret_cast<int32_t*>(hs);
+  int32_t* tl = ts + p->tiles_cap;
+  std::memcpy(ts, plan.tile_sample.data(), ntile_ent * sizeof(int32_t));
+  std::memcpy(tl, plan.tile_slot.data(), ntile_ent * sizeof(int32_t));
+  for (size_t i = 0; i < plan.used.size(); ++i)
+    std::memcpy(hs + codes_off + i * ucodes, p->reg[plan.used[i]].codes.data(), ucodes);
+  const size_t nbytes = codes_off + plan.used.size() * ucodes;
+  HIP_TRY(hipMemcpyAsync(p->d_plan, hs, nbytes, hipMemcpyHostToDevice, stream));
+  HIP_TRY(hipEventRecord(p->ev[st], stream));
+  p->stage ^= 1;
+
+  KParams kp;
+  std::memset(&kp, 0, sizeof(kp));
+  kp.L = s.L; kp.A = s.A; kp.n_obs = s.n_obs; kp.obs_dim = s.obs_dim; kp.obs_pad = p->obs_pad;
+  kp.T = s.T; kp.clip = s.clip; kp.n_tiles = plan.n_tiles;
+  kp.raw = p->d_raw; kp.pk = p->d_pk; kp.loff = p->d_loff; kp.poff = p->d_poff; kp.pk_obs = p->pk_obs;
+  const WeightOffsets& wo = p->wo;
+  kp.W_in = (uint32_t)wo.W_in; kp.b_in = (uint32_t)wo.b_in; kp.P_act = (uint32_t)wo.P_act;
+  kp.b_obs = (uint32_t)wo.b_obs; kp.P_mem = (uint32_t)wo.P_mem; kp.lnf_g = (uint32_t)wo.lnf_g;
+  kp.lnf_b = (uint32_t)wo.lnf_b; kp.W_out = (uint32_t)wo.W_out; kp.b_out = (uint32_t)wo.b_out;
+  kp.tkv = p->d_tkv; kp.ddpm = p->d_ddpm;
+  kp.tile_sample = reinterpret_cast<const int32_t*>(p->d_plan);
+  kp.tile_slot = reinterpret_cast<const int32_t*>(p->d_plan) + p->tiles_cap;
+  kp.codes = p->d_plan + codes_off;
+  kp.obs = obs_cond; kp.noise = noise; kp.out = actions_out; kp.okv = p->d_okv; kp.cache = p->d_cache;
+  kp.batch = batch;
+  KernelKey key{s.d, s.dh(), s.H, s.dff, s.dtype, spt};
+  HIP_TRY(launch_denoise(key, kp, stream));
+
+  call_stats(s, p->reg, schedule_ids, batch, &plan, &p->last);
+  p->has_last = true;
+  p->last_plan = std::move(plan);
+  p->last_threads = threads;
+  return EVO_OK;
+}
+
+int evo_get_stats(const evo_policy* p, evo_stats* out) {
+  clear_error();
+  if (!p || !out) return fail(EVO_E_INVALID, "NULL argument");
+  if (!p->has_last) return fail(EVO_E_STATE, "no evo_denoise call yet");
+  *out = p->last;
+  return EVO_OK;
+}
+
+int evo_schedule_stats(const evo_policy_desc* desc, const uint8_t* lattices, int32_t n_lat, int32_t rows,
+                       int32_t granularity, const int32_t* ids, int32_t batch, evo_stats* out) {
+  clear_error();
+  Shape s;
+  int rc = shape_from_desc(desc, &s);
+  if (rc) return rc;
+  if (!lattices || !out || n_lat < 1 || batch < 1) return fail(EVO_E_INVALID, "bad arguments");
+  std::vector<Schedule> reg(n_lat);
+  for (int i = 0; i < n_lat; ++i) {
+    rc = build_schedule(s, lattices + (size_t)i * rows * s.T, rows, granularity, &reg[i]);
+    if (rc) return rc;
+  }
+  for (int n = 0; n < batch; ++n) {
+    const int id = ids ? ids[n] : 0;
+    if (id < 0 || id >= n_lat) return fail(EVO_E_INVALID, "id %d of sample %d out of range", id, n);
+  }
+  call_stats(s, reg, ids, batch, nullptr, out);
+  return EVO_OK;
+}
+
+int evo_schedule_codes(const evo_policy_desc* desc, const uint8_t* lattice, int32_t rows, int32_t granularity,
+                       uint8_t* out) {
+  clear_error();
+  Shape s;
+  int rc = shape_from_desc(desc, &s);
+  if (rc) return rc;
+  if (!out) return fail(EVO_E_INVALID, "out is NULL");
+  Schedule sc;
+  rc = build_schedule(s, lattice, rows, granularity, &sc);
+  if (rc) return rc;
+  std::memcpy(out, sc.codes.data(), sc.codes.size());
+  return EVO_OK;
+}
+
+int evo_debug_read_cache(evo_policy* p, int32_t unit, int32_t sample, float* host_dst) {
+  clear_error();
+  if (!p || !host_dst) return fail(EVO_E_INVALID, "NULL argument");
+  if (!p->has_last) return fail(EVO_E_STATE, "no evo_denoise call yet");
+  const Shape& s = p->s;
+  if (unit < 0 || unit >= s.U()) return fail(EVO_E_INVALID, "unit out of range");
+  const Plan& pl = p->last_plan;
+  int tile = -1, slot = -1;
+  for (int q = 0; q < pl.n_tiles && tile < 0; ++q)
+    for (int j = 0; j < pl.spt; ++j)
+      if (pl.tile_sample[(size_t)q * pl.spt + j] == sample) { tile = q; slot = j; }
+  if (tile < 0) return fail(EVO_E_INVALID, "sample %d not in the last call", sample);
+  DeviceGuard guard(p->device);
+  HIP_TRY(hipDeviceSynchronize());
+  const int R = pl.spt * s.H, d = s.d, NW = p->last_threads / 64, RB = R / 16, CBW = d / 16 / NW;
+  std::vector<float> buf((size_t)R * d);
+  HIP_TRY(hipMemcpy(buf.data(), p->d_cache + ((size_t)tile * s.U() + unit) * R * d, buf.size() * sizeof(float),
+                    hipMemcpyDeviceToHost));
+  for (int i = 0; i < s.H; ++i) {
+    const int row = slot * s.H + i, rb = row / 16, rr = row % 16;
+    for (int col = 0; col < d; ++col) {
+      const int cbk = col / 16, w = cbk / CBW, c = cbk % CBW;
+      const int lane = (col % 16) + 16 * (rr / 4);
+      host_dst[(size_t)i * d + col] = buf[((size_t)((w * RB + rb) * CBW + c) * 64 + lane) * 4 + rr % 4];
+    }
+  }
+  return EVO_OK;
+}
+
+void evo_destroy_policy(evo_policy* p) {
+  if (!p) return;
+  DeviceGuard guard(p->device);
+  release(p);
+}
+
+}  // extern "C"

@@ -1,0 +1,103 @@
+// Host-side runtime of the cached denoising library: descriptor checks,
+// weight offsets, schedule execution codes, batch plans and integer
+// bookkeeping.  Pure C++ (no HIP), so every decision made here can be tested
+// on a machine without a GPU.
+#pragma once
+
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "../../include/evo.h"
+
+namespace evo {
+
+// thread-local error message of the last failed ABI call
+int fail(int code, const char* fmt, ...);
+void clear_error();
+
+// Execution code of one (unit, step) position for one schedule.
+enum : uint8_t {
+  CODE_EVAL = 1,    // evaluate the residual branch (Eq. 1, (b,t) in S')
+  CODE_STORE = 2,   // store the cache after evaluating (it is read later)
+  CODE_REUSE = 4,   // add the cached residual (Eq. 1, (b,t) not in S')
+  CODE_MERGED = 8,  // layer-merged caches: SA+CA+FFN residuals cached as one sum
+};
+
+enum { UNIT_SA = 0, UNIT_CA = 1, UNIT_FFN = 2 };
+
+struct Shape {
+  int L = 0, d = 0, nh = 0, dff = 0, H = 0, A = 0, n_obs = 0, obs_dim = 0, T = 0;
+  int dtype = EVO_BF16, cold = EVO_COLD_COMPUTE, clip = 1;
+  int max_batch = 0, max_sched = 0;
+  int U() const { return 3 * L; }
+  int dh() const { return d / nh; }
+  int S() const { return 1 + n_obs; }
+  int elt() const { return dtype == EVO_BF16 ? 2 : 4; }
+};
+
+// Validates field ranges; does not check compiled-shape support.
+int shape_from_desc(const evo_policy_desc* desc, Shape* out);
+
+// Offsets (in floats) of every tensor of the flat weight vector.
+struct WeightOffsets {
+  size_t W_in, b_in, P_act, W_obs, b_obs, P_mem;
+  struct Layer {
+    size_t ln1_g, ln1_b, W_qkv, b_qkv, W_o, b_o;
+    size_t ln2_g, ln2_b, W_q, b_q, W_kv, b_kv, W_o2, b_o2;
+    size_t ln3_g, ln3_b, W_1, b_1, W_2, b_2;
+  };
+  std::vector<Layer> layer;
+  size_t lnf_g, lnf_b, W_out, b_out;
+  size_t total;
+};
+WeightOffsets weight_offsets(const Shape& s);
+
+// Integer FLOP constants (2 per multiply-add) per sample.
+struct Flops {
+  uint64_t unit[3];          // convention of Tables 1-3 (CA includes memory K/V)
+  uint64_t unit_kernel[3];   // this implementation (CA memory K/V hoisted)
+  uint64_t always_step;      // embedding + head
+  uint64_t always_query;     // observation projection
+  uint64_t query_kernel;     // observation projection + observation-token K/V, all layers
+};
+Flops flops_of(const Shape& s);
+
+// Weight bytes an evaluation of each unit type streams (bf16 or fp32).
+void unit_weight_bytes(const Shape& s, uint64_t out[3]);
+
+struct Schedule {
+  bool valid = false;
+  bool merged = false;
+  std::vector<uint8_t> codes;   // [U][T]
+  uint64_t requested = 0;       // unit positions in S
+  uint64_t effective = 0;       // unit positions in S'
+  uint64_t flops = 0;           // Tables 1-3 convention, per sample
+  uint64_t flops_kernel = 0;    // this implementation, per sample (without per-query work)
+  uint64_t reuse_count = 0;     // positions with CODE_REUSE
+  uint64_t store_count = 0;     // positions with CODE_STORE
+  std::vector<uint64_t> eval_mask;  // [T] bitmask of evaluated units (U <= 64)
+};
+
+// Build execution codes from a lattice (rows = L or 3L, row-major [rows][T]).
+int build_schedule(const Shape& s, const uint8_t* lattice, int rows, int granularity,
+                   Schedule* out);
+
+// Per-call plan: samples grouped into tiles of `spt` samples sharing a
+// schedule where possible, tiles ordered so that consecutive tiles of the
+// sorted order land on the same XCD (workgroup i runs on XCD i % 8).
+struct Plan {
+  int spt = 1;
+  int n_tiles = 0;
+  std::vector<int32_t> tile_sample;   // [n_tiles][spt], -1 = empty slot
+  std::vector<int32_t> tile_slot;     // [n_tiles][spt], index into `used`
+  std::vector<int32_t> used;          // schedule ids referenced by the call
+};
+int build_plan(const Shape& s, const std::vector<Schedule>& reg, const int32_t* ids, int batch,
+               int spt, int n_xcd, Plan* out);
+
+// Bookkeeping of a call (refreshes, FLOPs, algorithmic bytes).
+void call_stats(const Shape& s, const std::vector<Schedule>& reg, const int32_t* ids, int batch,
+                const Plan* plan, evo_stats* out);
+
+}  // namespace evo

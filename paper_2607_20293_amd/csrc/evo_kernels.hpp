@@ -1,0 +1,64 @@
+// Device-side interface shared by the kernels and the ABI layer.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <cstdint>
+
+namespace evo {
+
+// Float offsets (into the fp32 parameter copy) of one layer's small tensors.
+struct LayerOff {
+  uint32_t ln1_g, ln1_b, b_qkv, b_o, ln2_g, ln2_b, b_q, b_kv, b_o2, ln3_g, ln3_b, b_1, b_2;
+  uint32_t pad_[3];
+};
+
+// Offsets (in 16-byte units) of one layer's packed matrices.
+struct PackOff {
+  uint64_t qkv, o, q, kv, o2, w1, w2, pad_;
+};
+
+struct KParams {
+  int L, A, n_obs, obs_dim, obs_pad, T, clip, n_tiles;
+  const float* raw;          // fp32 parameters (flat order of evo.h)
+  const uint4* pk;           // packed projection matrices
+  const LayerOff* loff;      // [L]
+  const PackOff* poff;       // [L]
+  uint64_t pk_obs;           // fragment offset of W_obs (K padded to obs_pad)
+  uint32_t W_in, b_in, P_act, b_obs, P_mem, lnf_g, lnf_b, W_out, b_out, pad_;
+  const float* tkv;          // [T][L][2d] time-token keys/values, indexed by timestep k
+  const float* ddpm;         // [T][8] sampler constants, indexed by timestep k
+  const int32_t* tile_sample;  // [n_tiles][spt] sample index or -1
+  const int32_t* tile_slot;    // [n_tiles][spt] schedule slot
+  const uint8_t* codes;        // [slots][3L][T]
+  const float* obs;          // [batch][n_obs][obs_dim]
+  const float* noise;        // [T][batch][H][A]
+  float* out;                // [batch][H][A]
+  float* okv;                // [batch][L][n_obs][2d] observation-token keys/values
+  float* cache;              // [n_tiles][3L][rows*d] per-tile residual caches
+  int batch, pad2_;
+};
+
+// Shape key of a compiled kernel instantiation.
+struct KernelKey {
+  int d, dh, horizon, d_ff, dtype, spt;
+};
+
+// Returns true and the workgroup size if `key` is compiled.
+bool kernel_available(const KernelKey& key, int* threads);
+// Largest supported action_dim (all shapes) and n_obs_tokens (per shape).
+int kernel_max_action_dim();
+int kernel_max_obs_tokens_for(const KernelKey& key);
+// Launch the denoising kernel: one workgroup per tile.
+hipError_t launch_denoise(const KernelKey& key, const KParams& p, hipStream_t stream);
+
+// Creation-time kernels.
+hipError_t launch_pack(const float* raw, size_t off, int N, int K, int Kpad, int dtype,
+                       uint4* dst, hipStream_t stream);
+// Time-token keys/values tkv[T][L][2d]; wkv/bkv: device arrays of the
+// layers' W_kv / b_kv float offsets; rows_scratch: device float[T][d].
+hipError_t launch_time_kv(const float* raw, uint32_t pmem0, const uint32_t* wkv, const uint32_t* bkv,
+                          int T, int L, int D, int dtype, float* rows_scratch, float* tkv,
+                          hipStream_t stream);
+hipError_t launch_ddpm_table(int T, float* table, hipStream_t stream);
+
+}  // namespace evo

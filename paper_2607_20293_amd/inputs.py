@@ -140,20 +140,24 @@ def make_weights(s: PolicyShape, seed: int = 0, variant: str = "default",
     activations, stronger attention contrast).
     """
     rng = np.random.default_rng([seed, 0])
-    parts = []
-    mstd = std * (5.0 if variant == "wide" else 1.0)
+    out = np.empty(n_weight_floats(s), np.float32)
+    mstd = np.float32(std * (5.0 if variant == "wide" else 1.0))
+    off = 0
     for _, shp, kind in weight_layout(s):
         n = int(np.prod(shp))
+        v = out[off:off + n]
+        off += n
         if kind == "mat":
-            v = rng.standard_normal(n, dtype=np.float32) * np.float32(mstd)
+            rng.standard_normal(out=v, dtype=np.float32)
+            v *= mstd
         elif variant == "default":
-            v = np.ones(n, np.float32) if kind == "ln_g" else np.zeros(n, np.float32)
+            v[:] = 1.0 if kind == "ln_g" else 0.0
         else:
-            v = rng.standard_normal(n, dtype=np.float32) * np.float32(std)
+            rng.standard_normal(out=v, dtype=np.float32)
+            v *= np.float32(std)
             if kind == "ln_g":
-                v = v + np.float32(1.0)
-        parts.append(v.astype(np.float32))
-    return np.concatenate(parts).astype(np.float32)
+                v += np.float32(1.0)
+    return out
 
 
 def split_weights(s: PolicyShape, flat: np.ndarray) -> Dict[str, np.ndarray]:

@@ -1,0 +1,292 @@
+"""GPU parity: the HIP path (through the C ABI) against the fp64 oracle on
+the same seeded inputs, plus the invariants of the cached loop that hold on
+the device (determinism, per-query reset, sample independence, cache
+contents).  Bars: fp32 max-abs <= 1e-4; bf16 normwise relative <= 3e-2;
+bookkeeping bit-exact."""
+import numpy as np
+import pytest
+
+from oracle import evo_oracle as O
+from paper_2607_20293_amd import evo
+from paper_2607_20293_amd import inputs as I
+from tests.conftest import printed_unit_lattice
+from tests.gpu_util import check_stats, compare, device, run_gpu, run_oracle, say
+
+pytestmark = pytest.mark.gpu
+
+
+def _policy(shape, weights, dtype, max_batch, max_sched, cold=O.COLD_COMPUTE, clip=True):
+    device()
+    return evo.Policy(shape, weights, dtype=dtype, max_batch=max_batch, max_schedules=max_sched,
+                      cold_policy=cold, clip=clip)
+
+
+def _case(name, shape, weights, obs, noise, lattices, ids, dtype, gran=O.GRAN_LAYER,
+          cold=O.COLD_COMPUTE, samples=None, max_batch=None, clip=True):
+    say(f"[gpu] {name}: dtype={dtype} batch={obs.shape[0]} schedules={len(lattices)} gran={gran} cold={cold}")
+    B = obs.shape[0]
+    pol = _policy(shape, weights, dtype, max_batch or B, len(lattices), cold, clip)
+    for j, lt in enumerate(lattices):
+        pol.set_schedule(j, lt, gran)
+    got, gst = run_gpu(pol, obs, noise, ids)
+    ref, ost = run_oracle(shape, weights, obs, noise, lattices, ids, gran, cold, dtype, samples, clip)
+    sel = got if samples is None else got[list(samples)]
+    err = compare(sel, ref, dtype, name)
+    check_stats(gst, ost)
+    return pol, got, gst, err
+
+
+# ---------------------------------------------------------------- workloads
+def test_tiny_fp32_b1_config():
+    w = I.WORKLOADS["tiny_fp32_b1"]
+    inp = I.make_inputs(w)
+    pol, *_ = _case("tiny_fp32_b1", w.shape, inp.weights, inp.obs, inp.noise, inp.lattices, inp.ids, "fp32")
+    pol.close()
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_tiny_perturbed_ragged_mixed(dtype):
+    """batch 5 (two samples per tile -> a half-empty last tile), three
+    schedules mixed within tiles, non-zero biases and LN affine."""
+    s = I.TINY
+    wts = I.make_weights(s, 1, "perturbed")
+    obs, noise = I.make_obs(s, 5, 1), I.make_noise(s, 5, 1)
+    rng = np.random.default_rng([1, 3])
+    lats = [I.lattice_bernoulli(2, 10, p, rng) for p in (0.2, 0.5, 0.9)]
+    ids = np.array([2, 0, 1, 0, 2], np.int32)
+    pol, *_ = _case(f"tiny_{dtype}_mixed", s, wts, obs, noise, lats, ids, dtype)
+    pol.close()
+
+
+def test_tiny_wide_weights_fp32():
+    """Larger weights: sharper attention and larger residuals."""
+    s = I.TINY
+    wts = I.make_weights(s, 2, "wide")
+    obs, noise = I.make_obs(s, 2, 2), I.make_noise(s, 2, 2)
+    lats = [I.lattice_bernoulli(2, 10, 0.5, np.random.default_rng(5))]
+    pol, *_ = _case("tiny_wide", s, wts, obs, noise, lats, np.zeros(2, np.int32), "fp32")
+    pol.close()
+
+
+@pytest.mark.parametrize("name", ["pusht_fp32_b1_d25", "pusht_fp32_b1_all", "pusht_bf16_b1_d25",
+                                  "pusht_bf16_b1_all"])
+def test_pusht_b1(name):
+    w = I.WORKLOADS[name]
+    inp = I.make_inputs(w)
+    pol, *_ = _case(name, w.shape, inp.weights, inp.obs, inp.noise, inp.lattices, inp.ids, w.dtype)
+    pol.close()
+
+
+@pytest.mark.parametrize("name", ["pusht_fp32_b64_d25", "pusht_bf16_b64_d25", "pusht_bf16_b64_all"])
+def test_pusht_b64_sampled(name):
+    w = I.WORKLOADS[name]
+    inp = I.make_inputs(w)
+    samples = [0, 1, 17, 42, 63]
+    pol, *_ = _case(name, w.shape, inp.weights, inp.obs, inp.noise, inp.lattices, inp.ids, w.dtype,
+                    samples=samples)
+    pol.close()
+
+
+def test_image_b256_sampled():
+    w = I.WORKLOADS["image_bf16_b256_d12"]
+    inp = I.make_inputs(w)
+    pol, *_ = _case("image_bf16_b256_d12", w.shape, inp.weights, inp.obs, inp.noise, inp.lattices, inp.ids,
+                    "bf16", samples=[0, 5, 128, 255])
+    pol.close()
+
+
+@pytest.mark.parametrize("name,samples", [("bimanual_bf16_b128_d20", [0, 127]),
+                                          ("bimanual_bf16_b128_all", [64])])
+def test_bimanual_b128_sampled(name, samples):
+    w = I.WORKLOADS[name]
+    inp = I.make_inputs(w)
+    pol, *_ = _case(name, w.shape, inp.weights, inp.obs, inp.noise, inp.lattices, inp.ids, "bf16",
+                    samples=samples)
+    pol.close()
+
+
+def test_population_b512_sampled():
+    """512 samples, 64 schedules (10-40% density), per-sample ids: two
+    samples per workgroup tile."""
+    w = I.WORKLOADS["population_bf16_b512"]
+    inp = I.make_inputs(w)
+    ids = inp.ids
+    samples = [0, 1, 2, 100, 255, 256, 300, 511]
+    pol, got, gst, _ = _case("population_bf16_b512", w.shape, inp.weights, inp.obs, inp.noise, inp.lattices,
+                             ids, "bf16", samples=samples)
+    assert gst["n_tiles"] == 256
+    pol.close()
+
+
+# ---------------------------------------------------------------- invariants
+def test_determinism_reset_and_independence():
+    """Same inputs -> bitwise-same chunk; a call in between does not leak
+    (caches are reset per query); a sample's chunk does not depend on the
+    other samples of the batch or on its tile position."""
+    w = I.WORKLOADS["pusht_bf16_b64_d25"]
+    s = w.shape
+    inp = I.make_inputs(w)
+    lats = I.population_lattices(s.n_layers, s.n_steps, 4, 0)
+    ids = np.arange(64, dtype=np.int32) % 4
+    say("[gpu] determinism/reset/independence pusht bf16 b64")
+    pol = _policy(s, inp.weights, "bf16", 64, 4)
+    for j, lt in enumerate(lats):
+        pol.set_schedule(j, lt, O.GRAN_LAYER)
+    a1, _ = run_gpu(pol, inp.obs, inp.noise, ids)
+    obs2, noise2 = I.make_obs(s, 64, 9), I.make_noise(s, 64, 9)
+    run_gpu(pol, obs2, noise2, ids[::-1].copy())
+    a2, _ = run_gpu(pol, inp.obs, inp.noise, ids)
+    assert np.array_equal(a1, a2)
+    for n in (0, 13, 63):
+        one, _ = run_gpu(pol, inp.obs[n:n + 1], inp.noise[:, n:n + 1], ids[n:n + 1])
+        assert np.array_equal(one[0], a1[n]), n
+    pol.close()
+
+
+def test_two_sample_tiles_match_single_sample_tiles():
+    """Population-sized batches use two samples per workgroup; the chunk of a
+    sample matches its single-sample-tile result."""
+    w = I.WORKLOADS["population_bf16_b512"]
+    s = w.shape
+    inp = I.make_inputs(w)
+    say("[gpu] two-sample tiles vs single-sample tiles")
+    pol = _policy(s, inp.weights, "bf16", 512, 64)
+    for j, lt in enumerate(inp.lattices):
+        pol.set_schedule(j, lt, O.GRAN_LAYER)
+    big, st = run_gpu(pol, inp.obs, inp.noise, inp.ids)
+    assert st["n_tiles"] == 256
+    for n in (3, 77, 400):
+        one, st1 = run_gpu(pol, inp.obs[n:n + 1], inp.noise[:, n:n + 1], inp.ids[n:n + 1])
+        assert st1["n_tiles"] == 1
+        np.testing.assert_allclose(one[0], big[n], rtol=0, atol=1e-5)
+    pol.close()
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_step0_only_cache_holds_step0_residuals(dtype):
+    """Only step 0 refreshed (unit-granular): after the query every unit's
+    cache holds r_{b,0}; the chunk matches the oracle."""
+    s = I.PUSHT
+    wts = I.make_weights(s, 3, "perturbed")
+    obs, noise = I.make_obs(s, 1, 3), I.make_noise(s, 1, 3)
+    lat = np.zeros((3 * s.n_layers, s.n_steps), np.uint8)
+    lat[:, 0] = 1
+    pol, got, gst, _ = _case(f"step0_only_{dtype}", s, wts, obs, noise, [lat], np.zeros(1, np.int32), dtype,
+                             gran=O.GRAN_UNIT)
+    P = O.prepare_params(I.split_weights(s, wts), dtype)
+    eff = O.effective_lattice(O.expand_lattice(lat, O.GRAN_UNIT, s.n_layers), O.COLD_COMPUTE)
+    tr = {}
+    O.denoise_group(s, P, obs, noise, eff, trace=tr)
+    worst = 0.0
+    for b in range(3 * s.n_layers):
+        c = pol.read_cache(b, 0).astype(np.float64)
+        r0 = tr["r"][0, b, 0]
+        e = float(np.max(np.abs(c - r0)))
+        scale = max(float(np.max(np.abs(r0))), 1e-6)
+        worst = max(worst, e / scale)
+        assert (e <= 1e-4) if dtype == "fp32" else (e / scale <= 3e-2), (b, e)
+    say(f"  cache readback worst relative error {worst:.2e}")
+    assert gst["cache_bytes_written"] == 3 * s.n_layers * s.horizon * s.d_model * 4
+    pol.close()
+
+
+@pytest.mark.parametrize("cold", [O.COLD_COMPUTE, O.COLD_ZERO])
+def test_printed_schedules(cold):
+    """The paper's printed 24 x 100 unit schedules (three tasks, BAC and
+    EVO; most EVO rows skip step 0) on the 8-layer policy."""
+    s = I.PUSHT
+    wts = I.make_weights(s, 4, "perturbed")
+    lats = [printed_unit_lattice(tag, m) for tag in ("pusht", "kitchen", "lift_ph") for m in ("BAC", "EVO")]
+    B = len(lats)
+    obs, noise = I.make_obs(s, B, 4), I.make_noise(s, B, 4)
+    ids = np.arange(B, dtype=np.int32)
+    for dtype in ("fp32", "bf16"):
+        pol, *_ = _case(f"printed_{dtype}_cold{cold}", s, wts, obs, noise, lats, ids, dtype, gran=O.GRAN_UNIT,
+                        cold=cold)
+        pol.close()
+
+
+def test_hand_lattice_most_recent_unit():
+    """One unit refreshed at steps {0, 2, 6} only, every other unit always."""
+    s = I.TINY
+    wts = I.make_weights(s, 6, "perturbed")
+    obs, noise = I.make_obs(s, 2, 6), I.make_noise(s, 2, 6)
+    lat = np.ones((6, 10), np.uint8)
+    lat[4] = 0
+    lat[4, [0, 2, 6]] = 1
+    pol, *_ = _case("hand_lattice", s, wts, obs, noise, [lat], np.zeros(2, np.int32), "fp32", gran=O.GRAN_UNIT)
+    pol.close()
+
+
+def test_cold_zero_without_step0():
+    s = I.TINY
+    wts = I.make_weights(s, 7, "perturbed")
+    obs, noise = I.make_obs(s, 2, 7), I.make_noise(s, 2, 7)
+    lat = (np.random.default_rng(7).random((6, 10)) < 0.4).astype(np.uint8)
+    lat[:, 0] = 0
+    pol, *_ = _case("cold_zero", s, wts, obs, noise, [lat], np.zeros(2, np.int32), "fp32", gran=O.GRAN_UNIT,
+                    cold=O.COLD_ZERO)
+    pol.close()
+
+
+def test_no_clip_fp32():
+    s = I.TINY
+    wts = I.make_weights(s, 8, "perturbed")
+    obs, noise = I.make_obs(s, 2, 8), I.make_noise(s, 2, 8)
+    lats = [I.lattice_bernoulli(2, 10, 0.5, np.random.default_rng(8))]
+    say("[gpu] no clip fp32")
+    pol = _policy(s, wts, "fp32", 2, 1, clip=False)
+    pol.set_schedule(0, lats[0], O.GRAN_LAYER)
+    got, _ = run_gpu(pol, obs, noise, np.zeros(2, np.int32))
+    ref, _ = run_oracle(s, wts, obs, noise, lats, np.zeros(2, np.int32), O.GRAN_LAYER, O.COLD_COMPUTE, "fp32",
+                        clip=False)
+    rel = float(np.max(np.abs(got - ref)) / np.max(np.abs(ref)))
+    say(f"  no-clip relative error {rel:.2e}")
+    assert rel <= 1e-5
+    pol.close()
+
+
+def test_pairs_entry_point_equals_lattice():
+    s = I.TINY
+    wts = I.make_weights(s, 9, "perturbed")
+    obs, noise = I.make_obs(s, 1, 9), I.make_noise(s, 1, 9)
+    lat = I.lattice_bernoulli(6, 10, 0.4, np.random.default_rng(9))
+    say("[gpu] pairs entry point")
+    pol = _policy(s, wts, "fp32", 1, 2)
+    pol.set_schedule(0, lat, O.GRAN_UNIT)
+    pol.set_schedule_pairs(1, np.argwhere(lat > 0), O.GRAN_UNIT)
+    a, _ = run_gpu(pol, obs, noise, np.array([0], np.int32))
+    b, _ = run_gpu(pol, obs, noise, np.array([1], np.int32))
+    assert np.array_equal(a, b)
+    with pytest.raises(evo.EvoError):
+        pol.set_schedule_pairs(1, [[0, 0], [0, 0]], O.GRAN_UNIT)
+    pol.close()
+
+
+def test_errors_leave_policy_usable():
+    import torch
+    s = I.TINY
+    wts = I.make_weights(s, 0)
+    say("[gpu] error paths")
+    pol = _policy(s, wts, "fp32", 2, 2)
+    pol.set_schedule(0, np.ones((2, 10), np.uint8), O.GRAN_LAYER)
+    dev = device()
+    obs = torch.zeros((2, s.n_obs, s.obs_dim), device=dev)
+    noise = torch.zeros((s.n_steps, 2, s.horizon, s.action_dim), device=dev)
+    with pytest.raises(evo.EvoError) as e:
+        pol.denoise(obs, noise, np.array([0, 1], np.int32))      # schedule 1 not registered
+    assert e.value.code == -2
+    with pytest.raises(evo.EvoError) as e:
+        pol.denoise(obs, noise, np.array([0, 5], np.int32))      # id out of range
+    assert e.value.code == -1
+    big_obs = torch.zeros((3, s.n_obs, s.obs_dim), device=dev)
+    big_noise = torch.zeros((s.n_steps, 3, s.horizon, s.action_dim), device=dev)
+    with pytest.raises(evo.EvoError) as e:
+        pol.denoise(big_obs, big_noise, None)                    # batch > max_batch
+    assert e.value.code == -1
+    with pytest.raises(evo.EvoError):
+        pol.set_schedule(0, np.ones((2, 9), np.uint8), O.GRAN_LAYER)
+    out = pol.denoise(obs, noise, None)
+    torch.cuda.synchronize()
+    assert torch.isfinite(out).all()
+    pol.close()

@@ -1,0 +1,137 @@
+"""CPU tests of the C-ABI library: it loads, exports every declared symbol,
+and its host-side decisions (descriptor checks, execution codes,
+bookkeeping) agree with the oracle.  No device calls."""
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import evo_oracle as O
+from paper_2607_20293_amd import evo
+from paper_2607_20293_amd import inputs as I
+from tests.conftest import printed_unit_lattice
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _lib_or_skip():
+    if not os.path.exists(evo.LIB_PATH):
+        pytest.skip("libevo.so not built (run __graft_entry__.build())")
+    return evo.lib()
+
+
+def test_exports_every_declared_symbol():
+    L = _lib_or_skip()
+    hdr = open(os.path.join(ROOT, "include", "evo.h")).read()
+    declared = set(re.findall(r"\b(evo_[a-z_]+)\s*\(", hdr))
+    assert declared == set(evo.EXPORTED)
+    for name in declared:
+        assert hasattr(L, name), name
+
+
+@pytest.mark.parametrize("shape", [I.TINY, I.PUSHT, I.IMAGE, I.BIMANUAL])
+def test_weight_count_matches_layout(shape):
+    _lib_or_skip()
+    d = evo.make_desc(shape, "bf16", 4, 2)
+    assert evo.weight_count(d) == I.n_weight_floats(shape)
+
+
+def test_descriptor_validation():
+    _lib_or_skip()
+    d = evo.make_desc(I.PUSHT, "bf16", 4, 2)
+    assert evo.check_desc(d) == 0
+    bad = evo.make_desc(I.PUSHT, "bf16", 4, 2)
+    bad.n_heads = 3
+    assert evo.check_desc(bad) == -1
+    bad = evo.make_desc(I.PUSHT, "bf16", 0, 2)
+    assert evo.check_desc(bad) == -1
+    bad = evo.make_desc(I.PUSHT, "bf16", 4, 2)
+    bad.dtype = 7
+    assert evo.check_desc(bad) == -1
+    odd = evo.make_desc(I.PUSHT, "bf16", 4, 2)
+    odd.d_model, odd.n_heads = 128, 2          # valid shape, not compiled
+    assert evo.check_desc(odd) == -5
+    assert "no kernel" in evo.lib().evo_last_error().decode()
+    # the 768-wide shape is compiled for bf16 only
+    assert evo.check_desc(evo.make_desc(I.BIMANUAL, "bf16", 4, 2)) == 0
+    assert evo.check_desc(evo.make_desc(I.BIMANUAL, "fp32", 4, 2)) == -5
+
+
+@pytest.mark.parametrize("gran", [O.GRAN_LAYER, O.GRAN_UNIT])
+@pytest.mark.parametrize("cold", [O.COLD_COMPUTE, O.COLD_ZERO])
+def test_codes_follow_effective_lattice(gran, cold):
+    _lib_or_skip()
+    s = I.PUSHT
+    rng = np.random.default_rng(11)
+    rows = s.n_layers if gran == O.GRAN_LAYER else 3 * s.n_layers
+    lat = (rng.random((rows, s.n_steps)) < 0.3).astype(np.uint8)
+    lat[:, 0] = 0
+    lat[2, 0] = 1
+    desc = evo.make_desc(s, "bf16", 1, 1, cold)
+    codes = evo.schedule_codes(desc, lat, gran)
+    eff = O.effective_lattice(O.expand_lattice(lat, gran, s.n_layers), cold)
+    assert np.array_equal((codes & evo.CODE_EVAL) != 0, eff)
+    merged = gran == O.GRAN_LAYER
+    assert np.all(((codes & evo.CODE_MERGED) != 0) == merged)
+    U, T = eff.shape
+    for b in range(U):
+        seen = False
+        for t in range(T):
+            c = int(codes[b, t])
+            owner = (not merged) or b % 3 == 2     # merged sums live at the FFN position
+            if eff[b, t]:
+                seen = True
+                want_store = owner and t + 1 < T and not eff[b, t + 1]
+                assert bool(c & evo.CODE_STORE) == want_store, (b, t)
+                assert not c & evo.CODE_REUSE
+            else:
+                assert not c & evo.CODE_STORE
+                assert bool(c & evo.CODE_REUSE) == (seen and owner), (b, t)
+
+
+def _check_stats(shape, lats, ids, gran, cold):
+    desc = evo.make_desc(shape, "bf16", len(ids), len(lats), cold)
+    got = evo.schedule_stats(desc, lats, ids, gran)
+    want = O.bookkeeping(shape, lats, ids, gran, cold)
+    for k, v in want.items():
+        assert got[k] == v, (k, got[k], v)
+    return got
+
+
+@pytest.mark.parametrize("name", sorted(I.WORKLOADS))
+def test_stats_match_oracle_bookkeeping(name):
+    _lib_or_skip()
+    w = I.WORKLOADS[name]
+    inp = I.make_inputs(w, batch=min(w.batch, 64)) if w.shape.d_model < 768 else None
+    if inp is None:
+        lats = [I.make_lattice(w.schedule, w.shape.n_layers, w.shape.n_steps, w.density, 0)]
+        ids = np.zeros(w.batch, np.int32)
+    else:
+        lats, ids = inp.lattices, inp.ids
+    for cold in (O.COLD_COMPUTE, O.COLD_ZERO):
+        _check_stats(w.shape, lats, ids, O.GRAN_LAYER, cold)
+
+
+@pytest.mark.parametrize("tag", ["pusht", "kitchen", "lift_ph"])
+@pytest.mark.parametrize("method", ["BAC", "EVO"])
+def test_stats_printed_unit_schedules(tag, method):
+    _lib_or_skip()
+    lat = printed_unit_lattice(tag, method)
+    for cold in (O.COLD_COMPUTE, O.COLD_ZERO):
+        st = _check_stats(I.PUSHT, [lat], np.zeros(3, np.int32), O.GRAN_UNIT, cold)
+        if cold == O.COLD_ZERO:
+            assert st["refreshes_effective"] == 3 * int(lat.sum())
+
+
+def test_schedule_validation():
+    _lib_or_skip()
+    s = I.TINY
+    desc = evo.make_desc(s, "fp32", 1, 1)
+    lat = np.ones((s.n_layers, s.n_steps), np.uint8)
+    lat[0, 3] = 2
+    with pytest.raises(evo.EvoError) as e:
+        evo.schedule_codes(desc, lat, O.GRAN_LAYER)
+    assert e.value.code == -1
+    with pytest.raises(evo.EvoError):
+        evo.schedule_codes(desc, np.ones((5, s.n_steps), np.uint8), O.GRAN_LAYER)
