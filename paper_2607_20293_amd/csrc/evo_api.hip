@@ -52,6 +52,9 @@ int check_supported(const Shape& s) {
     int th;
     if (!kernel_available(k, &th)) continue;
     if (s.A > kernel_max_action_dim()) return fail(EVO_E_UNSUPPORTED, "action_dim %d > %d", s.A, kernel_max_action_dim());
+    if (s.T * opts[i] > kernel_max_steps_x_spt())
+      return fail(EVO_E_UNSUPPORTED, "n_steps %d too large for %d samples per tile (max %d)", s.T, opts[i],
+                  kernel_max_steps_x_spt() / opts[i]);
     if (s.n_obs > kernel_max_obs_tokens_for(k))
       return fail(EVO_E_UNSUPPORTED, "n_obs_tokens %d > %d for this shape", s.n_obs, kernel_max_obs_tokens_for(k));
     any = true;
@@ -73,7 +76,7 @@ struct evo_policy {
   WeightOffsets wo;
   std::vector<LayerOff> loff_h;
   std::vector<PackOff> poff_h;
-  uint64_t pk_obs = 0;
+  uint64_t pk_obs = 0, pk_win = 0, pk_wout = 0;
   int obs_pad = 0;
   float* d_raw = nullptr;
   uint4* d_pk = nullptr;
@@ -89,6 +92,10 @@ struct evo_policy {
   uint8_t* h_stage[2] = {nullptr, nullptr};
   hipEvent_t ev[2] = {nullptr, nullptr};
   int stage = 0;
+  std::vector<uint8_t> uploaded;   // plan bytes currently in d_plan
+  hipEvent_t ev_done = nullptr;    // recorded after the last launch
+  hipStream_t last_stream = nullptr;
+  bool launched = false;
   std::vector<Schedule> reg;
   evo_stats last{};
   bool has_last = false;
@@ -99,19 +106,20 @@ struct evo_policy {
 static void release(evo_policy* p) {
   if (!p) return;
   (void)hipDeviceSynchronize();
-  hipFree(p->d_raw);
-  hipFree(p->d_pk);
-  hipFree(p->d_loff);
-  hipFree(p->d_poff);
-  hipFree(p->d_tkv);
-  hipFree(p->d_ddpm);
-  hipFree(p->d_cache);
-  hipFree(p->d_okv);
-  hipFree(p->d_plan);
+  (void)hipFree(p->d_raw);
+  (void)hipFree(p->d_pk);
+  (void)hipFree(p->d_loff);
+  (void)hipFree(p->d_poff);
+  (void)hipFree(p->d_tkv);
+  (void)hipFree(p->d_ddpm);
+  (void)hipFree(p->d_cache);
+  (void)hipFree(p->d_okv);
+  (void)hipFree(p->d_plan);
   for (int i = 0; i < 2; ++i) {
     if (p->h_stage[i]) (void)hipHostFree(p->h_stage[i]);
     if (p->ev[i]) (void)hipEventDestroy(p->ev[i]);
   }
+  if (p->ev_done) (void)hipEventDestroy(p->ev_done);
   delete p;
 }
 
@@ -180,6 +188,11 @@ int evo_create_policy(const evo_policy_desc* desc, const float* host_weights, si
   uint64_t off = 0;
   p->pk_obs = off;
   off += frag16(d, p->obs_pad);
+  // embedding and head matrices stay fp32 (16 k per fragment)
+  p->pk_win = off;
+  off += (uint64_t)(d / 16) * 1 * 64;
+  p->pk_wout = off;
+  off += (uint64_t)1 * (d / 16) * 64;
   p->poff_h.resize(L);
   for (int l = 0; l < L; ++l) {
     PackOff& po = p->poff_h[l];
@@ -193,17 +206,19 @@ int evo_create_policy(const evo_policy_desc* desc, const float* host_weights, si
     po.pad_ = 0;
   }
   CREATE_TRY(hipMalloc(&p->d_pk, off * sizeof(uint4)));
-  CREATE_TRY(launch_pack(p->d_raw, wo.W_obs, d, s.obs_dim, p->obs_pad, s.dtype, p->d_pk + p->pk_obs, 0));
+  CREATE_TRY(launch_pack(p->d_raw, wo.W_obs, d, d, s.obs_dim, p->obs_pad, s.dtype, p->d_pk + p->pk_obs, 0));
+  CREATE_TRY(launch_pack(p->d_raw, wo.W_in, d, d, s.A, 16, EVO_FP32, p->d_pk + p->pk_win, 0));
+  CREATE_TRY(launch_pack(p->d_raw, wo.W_out, 16, s.A, d, d, EVO_FP32, p->d_pk + p->pk_wout, 0));
   for (int l = 0; l < L; ++l) {
     const auto& y = wo.layer[l];
     const PackOff& po = p->poff_h[l];
-    CREATE_TRY(launch_pack(p->d_raw, y.W_qkv, 3 * d, d, d, s.dtype, p->d_pk + po.qkv, 0));
-    CREATE_TRY(launch_pack(p->d_raw, y.W_o, d, d, d, s.dtype, p->d_pk + po.o, 0));
-    CREATE_TRY(launch_pack(p->d_raw, y.W_q, d, d, d, s.dtype, p->d_pk + po.q, 0));
-    CREATE_TRY(launch_pack(p->d_raw, y.W_kv, 2 * d, d, d, s.dtype, p->d_pk + po.kv, 0));
-    CREATE_TRY(launch_pack(p->d_raw, y.W_o2, d, d, d, s.dtype, p->d_pk + po.o2, 0));
-    CREATE_TRY(launch_pack(p->d_raw, y.W_1, s.dff, d, d, s.dtype, p->d_pk + po.w1, 0));
-    CREATE_TRY(launch_pack(p->d_raw, y.W_2, d, s.dff, s.dff, s.dtype, p->d_pk + po.w2, 0));
+    CREATE_TRY(launch_pack(p->d_raw, y.W_qkv, 3 * d, 3 * d, d, d, s.dtype, p->d_pk + po.qkv, 0));
+    CREATE_TRY(launch_pack(p->d_raw, y.W_o, d, d, d, d, s.dtype, p->d_pk + po.o, 0));
+    CREATE_TRY(launch_pack(p->d_raw, y.W_q, d, d, d, d, s.dtype, p->d_pk + po.q, 0));
+    CREATE_TRY(launch_pack(p->d_raw, y.W_kv, 2 * d, 2 * d, d, d, s.dtype, p->d_pk + po.kv, 0));
+    CREATE_TRY(launch_pack(p->d_raw, y.W_o2, d, d, d, d, s.dtype, p->d_pk + po.o2, 0));
+    CREATE_TRY(launch_pack(p->d_raw, y.W_1, s.dff, s.dff, d, d, s.dtype, p->d_pk + po.w1, 0));
+    CREATE_TRY(launch_pack(p->d_raw, y.W_2, d, d, s.dff, s.dff, s.dtype, p->d_pk + po.w2, 0));
   }
   // per-layer offsets of the small tensors
   p->loff_h.resize(L);
@@ -238,9 +253,9 @@ int evo_create_policy(const evo_policy_desc* desc, const float* host_weights, si
     if (e == hipSuccess)
       e = launch_time_kv(p->d_raw, (uint32_t)wo.P_mem, d_wkv, d_bkv, T, L, d, s.dtype, rows, p->d_tkv, 0);
     if (e == hipSuccess) e = hipDeviceSynchronize();
-    hipFree(d_wkv);
-    hipFree(d_bkv);
-    hipFree(rows);
+    (void)hipFree(d_wkv);
+    (void)hipFree(d_bkv);
+    (void)hipFree(rows);
     CREATE_TRY(e);
   }
   CREATE_TRY(hipMalloc(&p->d_ddpm, (size_t)T * 8 * sizeof(float)));
@@ -262,13 +277,14 @@ int evo_create_policy(const evo_policy_desc* desc, const float* host_weights, si
     CREATE_TRY(hipMalloc(&p->d_cache, p->cache_floats * sizeof(float)));
     CREATE_TRY(hipMalloc(&p->d_okv, (size_t)s.max_batch * L * s.n_obs * 2 * d * sizeof(float)));
     p->tiles_cap = tiles * spt_max;
-    p->codes_cap = (size_t)std::min(s.max_sched, s.max_batch) * U * T;
+    p->codes_cap = (size_t)std::min(s.max_sched, s.max_batch) * T * 3 * sizeof(uint64_t);
     p->plan_bytes = (2 * p->tiles_cap * sizeof(int32_t) + 255) / 256 * 256 + p->codes_cap;
     CREATE_TRY(hipMalloc(&p->d_plan, p->plan_bytes));
     for (int i = 0; i < 2; ++i) {
       CREATE_TRY(hipHostMalloc((void**)&p->h_stage[i], p->plan_bytes, hipHostMallocDefault));
       CREATE_TRY(hipEventCreateWithFlags(&p->ev[i], hipEventDisableTiming));
     }
+    CREATE_TRY(hipEventCreateWithFlags(&p->ev_done, hipEventDisableTiming));
   }
   CREATE_TRY(hipDeviceSynchronize());
 #undef CREATE_TRY
@@ -343,24 +359,31 @@ int evo_denoise(evo_policy* p, int32_t batch, const float* obs_cond, const float
   if (rc) return rc;
   const size_t ntile_ent = (size_t)plan.n_tiles * spt;
   const size_t codes_off = (2 * p->tiles_cap * sizeof(int32_t) + 255) / 256 * 256;
-  const size_t ucodes = (size_t)s.U() * s.T;
+  const size_t ucodes = (size_t)s.T * 3 * sizeof(uint64_t);
   if (ntile_ent > p->tiles_cap || plan.used.size() * ucodes > p->codes_cap)
     return fail(EVO_E_STATE, "plan exceeds the policy's buffers");
-  // stage the plan in pinned memory; the buffer is reused only after its
-  // previous copy has completed
-  const int st = p->stage;
-  if (hipEventSynchronize(p->ev[st]) != hipSuccess) return fail(EVO_E_HIP, "event synchronize failed");
-  uint8_t* hs = p->h_stage[st];
-  int32_t* ts = reinterpret_cast<int32_t*>(hs);
-  int32_t* tl = ts + p->tiles_cap;
-  std::memcpy(ts, plan.tile_sample.data(), ntile_ent * sizeof(int32_t));
-  std::memcpy(tl, plan.tile_slot.data(), ntile_ent * sizeof(int32_t));
-  for (size_t i = 0; i < plan.used.size(); ++i)
-    std::memcpy(hs + codes_off + i * ucodes, p->reg[plan.used[i]].codes.data(), ucodes);
+  // Calls on a different stream than the previous one wait for it: the
+  // plan, caches and observation keys/values are per-policy buffers.
+  if (p->launched && stream != p->last_stream) HIP_TRY(hipStreamWaitEvent(stream, p->ev_done, 0));
+  // Stage the plan in pinned memory and upload it, unless the device copy
+  // already holds exactly these bytes (repeated calls with the same ids).
   const size_t nbytes = codes_off + plan.used.size() * ucodes;
-  HIP_TRY(hipMemcpyAsync(p->d_plan, hs, nbytes, hipMemcpyHostToDevice, stream));
-  HIP_TRY(hipEventRecord(p->ev[st], stream));
-  p->stage ^= 1;
+  {
+    std::vector<uint8_t> bytes(nbytes, 0);
+    std::memcpy(bytes.data(), plan.tile_sample.data(), ntile_ent * sizeof(int32_t));
+    std::memcpy(bytes.data() + p->tiles_cap * sizeof(int32_t), plan.tile_slot.data(), ntile_ent * sizeof(int32_t));
+    for (size_t i = 0; i < plan.used.size(); ++i)
+      std::memcpy(bytes.data() + codes_off + i * ucodes, p->reg[plan.used[i]].masks.data(), ucodes);
+    if (bytes != p->uploaded) {
+      const int st = p->stage;
+      if (hipEventSynchronize(p->ev[st]) != hipSuccess) return fail(EVO_E_HIP, "event synchronize failed");
+      std::memcpy(p->h_stage[st], bytes.data(), nbytes);
+      HIP_TRY(hipMemcpyAsync(p->d_plan, p->h_stage[st], nbytes, hipMemcpyHostToDevice, stream));
+      HIP_TRY(hipEventRecord(p->ev[st], stream));
+      p->stage ^= 1;
+      p->uploaded.swap(bytes);
+    }
+  }
 
   KParams kp;
   std::memset(&kp, 0, sizeof(kp));
@@ -374,11 +397,16 @@ int evo_denoise(evo_policy* p, int32_t batch, const float* obs_cond, const float
   kp.tkv = p->d_tkv; kp.ddpm = p->d_ddpm;
   kp.tile_sample = reinterpret_cast<const int32_t*>(p->d_plan);
   kp.tile_slot = reinterpret_cast<const int32_t*>(p->d_plan) + p->tiles_cap;
-  kp.codes = p->d_plan + codes_off;
+  kp.masks = reinterpret_cast<const uint64_t*>(p->d_plan + codes_off);
+  kp.pk_win = p->pk_win;
+  kp.pk_wout = p->pk_wout;
   kp.obs = obs_cond; kp.noise = noise; kp.out = actions_out; kp.okv = p->d_okv; kp.cache = p->d_cache;
   kp.batch = batch;
   KernelKey key{s.d, s.dh(), s.H, s.dff, s.dtype, spt};
   HIP_TRY(launch_denoise(key, kp, stream));
+  HIP_TRY(hipEventRecord(p->ev_done, stream));
+  p->last_stream = stream;
+  p->launched = true;
 
   call_stats(s, p->reg, schedule_ids, batch, &plan, &p->last);
   p->has_last = true;

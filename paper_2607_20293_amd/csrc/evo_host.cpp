@@ -144,6 +144,19 @@ int build_schedule(const Shape& s, const uint8_t* lattice, int rows, int granula
       sc.codes[(size_t)b * T + t] = c;
     }
   }
+  sc.masks.assign((size_t)T * 3, 0);
+  for (int t = 0; t < T; ++t) {
+    uint64_t ev = 0, ru = 0, st = 0;
+    for (int b = 0; b < U; ++b) {
+      const uint8_t c = sc.codes[(size_t)b * T + t];
+      if (c & CODE_EVAL) ev |= 1ull << b;
+      if (c & CODE_REUSE) ru |= 1ull << b;
+      if (c & CODE_STORE) st |= 1ull << b;
+    }
+    sc.masks[(size_t)t * 3 + 0] = ev | (sc.merged ? MASK_MERGED_BIT : 0);
+    sc.masks[(size_t)t * 3 + 1] = ru;
+    sc.masks[(size_t)t * 3 + 2] = st;
+  }
   *out = std::move(sc);
   return EVO_OK;
 }

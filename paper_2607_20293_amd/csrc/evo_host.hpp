@@ -8,7 +8,7 @@
 #include <string>
 #include <vector>
 
-#include "../../include/evo.h"
+#include "evo.h"
 
 namespace evo {
 
@@ -76,8 +76,13 @@ struct Schedule {
   uint64_t flops_kernel = 0;    // this implementation, per sample (without per-query work)
   uint64_t reuse_count = 0;     // positions with CODE_REUSE
   uint64_t store_count = 0;     // positions with CODE_STORE
-  std::vector<uint64_t> eval_mask;  // [T] bitmask of evaluated units (U <= 64)
+  std::vector<uint64_t> eval_mask;  // [T] bitmask of evaluated units (U <= 63)
+  // Device form of the codes: per step t, three unit bitmasks
+  // {evaluate, reuse, store} (bit 63 of the evaluate mask = layer-merged).
+  std::vector<uint64_t> masks;      // [T][3]
 };
+
+constexpr uint64_t MASK_MERGED_BIT = 1ull << 63;
 
 // Build execution codes from a lattice (rows = L or 3L, row-major [rows][T]).
 int build_schedule(const Shape& s, const uint8_t* lattice, int rows, int granularity,

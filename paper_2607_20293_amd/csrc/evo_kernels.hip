@@ -6,20 +6,24 @@
 // whole query is one launch with no grid-wide synchronisation.
 //
 //  * The residual stream h of the tile lives in registers, laid out as the
-//    accumulator fragments of the 16x16 MFMA tiles (each wave owns a fixed
-//    set of 16-column blocks of d).
-//  * Cacheable units (Sec. 3.1: SA, CA, FFN residual branches) are evaluated
-//    only where the schedule says so (Eq. 1); their residual is then
-//    stored in a per-tile cache in HBM only if a later step reuses it.
-//    Elsewhere the unit adds the cached residual of its most recent refresh.
+//    accumulator fragments of 16x16 MFMA tiles (each wave owns a fixed set
+//    of 16-column blocks of d).
+//  * The schedule arrives as per-step unit bitmasks {evaluate, reuse,
+//    store}.  Cacheable units (Sec. 3.1: SA, CA, FFN residual branches) are
+//    evaluated only where the schedule says so (Eq. 1); a refreshed residual
+//    is stored in the tile's cache in HBM only if a later step reuses it.
+//    Between two evaluated units the reused residuals of the skipped units
+//    are added in order, their cache loads issued in batches.
 //  * Every unit is "LayerNorm -> chunked stage-1 product -> per-chunk
 //    transform (attention per head group, or GELU) -> stage-2 product
 //    accumulated into the unit's residual".  Activations stay in LDS;
 //    projection weights are streamed from L2/HBM as pre-packed 1 KiB MFMA
 //    fragments (16 output columns x 32 bf16 / 16 fp32 of K, 16 bytes per
-//    lane), so every weight load is one coalesced 16-byte load per lane.
-//  * The head (final LayerNorm + linear) and the DDPM update are fused at
-//    the end of every step.
+//    lane), so every weight load is one coalesced 16-byte load per lane, and
+//    the first fragments of each product are requested before the phase
+//    that precedes it.
+//  * Attention, the action embedding and the head use fp32 16x16x4 MFMA
+//    tiles; the DDPM update is fused at the end of every step.
 #include "evo_kernels.hpp"
 
 #include <cmath>
@@ -30,13 +34,26 @@ namespace evo {
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
-enum : uint8_t { C_EVAL = 1, C_STORE = 2, C_REUSE = 4, C_MERGED = 8 };
+constexpr uint64_t kMergedBit = 1ull << 63;
+constexpr int kMaskEntries = 341;  // (T x samples per tile) entries of 3 x u64 in LDS (8 KiB)
 
 // float -> bfloat16 bits, round to nearest even (finite inputs)
 __device__ __forceinline__ uint32_t bf16_rne(float f) {
   uint32_t u = __float_as_uint(f);
   u += 0x7FFFu + ((u >> 16) & 1u);
   return u >> 16;
+}
+
+__device__ __forceinline__ f32x4 mfma4(float a, float b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
+// Orders a wave's own LDS writes before its following LDS reads (other
+// lanes' data) without a workgroup barrier.
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
 // Operand traits of the two matmul precisions.  A fragment is 16 bytes per
@@ -64,34 +81,50 @@ template <> struct Op<float> {
     buf[row * ld + pcol(k)] = v;
   }
   __device__ static __forceinline__ void mma(f32x4& acc, uint4 a, uint4 b) {
-    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.x), __uint_as_float(b.x), acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.y), __uint_as_float(b.y), acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.z), __uint_as_float(b.z), acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.w), __uint_as_float(b.w), acc, 0, 0, 0);
+    acc = mfma4(__uint_as_float(a.x), __uint_as_float(b.x), acc);
+    acc = mfma4(__uint_as_float(a.y), __uint_as_float(b.y), acc);
+    acc = mfma4(__uint_as_float(a.z), __uint_as_float(b.z), acc);
+    acc = mfma4(__uint_as_float(a.w), __uint_as_float(b.w), acc);
   }
 };
 
+// First weight fragments of a product (issued ahead of the product).
+template <int MPW, class GCB>
+__device__ __forceinline__ void gemm_pref(uint4 (&bc)[MPW], const uint4* W, int KBT, int kf0, GCB gcb, int lane) {
+#pragma unroll
+  for (int m = 0; m < MPW; ++m) bc[m] = W[((size_t)gcb(m) * KBT + kf0) * 64 + lane];
+}
+
 // acc[m][rb] += A[rb*16 .. +16][k-range] x W[col block gcb(m)][k-range]^T
-// A: LDS operand, row stride lda elements, already offset to the k-range
-// start.  W: packed fragments of a matrix with KBT fragments per column
-// block; kf0 is the first fragment of the k-range, NKF its length.  The
-// next k step's weight fragments are loaded before the current MFMAs.
+// A: LDS operand, row stride lda elements, offset to the k-range start.
+// W: packed fragments of a matrix with KBT fragments per column block; kf0
+// is the first fragment of the k-range, NKF its length; bc holds the
+// fragments of kf0 (gemm_pref).  Weight fragments are requested PD k-steps
+// ahead of their MFMAs (about six 1 KiB fragments in flight per wave); a
+// scheduling fence per step keeps the compiler from hoisting further loads.
 template <class AT, int RBk, int MPW, int NKF, class GCB>
-__device__ __forceinline__ void gemm_acc(f32x4 (&acc)[MPW][RBk], const AT* A, int lda, const uint4* W,
-                                         int KBT, int kf0, GCB gcb, int lane) {
+__device__ __forceinline__ void gemm_run(f32x4 (&acc)[MPW][RBk], const AT* A, int lda, const uint4* W, int KBT,
+                                         int kf0, GCB gcb, int lane, uint4 (&bc)[MPW]) {
   using O = Op<AT>;
+  constexpr int PD0 = 6 / MPW > 0 ? 6 / MPW : 1;
+  constexpr int PD = PD0 < NKF ? PD0 : (NKF > 1 ? NKF - 1 : 1);
   const int lc = lane & 15, lq = lane >> 4;
   const uint4* wp[MPW];
 #pragma unroll
   for (int m = 0; m < MPW; ++m) wp[m] = W + ((size_t)gcb(m) * KBT + kf0) * 64 + lane;
-  uint4 bc[MPW], bn[MPW];
+  uint4 buf[PD + 1][MPW];
 #pragma unroll
-  for (int m = 0; m < MPW; ++m) bc[m] = wp[m][0];
+  for (int m = 0; m < MPW; ++m) buf[0][m] = bc[m];
+#pragma unroll
+  for (int d = 1; d < PD; ++d)
+#pragma unroll
+    for (int m = 0; m < MPW; ++m)
+      if (d < NKF) buf[d][m] = wp[m][d * 64];
 #pragma unroll
   for (int kf = 0; kf < NKF; ++kf) {
-    if (kf + 1 < NKF) {
+    if (kf + PD < NKF) {
 #pragma unroll
-      for (int m = 0; m < MPW; ++m) bn[m] = wp[m][(kf + 1) * 64];
+      for (int m = 0; m < MPW; ++m) buf[(kf + PD) % (PD + 1)][m] = wp[m][(kf + PD) * 64];
     }
     uint4 a[RBk];
 #pragma unroll
@@ -100,12 +133,17 @@ __device__ __forceinline__ void gemm_acc(f32x4 (&acc)[MPW][RBk], const AT* A, in
 #pragma unroll
     for (int m = 0; m < MPW; ++m)
 #pragma unroll
-      for (int rb = 0; rb < RBk; ++rb) O::mma(acc[m][rb], a[rb], bc[m]);
-    if (kf + 1 < NKF) {
-#pragma unroll
-      for (int m = 0; m < MPW; ++m) bc[m] = bn[m];
-    }
+      for (int rb = 0; rb < RBk; ++rb) O::mma(acc[m][rb], a[rb], buf[kf % (PD + 1)][m]);
+    __builtin_amdgcn_sched_barrier(0);
   }
+}
+
+template <class AT, int RBk, int MPW, int NKF, class GCB>
+__device__ __forceinline__ void gemm_acc(f32x4 (&acc)[MPW][RBk], const AT* A, int lda, const uint4* W, int KBT,
+                                         int kf0, GCB gcb, int lane) {
+  uint4 bc[MPW];
+  gemm_pref<MPW>(bc, W, KBT, kf0, gcb, lane);
+  gemm_run<AT, RBk, MPW, NKF>(acc, A, lda, W, KBT, kf0, gcb, lane, bc);
 }
 
 __device__ __forceinline__ float gelu_erf(float v) { return 0.5f * v * (1.0f + erff(v * 0.70710678118654752f)); }
@@ -122,112 +160,117 @@ struct Cfg {
   static constexpr int GW = HG * DH;
   static constexpr int LDY = 3 * GW + 4;
   static constexpr int ZW = GW > FC ? GW : FC;
-  static constexpr int AMAX = 16;
   static constexpr int KOBS = 64;
-  static constexpr int PW = HZ > SMAX ? HZ : SMAX;
+  static constexpr int NJB = HZ >= 16 ? HZ / 16 : 1;   // key blocks per query block (self-attention)
+  static constexpr int SPB = HZ >= 16 ? 1 : 16 / HZ;   // samples per 16-row block
+  static constexpr int SLOTS = 16 / SPB;               // memory columns per sample in a 16-wide tile
+  static constexpr int PS = 17;                        // stride of a 16x16 fp32 scratch tile
+  static constexpr int PWN = (NJB > RB ? NJB : RB) * 16 * PS;
+  static constexpr int NB = (4 / (CBW * RB)) > 0 ? (4 / (CBW * RB)) : 1;  // reuse loads per batch
 };
 
-// Per-lane rows of the fragment layout: row = rb*16 + lq*4 + i.
-// LayerNorm statistics of the tile rows from the register-resident stream.
+// LayerNorm statistics of the tile rows from the register-resident stream:
+// per-lane (mean, M2) over its columns, merged across the 16 lanes of a row
+// group with shuffles and across waves through LDS (one barrier).
 template <class C>
-__device__ __forceinline__ void row_stats(const f32x4 (&h)[C::CBW][C::RB], float (*red)[C::NWV][C::R],
-                                          float (&mu)[C::RB][4], float (&rs)[C::RB][4], int w, int lc,
-                                          int lq) {
+__device__ __forceinline__ void ln_stats(const f32x4 (&h)[C::CBW][C::RB], float (*red)[C::R][2],
+                                         float (&mu)[C::RB][4], float (&rs)[C::RB][4], int w, int lc, int lq) {
   constexpr int D = C::CB * 16;
-  float s[C::RB][4];
+  constexpr float nw = 16.0f * C::CBW;
 #pragma unroll
   for (int rb = 0; rb < C::RB; ++rb)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      float v = 0.f;
+      float m = 0.f;
 #pragma unroll
-      for (int c = 0; c < C::CBW; ++c) v += h[c][rb][i];
-#pragma unroll
-      for (int off = 1; off < 16; off <<= 1) v += __shfl_xor(v, off);
-      s[rb][i] = v;
-    }
-  if (lc == 0) {
-#pragma unroll
-    for (int rb = 0; rb < C::RB; ++rb)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) red[0][w][rb * 16 + lq * 4 + i] = s[rb][i];
-  }
-  __syncthreads();
-#pragma unroll
-  for (int rb = 0; rb < C::RB; ++rb)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      float v = 0.f;
-#pragma unroll
-      for (int ww = 0; ww < C::NWV; ++ww) v += red[0][ww][rb * 16 + lq * 4 + i];
-      mu[rb][i] = v * (1.0f / D);
+      for (int c = 0; c < C::CBW; ++c) m += h[c][rb][i];
+      m *= (1.0f / C::CBW);
       float q = 0.f;
 #pragma unroll
       for (int c = 0; c < C::CBW; ++c) {
-        const float e = h[c][rb][i] - mu[rb][i];
+        const float e = h[c][rb][i] - m;
         q += e * e;
       }
+      float n = (float)C::CBW;
 #pragma unroll
-      for (int off = 1; off < 16; off <<= 1) q += __shfl_xor(q, off);
-      s[rb][i] = q;
+      for (int off = 1; off < 16; off <<= 1) {
+        const float mo = __shfl_xor(m, off), qo = __shfl_xor(q, off);
+        const float d = mo - m;
+        m = 0.5f * (m + mo);
+        q = q + qo + d * d * (0.5f * n);
+        n *= 2.f;
+      }
+      if (lc == 0) {
+        red[w][rb * 16 + lq * 4 + i][0] = m;
+        red[w][rb * 16 + lq * 4 + i][1] = q;
+      }
     }
-  if (lc == 0) {
-#pragma unroll
-    for (int rb = 0; rb < C::RB; ++rb)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) red[1][w][rb * 16 + lq * 4 + i] = s[rb][i];
-  }
   __syncthreads();
 #pragma unroll
   for (int rb = 0; rb < C::RB; ++rb)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      float v = 0.f;
+      const int row = rb * 16 + lq * 4 + i;
+      float M = red[0][row][0], Q = red[0][row][1], n = nw;
 #pragma unroll
-      for (int ww = 0; ww < C::NWV; ++ww) v += red[1][ww][rb * 16 + lq * 4 + i];
-      rs[rb][i] = 1.0f / sqrtf(v * (1.0f / D) + 1e-5f);
+      for (int ww = 1; ww < C::NWV; ++ww) {
+        const float mb = red[ww][row][0], qb = red[ww][row][1];
+        const float d = mb - M, tot = n + nw;
+        M += d * (nw / tot);
+        Q += qb + d * d * (n * nw / tot);
+        n = tot;
+      }
+      mu[rb][i] = M;
+      rs[rb][i] = 1.0f / sqrtf(Q * (1.0f / D) + 1e-5f);
     }
 }
 
 template <class AT, int D, int DH, int HZ, int SPT, int DFF, int NW, int HG, int FC, int SMAX>
 __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
   using O = Op<AT>;
+  using OF = Op<float>;
   using C = Cfg<D, DH, HZ, SPT, DFF, NW, HG, FC, SMAX>;
   constexpr int NT = C::NT, R = C::R, RB = C::RB, NH = C::NH, CB = C::CB, CBW = C::CBW, GW = C::GW;
-  constexpr int LDA = D + O::PAD, LDY = C::LDY, LDZ = C::ZW + O::PAD, AMAX = C::AMAX;
+  constexpr int LDA = D + O::PAD, LDY = C::LDY, LDZ = C::ZW + O::PAD;
   constexpr int KOBS = C::KOBS, LDO = KOBS + O::PAD;
+  constexpr int NJB = C::NJB, SLOTS = C::SLOTS, PS = C::PS, PWN = C::PWN, NB = C::NB;
   static_assert(R % 16 == 0 && CB % NW == 0 && NH % HG == 0 && DFF % FC == 0, "tile shape");
   static_assert((3 * GW / 16) % NW == 0 && (GW / 16) % NW == 0 && (FC / 16) % NW == 0, "block split");
   static_assert(HZ % 4 == 0 && (HZ & (HZ - 1)) == 0 && HZ <= 64, "horizon must be a power of two in [4, 64]");
-  static_assert(NW * R * AMAX <= R * LDY, "head partials must fit the stage-1 buffer");
+  static_assert(NW * R * 16 <= R * LDY, "head partials must fit the stage-1 buffer");
   static_assert(16 * LDO * (int)sizeof(AT) <= R * LDY * 4, "observation operand must fit");
+  static_assert(SMAX <= SLOTS, "memory tokens per sample must fit a 16-column tile");
+  static_assert(DH % 16 == 0, "head dim");
+  constexpr bool KEEP_EMB = RB == 1 && CBW <= 4;  // embedding constants kept in registers across steps
+  constexpr float kScale = (DH == 64) ? 0.125f : (DH == 32 ? 0.17677669529663688f : 0.0f);
+  static_assert(DH == 64 || DH == 32, "head dim");
 
   __shared__ __attribute__((aligned(16))) AT xa[R * LDA];
   __shared__ __attribute__((aligned(16))) float ybuf[R * LDY];
   __shared__ __attribute__((aligned(16))) AT zbuf[R * LDZ];
-  __shared__ float pbuf[SPT * HG * HZ * C::PW];
+  __shared__ __attribute__((aligned(16))) float pw[NW * PWN];
   __shared__ __attribute__((aligned(16))) float kvbuf[SPT * SMAX * 2 * GW];
-  __shared__ float red[2][NW][R];
-  __shared__ float xs[R * AMAX];
-  __shared__ int smp[SPT], slt[SPT];
+  __shared__ float red[NW][R][2];
+  __shared__ __attribute__((aligned(16))) float xs[R * 16];
+  __shared__ uint64_t msk[kMaskEntries * 3];
+  __shared__ int smp[SPT];
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, lc = lane & 15, lq = lane >> 4;
   const int tile = blockIdx.x;
   const int L = p.L, A = p.A, T = p.T, U = 3 * L, nobs = p.n_obs, S = 1 + nobs;
   const float* raw = p.raw;
-  constexpr float kScale = (DH == 64) ? 0.125f : (DH == 32 ? 0.17677669529663688f : 0.0f);
-  static_assert(DH == 64 || DH == 32, "head dim");
 
-  if (tid < SPT) {
-    smp[tid] = p.tile_sample[tile * SPT + tid];
-    slt[tid] = p.tile_slot[tile * SPT + tid];
+  if (tid < SPT) smp[tid] = p.tile_sample[tile * SPT + tid];
+  for (int it = tid; it < SPT * T * 3; it += NT) {
+    const int j = it / (T * 3), r = it % (T * 3);
+    msk[it] = p.masks[(size_t)p.tile_slot[tile * SPT + j] * T * 3 + r];
   }
   __syncthreads();
 
-  // initial sample x_T
-  for (int it = tid; it < R * A; it += NT) {
-    const int row = it / A, a = it % A, j = row / HZ, s = smp[j];
-    xs[row * AMAX + a] = s >= 0 ? p.noise[((size_t)s * HZ + (row % HZ)) * A + a] : 0.f;
+  // initial sample x_T, stored [row][pcol(a)] (zero-padded to 16 columns)
+  for (int it = tid; it < R * 16; it += NT) {
+    const int row = it / 16, a = it % 16, s = smp[row / HZ];
+    xs[row * 16 + OF::pcol(a)] = (s >= 0 && a < A) ? p.noise[((size_t)s * HZ + (row % HZ)) * A + a] : 0.f;
   }
 
   // ---- per query: observation tokens and their keys/values in every layer
@@ -250,8 +293,8 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
         O::store(ob, LDO, row, k, v);
       }
       __syncthreads();
-      gemm_acc<AT, 1, MPWO, KOBS / O::KF>(acc, ob, LDO, p.pk + p.pk_obs, p.obs_pad / O::KF,
-                                           c * (KOBS / O::KF), [&](int m) { return w + NW * m; }, lane);
+      gemm_acc<AT, 1, MPWO, KOBS / O::KF>(acc, ob, LDO, p.pk + p.pk_obs, p.obs_pad / O::KF, c * (KOBS / O::KF),
+                                           [&](int m) { return w + NW * m; }, lane);
     }
     // memory-token operand rows (row = slot*n_obs + token) in xa
 #pragma unroll
@@ -294,10 +337,35 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
     __syncthreads();
   }
 
-  const uint8_t* codes[SPT];
+  // sample slot of each of this lane's fragment row groups (4 rows, one sample)
+  int jrow[RB];
 #pragma unroll
-  for (int j = 0; j < SPT; ++j) codes[j] = p.codes + (size_t)slt[j] * U * T;
+  for (int rb = 0; rb < RB; ++rb) jrow[rb] = (rb * 16 + lq * 4) / HZ;
   float* cbase = p.cache + (size_t)tile * U * (R * D);
+  const auto cfrag = [&](int unit, int c, int rb) {
+    return reinterpret_cast<f32x4*>(cbase + (size_t)unit * (R * D) +
+                                    ((size_t)((w * RB + rb) * CBW + c) * 64 + lane) * 4);
+  };
+  const uint4* pk = p.pk;
+
+  // embedding / head constants of this lane's columns
+  uint4 win[KEEP_EMB ? CBW : 1];
+  f32x4 pb[KEEP_EMB ? CBW : 1][KEEP_EMB ? RB : 1];
+  float lfg[KEEP_EMB ? CBW : 1], lfb[KEEP_EMB ? CBW : 1];
+  if constexpr (KEEP_EMB) {
+#pragma unroll
+    for (int c = 0; c < CBW; ++c) {
+      const int col = (w * CBW + c) * 16 + lc;
+      win[c] = pk[p.pk_win + (size_t)(w * CBW + c) * 64 + lane];
+      const float bi = raw[p.b_in + col];
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) pb[c][rb][i] = bi + raw[p.P_act + (size_t)((rb * 16 + lq * 4 + i) % HZ) * D + col];
+      lfg[c] = raw[p.lnf_g + col];
+      lfb[c] = raw[p.lnf_b + col];
+    }
+  }
 
   f32x4 h[CBW][RB], mac[CBW][RB];
 #pragma unroll
@@ -305,10 +373,34 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) mac[c][rb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+  constexpr int ZPT = (R * 16 + NT - 1) / NT;
+  constexpr int MPWQ = (3 * GW / 16) / NW, MPWC = (GW / 16) / NW, MPWF = (FC / 16) / NW;
+
   for (int t = 0; t < T; ++t) {
     const int k = T - 1 - t;
+    // schedule of this step for every sample slot
+    uint64_t mev[SPT], mru[SPT], mst[SPT];
+    bool mmg[SPT];
+    uint64_t evT = 0, ruT = 0;
+#pragma unroll
+    for (int j = 0; j < SPT; ++j) {
+      const bool live = smp[j] >= 0;
+      const uint64_t e0 = live ? msk[(j * T + t) * 3 + 0] : 0ull;
+      mmg[j] = (e0 & kMergedBit) != 0;
+      mev[j] = e0 & ~kMergedBit;
+      mru[j] = live ? msk[(j * T + t) * 3 + 1] : 0ull;
+      mst[j] = live ? msk[(j * T + t) * 3 + 2] : 0ull;
+      evT |= mev[j];
+      ruT |= mru[j];
+    }
+    const auto pick = [&](const uint64_t (&m)[SPT], int j) {
+      uint64_t v = m[0];
+#pragma unroll
+      for (int jj = 1; jj < SPT; ++jj)
+        if (j == jj) v = m[jj];
+      return v;
+    };
     // noise added by this step's update (prefetched)
-    constexpr int ZPT = (R * AMAX + NT - 1) / NT;
     float zpre[ZPT];
 #pragma unroll
     for (int q = 0; q < ZPT; ++q) {
@@ -319,295 +411,396 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
         if (s >= 0) zpre[q] = p.noise[(((size_t)(t + 1) * p.batch + s) * HZ + (row % HZ)) * A + a];
       }
     }
-    // embedding of the current sample: h = x W_in^T + b_in + P_act
+    // ---- embedding of the current sample on fp32 MFMA: h = (b_in + P_act) + x W_in^T
+    {
+      uint4 xf[RB];
 #pragma unroll
-    for (int c = 0; c < CBW; ++c) {
-      const int col = (w * CBW + c) * 16 + lc;
-      const float bi = raw[p.b_in + col];
+      for (int rb = 0; rb < RB; ++rb) xf[rb] = *reinterpret_cast<const uint4*>(xs + (rb * 16 + lc) * 16 + lq * 4);
 #pragma unroll
-      for (int rb = 0; rb < RB; ++rb)
+      for (int c = 0; c < CBW; ++c) {
+        uint4 wv;
+        if constexpr (KEEP_EMB) wv = win[c];
+        else wv = pk[p.pk_win + (size_t)(w * CBW + c) * 64 + lane];
+        const int col = (w * CBW + c) * 16 + lc;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int row = rb * 16 + lq * 4 + i;
-          float v = 0.f;
-          for (int a = 0; a < A; ++a) v += xs[row * AMAX + a] * raw[p.W_in + (size_t)col * A + a];
-          h[c][rb][i] = v + bi + raw[p.P_act + (size_t)(row % HZ) * D + col];
+        for (int rb = 0; rb < RB; ++rb) {
+          f32x4 acc;
+          if constexpr (KEEP_EMB) {
+            acc = pb[c][rb];
+          } else {
+            const float bi = raw[p.b_in + col];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) acc[i] = bi + raw[p.P_act + (size_t)((rb * 16 + lq * 4 + i) % HZ) * D + col];
+          }
+          OF::mma(acc, xf[rb], wv);
+          h[c][rb] = acc;
         }
+      }
     }
 
-    for (int b = 0; b < U; ++b) {
-      const int l = b / 3, u = b - 3 * (b / 3);
-      uint8_t code[SPT];
-      bool ev = false;
+    // ---- the cacheable units (Eq. 1)
+    int b = 0;
+    while (true) {
+      const uint64_t rest = evT >> b;
+      const int e = rest ? b + __builtin_ctzll(rest) : U;
+      // reused residuals of the units in [b, e), in unit order
+      {
+        const uint64_t lo_m = (b >= 64) ? ~0ull : ((1ull << b) - 1);
+        const uint64_t hi_m = (e >= 64) ? ~0ull : ((1ull << e) - 1);
+        uint64_t um = ruT & hi_m & ~lo_m;
+        while (um) {
+          int ub[NB];
 #pragma unroll
-      for (int j = 0; j < SPT; ++j) {
-        code[j] = smp[j] >= 0 ? codes[j][(size_t)b * T + t] : (uint8_t)0;
-        ev |= (code[j] & C_EVAL) != 0;
+          for (int q = 0; q < NB; ++q) {
+            ub[q] = um ? __builtin_ctzll(um) : -1;
+            um = um ? (um & (um - 1)) : 0ull;
+          }
+          f32x4 v[NB][CBW][RB];
+#pragma unroll
+          for (int q = 0; q < NB; ++q)
+#pragma unroll
+            for (int c = 0; c < CBW; ++c)
+#pragma unroll
+              for (int rb = 0; rb < RB; ++rb) {
+                v[q][c][rb] = f32x4{0.f, 0.f, 0.f, 0.f};
+                if (ub[q] >= 0 && ((pick(mru, jrow[rb]) >> ub[q]) & 1ull)) v[q][c][rb] = *cfrag(ub[q], c, rb);
+              }
+#pragma unroll
+          for (int q = 0; q < NB; ++q)
+#pragma unroll
+            for (int c = 0; c < CBW; ++c)
+#pragma unroll
+              for (int rb = 0; rb < RB; ++rb) h[c][rb] += v[q][c][rb];
+        }
       }
+      if (e >= U) break;
+
+      // ---- evaluate unit e for the tile
+      const int l = e / 3, u = e - 3 * l;
+      const LayerOff lo = p.loff[l];
+      const PackOff po = p.poff[l];
+      const uint32_t gofs = u == 0 ? lo.ln1_g : (u == 1 ? lo.ln2_g : lo.ln3_g);
+      const uint32_t bofs = u == 0 ? lo.ln1_b : (u == 1 ? lo.ln2_b : lo.ln3_b);
+      const uint32_t r_bias = u == 0 ? lo.b_o : (u == 1 ? lo.b_o2 : lo.b_2);
+      float lg[CBW], lb[CBW], rbias[CBW];
+#pragma unroll
+      for (int c = 0; c < CBW; ++c) {
+        const int col = (w * CBW + c) * 16 + lc;
+        lg[c] = raw[gofs + col];
+        lb[c] = raw[bofs + col];
+        rbias[c] = raw[r_bias + col];
+      }
+      const auto gcb_sa = [&](int g) {
+        return [=](int m) {
+          const int iloc = w + NW * m, part = iloc / (GW / 16), within = iloc % (GW / 16);
+          return part * CB + g * (GW / 16) + within;
+        };
+      };
+      const auto gcb_ca = [&](int g) { return [=](int m) { return g * (GW / 16) + w + NW * m; }; };
+      const auto gcb_ff = [&](int ch) { return [=](int m) { return ch * (FC / 16) + w + NW * m; }; };
+      const auto own = [&](int m) { return w * CBW + m; };
       f32x4 r[CBW][RB];
-      if (ev) {
-        const LayerOff lo = p.loff[l];
-        const PackOff po = p.poff[l];
+#pragma unroll
+      for (int c = 0; c < CBW; ++c)
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) r[c][rb] = f32x4{0.f, 0.f, 0.f, 0.f};
+      // LayerNorm of the unit's input into the stage-1 operand buffer
+      const auto layer_norm_to_xa = [&]() {
         float mu[RB][4], rs[RB][4];
-        row_stats<C>(h, red, mu, rs, w, lc, lq);
-        const uint32_t gofs = u == 0 ? lo.ln1_g : (u == 1 ? lo.ln2_g : lo.ln3_g);
-        const uint32_t bofs = u == 0 ? lo.ln1_b : (u == 1 ? lo.ln2_b : lo.ln3_b);
+        ln_stats<C>(h, red, mu, rs, w, lc, lq);
 #pragma unroll
         for (int c = 0; c < CBW; ++c) {
           const int col = (w * CBW + c) * 16 + lc;
-          const float g = raw[gofs + col], bb = raw[bofs + col];
 #pragma unroll
           for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
             for (int i = 0; i < 4; ++i)
-              O::store(xa, LDA, rb * 16 + lq * 4 + i, col, (h[c][rb][i] - mu[rb][i]) * rs[rb][i] * g + bb);
+              O::store(xa, LDA, rb * 16 + lq * 4 + i, col, (h[c][rb][i] - mu[rb][i]) * rs[rb][i] * lg[c] + lb[c]);
         }
-#pragma unroll
-        for (int c = 0; c < CBW; ++c)
-#pragma unroll
-          for (int rb = 0; rb < RB; ++rb) r[c][rb] = f32x4{0.f, 0.f, 0.f, 0.f};
         __syncthreads();
-        const auto own = [&](int m) { return w * CBW + m; };
+      };
 
-        if (u == 0) {
-          // ---------------- self-attention unit (causal over the action tokens)
-          for (int g = 0; g < NH / HG; ++g) {
-            constexpr int MPW1 = (3 * GW / 16) / NW;
-            const auto gcb = [&](int m) {
-              const int iloc = w + NW * m, part = iloc / (GW / 16), within = iloc % (GW / 16);
-              return part * CB + g * (GW / 16) + within;
-            };
-            f32x4 y[MPW1][RB];
+      if (u == 0) {
+        // ---------------- self-attention unit (causal over the action tokens)
+        uint4 b1q[MPWQ];  // stage-1 weights of the first chunk, requested before the LayerNorm
+        gemm_pref<MPWQ>(b1q, pk + po.qkv, D / O::KF, 0, gcb_sa(0), lane);
+        layer_norm_to_xa();
+        for (int g = 0; g < NH / HG; ++g) {
+          f32x4 y[MPWQ][RB];
 #pragma unroll
-            for (int m = 0; m < MPW1; ++m)
+          for (int m = 0; m < MPWQ; ++m)
 #pragma unroll
-              for (int rb = 0; rb < RB; ++rb) y[m][rb] = f32x4{0.f, 0.f, 0.f, 0.f};
-            gemm_acc<AT, RB, MPW1, D / O::KF>(y, xa, LDA, p.pk + po.qkv, D / O::KF, 0, gcb, lane);
+            for (int rb = 0; rb < RB; ++rb) y[m][rb] = f32x4{0.f, 0.f, 0.f, 0.f};
+          if (g > 0) gemm_pref<MPWQ>(b1q, pk + po.qkv, D / O::KF, 0, gcb_sa(g), lane);
+          gemm_run<AT, RB, MPWQ, D / O::KF>(y, xa, LDA, pk + po.qkv, D / O::KF, 0, gcb_sa(g), lane, b1q);
+          uint4 b2[CBW];
+          gemm_pref<CBW>(b2, pk + po.o, D / O::KF, g * (GW / O::KF), own, lane);
 #pragma unroll
-            for (int m = 0; m < MPW1; ++m) {
-              const int loc = (w + NW * m) * 16 + lc, gcol = gcb(m) * 16 + lc;
-              const float bq = raw[lo.b_qkv + gcol];
+          for (int m = 0; m < MPWQ; ++m) {
+            const int loc = (w + NW * m) * 16 + lc, gcol = gcb_sa(g)(m) * 16 + lc;
+            const float bq = raw[lo.b_qkv + gcol];
 #pragma unroll
-              for (int rb = 0; rb < RB; ++rb)
+            for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-                for (int i = 0; i < 4; ++i) ybuf[(rb * 16 + lq * 4 + i) * LDY + loc] = y[m][rb][i] + bq;
-            }
-            __syncthreads();
-            // scores and softmax: one lane per (sample, head, query, key)
-            constexpr int NIT = SPT * HG * HZ * HZ;
-            for (int base = 0; base < NIT; base += NT) {
-              const int it = base + tid;
-              const bool valid = it < NIT;
-              const int kk = it % HZ, qi = (it / HZ) % HZ, hh = (it / (HZ * HZ)) % HG, j = it / (HZ * HZ * HG);
-              const bool live = valid && kk <= qi;
-              float s = -INFINITY;
-              if (live) {
-                const float* qp = ybuf + (j * HZ + qi) * LDY + hh * DH;
-                const float* kp = ybuf + (j * HZ + kk) * LDY + GW + hh * DH;
-                float acc = 0.f;
+              for (int i = 0; i < 4; ++i) ybuf[(rb * 16 + lq * 4 + i) * LDY + loc] = y[m][rb][i] + bq;
+          }
+          __syncthreads();
+          // scores, softmax and values on fp32 MFMA tiles: wave per (head, query block)
+          for (int pr = w; pr < HG * RB; pr += NW) {
+            const int hh = pr % HG, ib = pr / HG;
+            const int jb0 = (HZ >= 16) ? ((ib * 16) / HZ) * (HZ / 16) : ib;
+            f32x4 s[NJB];
 #pragma unroll
-                for (int cc = 0; cc < DH; cc += 4) {
-                  const float4 a4 = *reinterpret_cast<const float4*>(qp + cc);
-                  const float4 b4 = *reinterpret_cast<const float4*>(kp + cc);
-                  acc += a4.x * b4.x + a4.y * b4.y + a4.z * b4.z + a4.w * b4.w;
-                }
-                s = acc * kScale;
+            for (int jj = 0; jj < NJB; ++jj) {
+              s[jj] = f32x4{0.f, 0.f, 0.f, 0.f};
+              const int jb = jb0 + jj;
+              if (jb <= ib) {
+                const float* qp = ybuf + (ib * 16 + lc) * LDY + hh * DH + lq;
+                const float* kp = ybuf + (jb * 16 + lc) * LDY + GW + hh * DH + lq;
+#pragma unroll
+                for (int kk = 0; kk < DH / 4; ++kk) s[jj] = mfma4(qp[4 * kk], kp[4 * kk], s[jj]);
               }
-              float mx = s;
-#pragma unroll
-              for (int off = HZ / 2; off >= 1; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
-              const float e = live ? expf(s - mx) : 0.f;
-              float sum = e;
-#pragma unroll
-              for (int off = HZ / 2; off >= 1; off >>= 1) sum += __shfl_xor(sum, off);
-              if (valid) pbuf[it] = e / sum;
             }
-            __syncthreads();
-            constexpr int NIT2 = SPT * HG * HZ * DH;
-            for (int it = tid; it < NIT2; it += NT) {
-              const int cc = it % DH, qi = (it / DH) % HZ, hh = (it / (DH * HZ)) % HG, j = it / (DH * HZ * HG);
-              const float* pr = pbuf + ((j * HG + hh) * HZ + qi) * HZ;
-              const float* vp = ybuf + (j * HZ) * LDY + 2 * GW + hh * DH + cc;
-              float o = 0.f;
-              for (int kk = 0; kk <= qi; ++kk) o += pr[kk] * vp[kk * LDY];
-              O::store(zbuf, LDZ, j * HZ + qi, hh * DH + cc, o);
+            float sm[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const int gi = ib * 16 + lq * 4 + i;
+              float m = -INFINITY;
+#pragma unroll
+              for (int jj = 0; jj < NJB; ++jj) {
+                const int gj = (jb0 + jj) * 16 + lc;
+                const bool ok = (gj <= gi) && (gj / HZ == gi / HZ);
+                s[jj][i] = ok ? s[jj][i] * kScale : -INFINITY;
+                m = fmaxf(m, s[jj][i]);
+              }
+#pragma unroll
+              for (int off = 1; off < 16; off <<= 1) m = fmaxf(m, __shfl_xor(m, off));
+              float su = 0.f;
+#pragma unroll
+              for (int jj = 0; jj < NJB; ++jj) {
+                const float ev = (s[jj][i] == -INFINITY) ? 0.f : expf(s[jj][i] - m);
+                s[jj][i] = ev;
+                su += ev;
+              }
+#pragma unroll
+              for (int off = 1; off < 16; off <<= 1) su += __shfl_xor(su, off);
+              sm[i] = su;
             }
-            __syncthreads();
-            gemm_acc<AT, RB, CBW, GW / O::KF>(r, zbuf, LDZ, p.pk + po.o, D / O::KF, g * (GW / O::KF), own, lane);
-          }
+            float* sc = pw + w * PWN;
 #pragma unroll
-          for (int c = 0; c < CBW; ++c) {
-            const float bo = raw[lo.b_o + (w * CBW + c) * 16 + lc];
+            for (int jj = 0; jj < NJB; ++jj)
 #pragma unroll
-            for (int rb = 0; rb < RB; ++rb) r[c][rb] += bo;
-          }
-        } else if (u == 1) {
-          // ---------------- cross-attention unit (time token + observation tokens)
-          for (int g = 0; g < NH / HG; ++g) {
-            for (int it = tid; it < SPT * S * 2 * GW; it += NT) {
-              const int col = it % (2 * GW), sm = (it / (2 * GW)) % S, j = it / (2 * GW * S);
-              const int gcol = col < GW ? g * GW + col : D + g * GW + (col - GW);
-              float v = 0.f;
-              if (smp[j] >= 0)
-                v = sm == 0 ? p.tkv[((size_t)k * L + l) * (2 * D) + gcol]
-                            : p.okv[(((size_t)smp[j] * L + l) * nobs + (sm - 1)) * (2 * D) + gcol];
-              kvbuf[(j * SMAX + sm) * (2 * GW) + col] = v;
-            }
-            constexpr int MPW1 = (GW / 16) / NW;
-            const auto gcb = [&](int m) { return g * (GW / 16) + w + NW * m; };
-            f32x4 y[MPW1][RB];
+              for (int i = 0; i < 4; ++i) sc[(jj * 16 + lq * 4 + i) * PS + lc] = s[jj][i] / sm[i];
+            wave_lds_sync();
 #pragma unroll
-            for (int m = 0; m < MPW1; ++m)
+            for (int cb = 0; cb < DH / 16; ++cb) {
+              f32x4 o = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-              for (int rb = 0; rb < RB; ++rb) y[m][rb] = f32x4{0.f, 0.f, 0.f, 0.f};
-            gemm_acc<AT, RB, MPW1, D / O::KF>(y, xa, LDA, p.pk + po.q, D / O::KF, 0, gcb, lane);
+              for (int jj = 0; jj < NJB; ++jj) {
+                const int jb = jb0 + jj;
+                if (jb <= ib) {
 #pragma unroll
-            for (int m = 0; m < MPW1; ++m) {
-              const int loc = (w + NW * m) * 16 + lc, gcol = gcb(m) * 16 + lc;
-              const float bq = raw[lo.b_q + gcol];
-#pragma unroll
-              for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) ybuf[(rb * 16 + lq * 4 + i) * LDY + loc] = y[m][rb][i] + bq;
-            }
-            __syncthreads();
-            for (int it = tid; it < SPT * HG * HZ; it += NT) {
-              const int qi = it % HZ, hh = (it / HZ) % HG, j = it / (HZ * HG);
-              const float* qp = ybuf + (j * HZ + qi) * LDY + hh * DH;
-              float sc[SMAX];
-              float mx = -INFINITY;
-#pragma unroll
-              for (int sm = 0; sm < SMAX; ++sm) {
-                sc[sm] = -INFINITY;
-                if (sm < S) {
-                  const float* kp = kvbuf + (j * SMAX + sm) * (2 * GW) + hh * DH;
-                  float acc = 0.f;
-#pragma unroll
-                  for (int cc = 0; cc < DH; cc += 4) {
-                    const float4 a4 = *reinterpret_cast<const float4*>(qp + cc);
-                    const float4 b4 = *reinterpret_cast<const float4*>(kp + cc);
-                    acc += a4.x * b4.x + a4.y * b4.y + a4.z * b4.z + a4.w * b4.w;
+                  for (int kk = 0; kk < 4; ++kk) {
+                    const float a = sc[(jj * 16 + lc) * PS + 4 * kk + lq];
+                    const float v = ybuf[(jb * 16 + 4 * kk + lq) * LDY + 2 * GW + hh * DH + cb * 16 + lc];
+                    o = mfma4(a, v, o);
                   }
-                  sc[sm] = acc * kScale;
-                  mx = fmaxf(mx, sc[sm]);
                 }
               }
-              float sum = 0.f;
 #pragma unroll
-              for (int sm = 0; sm < SMAX; ++sm) {
-                const float e = sm < S ? expf(sc[sm] - mx) : 0.f;
-                sc[sm] = e;
-                sum += e;
+              for (int i = 0; i < 4; ++i) O::store(zbuf, LDZ, ib * 16 + lq * 4 + i, hh * DH + cb * 16 + lc, o[i]);
+            }
+            wave_lds_sync();
+          }
+          __syncthreads();
+          gemm_run<AT, RB, CBW, GW / O::KF>(r, zbuf, LDZ, pk + po.o, D / O::KF, g * (GW / O::KF), own, lane, b2);
+        }
+      } else if (u == 1) {
+        // ---------------- cross-attention unit (time token + observation tokens)
+        uint4 b1c[MPWC];
+        gemm_pref<MPWC>(b1c, pk + po.q, D / O::KF, 0, gcb_ca(0), lane);
+        layer_norm_to_xa();
+        for (int g = 0; g < NH / HG; ++g) {
+          for (int it = tid; it < SPT * S * 2 * GW; it += NT) {
+            const int col = it % (2 * GW), sm_ = (it / (2 * GW)) % S, j = it / (2 * GW * S);
+            const int gcol = col < GW ? g * GW + col : D + g * GW + (col - GW);
+            float v = 0.f;
+            if (smp[j] >= 0)
+              v = sm_ == 0 ? p.tkv[((size_t)k * L + l) * (2 * D) + gcol]
+                           : p.okv[(((size_t)smp[j] * L + l) * nobs + (sm_ - 1)) * (2 * D) + gcol];
+            kvbuf[(j * SMAX + sm_) * (2 * GW) + col] = v;
+          }
+          f32x4 y[MPWC][RB];
+#pragma unroll
+          for (int m = 0; m < MPWC; ++m)
+#pragma unroll
+            for (int rb = 0; rb < RB; ++rb) y[m][rb] = f32x4{0.f, 0.f, 0.f, 0.f};
+          if (g > 0) gemm_pref<MPWC>(b1c, pk + po.q, D / O::KF, 0, gcb_ca(g), lane);
+          gemm_run<AT, RB, MPWC, D / O::KF>(y, xa, LDA, pk + po.q, D / O::KF, 0, gcb_ca(g), lane, b1c);
+          uint4 b2[CBW];
+          gemm_pref<CBW>(b2, pk + po.o2, D / O::KF, g * (GW / O::KF), own, lane);
+#pragma unroll
+          for (int m = 0; m < MPWC; ++m) {
+            const int loc = (w + NW * m) * 16 + lc, gcol = gcb_ca(g)(m) * 16 + lc;
+            const float bq = raw[lo.b_q + gcol];
+#pragma unroll
+            for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+              for (int i = 0; i < 4; ++i) ybuf[(rb * 16 + lq * 4 + i) * LDY + loc] = y[m][rb][i] + bq;
+          }
+          __syncthreads();
+          for (int pr = w; pr < HG * RB; pr += NW) {
+            const int hh = pr % HG, ib = pr / HG;
+            const int js0 = (ib * 16) / HZ;  // first sample slot of this row block
+            // memory column n of the tile: sample js0 + n / SLOTS, token n % SLOTS
+            const int jn = js0 + lc / SLOTS, sn = lc % SLOTS;
+            const bool nok = sn < S && jn < SPT;
+            f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f};
+            {
+              const float* qp = ybuf + (ib * 16 + lc) * LDY + hh * DH + lq;
+              const float* kp = kvbuf + ((nok ? jn : 0) * SMAX + (nok ? sn : 0)) * (2 * GW) + hh * DH + lq;
+#pragma unroll
+              for (int kk = 0; kk < DH / 4; ++kk) s = mfma4(qp[4 * kk], nok ? kp[4 * kk] : 0.f, s);
+            }
+            float sm[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const int gi = ib * 16 + lq * 4 + i;
+              const bool ok = nok && (jn == gi / HZ);
+              const float v = ok ? s[i] * kScale : -INFINITY;
+              float m = v;
+#pragma unroll
+              for (int off = 1; off < 16; off <<= 1) m = fmaxf(m, __shfl_xor(m, off));
+              const float ev = ok ? expf(v - m) : 0.f;
+              float su = ev;
+#pragma unroll
+              for (int off = 1; off < 16; off <<= 1) su += __shfl_xor(su, off);
+              s[i] = ev;
+              sm[i] = su;
+            }
+            float* sc = pw + w * PWN;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) sc[(lq * 4 + i) * PS + lc] = s[i] / sm[i];
+            wave_lds_sync();
+#pragma unroll
+            for (int cb = 0; cb < DH / 16; ++cb) {
+              f32x4 o = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+              for (int kk = 0; kk < 4; ++kk) {
+                const int n = 4 * kk + lq, jv = js0 + n / SLOTS, sv = n % SLOTS;
+                const bool vok = sv < S && jv < SPT;
+                const float a = sc[lc * PS + n];
+                const float v = vok ? kvbuf[(jv * SMAX + sv) * (2 * GW) + GW + hh * DH + cb * 16 + lc] : 0.f;
+                o = mfma4(a, v, o);
               }
 #pragma unroll
-              for (int sm = 0; sm < SMAX; ++sm) pbuf[it * SMAX + sm] = sc[sm] / sum;
+              for (int i = 0; i < 4; ++i) O::store(zbuf, LDZ, ib * 16 + lq * 4 + i, hh * DH + cb * 16 + lc, o[i]);
             }
-            __syncthreads();
-            constexpr int NIT2 = SPT * HG * HZ * DH;
-            for (int it = tid; it < NIT2; it += NT) {
-              const int cc = it % DH, qi = (it / DH) % HZ, hh = (it / (DH * HZ)) % HG, j = it / (DH * HZ * HG);
-              const float* pr = pbuf + ((j * HG + hh) * HZ + qi) * SMAX;
-              float o = 0.f;
-              for (int sm = 0; sm < S; ++sm) o += pr[sm] * kvbuf[(j * SMAX + sm) * (2 * GW) + GW + hh * DH + cc];
-              O::store(zbuf, LDZ, j * HZ + qi, hh * DH + cc, o);
-            }
-            __syncthreads();
-            gemm_acc<AT, RB, CBW, GW / O::KF>(r, zbuf, LDZ, p.pk + po.o2, D / O::KF, g * (GW / O::KF), own, lane);
+            wave_lds_sync();
           }
+          __syncthreads();
+          gemm_run<AT, RB, CBW, GW / O::KF>(r, zbuf, LDZ, pk + po.o2, D / O::KF, g * (GW / O::KF), own, lane, b2);
+        }
+      } else {
+        // ---------------- feed-forward unit, d_ff streamed in chunks of FC
+        uint4 b1f[MPWF];
+        gemm_pref<MPWF>(b1f, pk + po.w1, D / O::KF, 0, gcb_ff(0), lane);
+        layer_norm_to_xa();
+        for (int ch = 0; ch < DFF / FC; ++ch) {
+          f32x4 y[MPWF][RB];
 #pragma unroll
-          for (int c = 0; c < CBW; ++c) {
-            const float bo = raw[lo.b_o2 + (w * CBW + c) * 16 + lc];
+          for (int m = 0; m < MPWF; ++m)
 #pragma unroll
-            for (int rb = 0; rb < RB; ++rb) r[c][rb] += bo;
+            for (int rb = 0; rb < RB; ++rb) y[m][rb] = f32x4{0.f, 0.f, 0.f, 0.f};
+          if (ch > 0) gemm_pref<MPWF>(b1f, pk + po.w1, D / O::KF, 0, gcb_ff(ch), lane);
+          gemm_run<AT, RB, MPWF, D / O::KF>(y, xa, LDA, pk + po.w1, D / O::KF, 0, gcb_ff(ch), lane, b1f);
+          uint4 b2[CBW];
+          gemm_pref<CBW>(b2, pk + po.w2, DFF / O::KF, ch * (FC / O::KF), own, lane);
+#pragma unroll
+          for (int m = 0; m < MPWF; ++m) {
+            const int loc = (w + NW * m) * 16 + lc;
+            const float b1 = raw[lo.b_1 + ch * FC + loc];
+#pragma unroll
+            for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+              for (int i = 0; i < 4; ++i)
+                O::store(zbuf, LDZ, rb * 16 + lq * 4 + i, loc, gelu_erf(y[m][rb][i] + b1));
           }
-        } else {
-          // ---------------- feed-forward unit, d_ff streamed in chunks of FC
-          for (int ch = 0; ch < DFF / FC; ++ch) {
-            constexpr int MPW1 = (FC / 16) / NW;
-            const auto gcb = [&](int m) { return ch * (FC / 16) + w + NW * m; };
-            f32x4 y[MPW1][RB];
-#pragma unroll
-            for (int m = 0; m < MPW1; ++m)
-#pragma unroll
-              for (int rb = 0; rb < RB; ++rb) y[m][rb] = f32x4{0.f, 0.f, 0.f, 0.f};
-            gemm_acc<AT, RB, MPW1, D / O::KF>(y, xa, LDA, p.pk + po.w1, D / O::KF, 0, gcb, lane);
-#pragma unroll
-            for (int m = 0; m < MPW1; ++m) {
-              const int loc = (w + NW * m) * 16 + lc;
-              const float b1 = raw[lo.b_1 + ch * FC + loc];
-#pragma unroll
-              for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
-                  O::store(zbuf, LDZ, rb * 16 + lq * 4 + i, loc, gelu_erf(y[m][rb][i] + b1));
-            }
-            __syncthreads();
-            gemm_acc<AT, RB, CBW, FC / O::KF>(r, zbuf, LDZ, p.pk + po.w2, DFF / O::KF, ch * (FC / O::KF), own, lane);
-            __syncthreads();
-          }
-#pragma unroll
-          for (int c = 0; c < CBW; ++c) {
-            const float b2 = raw[lo.b_2 + (w * CBW + c) * 16 + lc];
-#pragma unroll
-            for (int rb = 0; rb < RB; ++rb) r[c][rb] += b2;
-          }
+          __syncthreads();
+          gemm_run<AT, RB, CBW, FC / O::KF>(r, zbuf, LDZ, pk + po.w2, DFF / O::KF, ch * (FC / O::KF), own, lane, b2);
+          __syncthreads();
         }
       }
-      // Eq. 1 per sample: evaluated residual (and cache refresh) or the
-      // residual cached at the unit's most recent refresh.
-      float* cunit = cbase + (size_t)b * (R * D);
+#pragma unroll
+      for (int c = 0; c < CBW; ++c)
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) r[c][rb] += rbias[c];
+
+      // Eq. 1 per sample at unit e: evaluated residual (and cache refresh) or
+      // the residual cached at the unit's most recent refresh.
 #pragma unroll
       for (int c = 0; c < CBW; ++c)
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb) {
-          const int j = (rb * 16 + lq * 4) / HZ;
-          uint8_t cd = code[0];
+          const int j = jrow[rb];
+          const uint64_t bit = 1ull << e;
+          bool mg = mmg[0];
 #pragma unroll
           for (int jj = 1; jj < SPT; ++jj)
-            if (j == jj) cd = code[jj];
-          f32x4* cp = reinterpret_cast<f32x4*>(cunit + ((size_t)((w * RB + rb) * CBW + c) * 64 + lane) * 4);
-          if (cd & C_EVAL) {
+            if (j == jj) mg = mmg[jj];
+          if (pick(mev, j) & bit) {
             const f32x4 v = r[c][rb];
-            if (cd & C_MERGED) mac[c][rb] = (u == 0) ? v : mac[c][rb] + v;
-            if (cd & C_STORE) *cp = (cd & C_MERGED) ? mac[c][rb] : v;
+            if (mg) mac[c][rb] = (u == 0) ? v : mac[c][rb] + v;
+            if (pick(mst, j) & bit) *cfrag(e, c, rb) = mg ? mac[c][rb] : v;
             h[c][rb] += v;
-          } else if (cd & C_REUSE) {
-            h[c][rb] += *cp;
+          } else if (pick(mru, j) & bit) {
+            h[c][rb] += *cfrag(e, c, rb);
           }
         }
+      b = e + 1;
     }
 
-    // ---- head (final LayerNorm + linear, predicts epsilon) and DDPM update
+    // ---- head (final LayerNorm + linear on fp32 MFMA) and DDPM update
     {
       float mu[RB][4], rs[RB][4];
-      row_stats<C>(h, red, mu, rs, w, lc, lq);
-      f32x4 nrm[CBW][RB];
+      ln_stats<C>(h, red, mu, rs, w, lc, lq);
+      f32x4 eacc[RB];
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) eacc[rb] = f32x4{0.f, 0.f, 0.f, 0.f};
+      float* sc = pw + w * PWN;
 #pragma unroll
       for (int c = 0; c < CBW; ++c) {
-        const int col = (w * CBW + c) * 16 + lc;
-        const float g = raw[p.lnf_g + col], bb = raw[p.lnf_b + col];
+        float g_, b_;
+        if constexpr (KEEP_EMB) {
+          g_ = lfg[c];
+          b_ = lfb[c];
+        } else {
+          const int col = (w * CBW + c) * 16 + lc;
+          g_ = raw[p.lnf_g + col];
+          b_ = raw[p.lnf_b + col];
+        }
+        const uint4 wo = pk[p.pk_wout + (size_t)(w * CBW + c) * 64 + lane];
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-          for (int i = 0; i < 4; ++i) nrm[c][rb][i] = (h[c][rb][i] - mu[rb][i]) * rs[rb][i] * g + bb;
+          for (int i = 0; i < 4; ++i)
+            sc[(rb * 16 + lq * 4 + i) * PS + lc] = (h[c][rb][i] - mu[rb][i]) * rs[rb][i] * g_ + b_;
+        wave_lds_sync();
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) {
+          const float* ar = sc + (rb * 16 + lc) * PS + lq;
+          eacc[rb] = mfma4(ar[0], __uint_as_float(wo.x), eacc[rb]);
+          eacc[rb] = mfma4(ar[4], __uint_as_float(wo.y), eacc[rb]);
+          eacc[rb] = mfma4(ar[8], __uint_as_float(wo.z), eacc[rb]);
+          eacc[rb] = mfma4(ar[12], __uint_as_float(wo.w), eacc[rb]);
+        }
+        wave_lds_sync();
       }
-      float* epsp = ybuf;  // [NW][R][AMAX] partial dot products
-      for (int a = 0; a < A; ++a) {
-        float wo[CBW];
+      float* epsp = ybuf;  // [NW][R][16] partial products of this wave's columns
 #pragma unroll
-        for (int c = 0; c < CBW; ++c) wo[c] = raw[p.W_out + (size_t)a * D + (w * CBW + c) * 16 + lc];
+      for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-        for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            float v = 0.f;
-#pragma unroll
-            for (int c = 0; c < CBW; ++c) v += nrm[c][rb][i] * wo[c];
-#pragma unroll
-            for (int off = 1; off < 16; off <<= 1) v += __shfl_xor(v, off);
-            if (lc == 0) epsp[(w * R + rb * 16 + lq * 4 + i) * AMAX + a] = v;
-          }
-      }
+        for (int i = 0; i < 4; ++i) epsp[(w * R + rb * 16 + lq * 4 + i) * 16 + lc] = eacc[rb][i];
       __syncthreads();
       const float* dd = p.ddpm + (size_t)k * 8;
       const float s1 = dd[0], sa = dd[1], c0 = dd[2], ct = dd[3], sg = dd[4];
@@ -616,17 +809,17 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
         const int it = tid + q * NT;
         if (it < R * A) {
           const int row = it / A, a = it % A;
-          float e = raw[p.b_out + a];
           float part = 0.f;
 #pragma unroll
-          for (int ww = 0; ww < NW; ++ww) part += epsp[(ww * R + row) * AMAX + a];
-          e += part;
-          const float x = xs[row * AMAX + a];
+          for (int ww = 0; ww < NW; ++ww) part += epsp[(ww * R + row) * 16 + a];
+          const float e = raw[p.b_out + a] + part;
+          float* xp = xs + row * 16 + OF::pcol(a);
+          const float x = *xp;
           float x0 = (x - s1 * e) / sa;
           if (p.clip) x0 = fminf(fmaxf(x0, -1.f), 1.f);
           float xn = c0 * x0 + ct * x;
           if (k > 0) xn += sg * zpre[q];
-          xs[row * AMAX + a] = xn;
+          *xp = xn;
           if (t == T - 1) {
             const int s = smp[row / HZ];
             if (s >= 0) p.out[((size_t)s * HZ + (row % HZ)) * A + a] = xn;
@@ -639,7 +832,7 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
 }
 
 // ---------------------------------------------------------------- creation
-__global__ void pack_kernel(const float* __restrict__ raw, size_t off, int N, int K, int Kpad, int bf,
+__global__ void pack_kernel(const float* __restrict__ raw, size_t off, int N, int Nvalid, int K, int Kpad, int bf,
                             uint4* __restrict__ dst) {
   const int KF = bf ? 32 : 16;
   const int KBT = Kpad / KF;
@@ -650,19 +843,21 @@ __global__ void pack_kernel(const float* __restrict__ raw, size_t off, int N, in
   const size_t fr = gid / 64;
   const int kb = (int)(fr % KBT), nb = (int)(fr / KBT);
   const int n = nb * 16 + (lane & 15), q = lane >> 4;
-  const float* W = raw + off + (size_t)n * K;
-  uint32_t e[4];
-  if (bf) {
-    for (int i = 0; i < 4; ++i) {
-      const int k0 = kb * 32 + q * 8 + 2 * i;
-      const uint32_t lo = k0 < K ? bf16_rne(W[k0]) : 0u;
-      const uint32_t hi = k0 + 1 < K ? bf16_rne(W[k0 + 1]) : 0u;
-      e[i] = lo | (hi << 16);
-    }
-  } else {
-    for (int j = 0; j < 4; ++j) {
-      const int kk = kb * 16 + 4 * j + q;
-      e[j] = kk < K ? __float_as_uint(W[kk]) : 0u;
+  uint32_t e[4] = {0u, 0u, 0u, 0u};
+  if (n < Nvalid) {
+    const float* W = raw + off + (size_t)n * K;
+    if (bf) {
+      for (int i = 0; i < 4; ++i) {
+        const int k0 = kb * 32 + q * 8 + 2 * i;
+        const uint32_t lo = k0 < K ? bf16_rne(W[k0]) : 0u;
+        const uint32_t hi = k0 + 1 < K ? bf16_rne(W[k0 + 1]) : 0u;
+        e[i] = lo | (hi << 16);
+      }
+    } else {
+      for (int j = 0; j < 4; ++j) {
+        const int kk = kb * 16 + 4 * j + q;
+        e[j] = kk < K ? __float_as_uint(W[kk]) : 0u;
+      }
     }
   }
   dst[gid] = make_uint4(e[0], e[1], e[2], e[3]);
@@ -728,19 +923,18 @@ __global__ void ddpm_kernel(int T, float* tab) {
   }
 }
 
-hipError_t launch_pack(const float* raw, size_t off, int N, int K, int Kpad, int dtype, uint4* dst,
+hipError_t launch_pack(const float* raw, size_t off, int N, int Nvalid, int K, int Kpad, int dtype, uint4* dst,
                        hipStream_t stream) {
   const int KF = dtype == 1 ? 32 : 16;
   const size_t n = (size_t)(N / 16) * (Kpad / KF) * 64;
   const int bs = 256;
-  hipLaunchKernelGGL(pack_kernel, dim3((unsigned)((n + bs - 1) / bs)), dim3(bs), 0, stream, raw, off, N, K,
-                     Kpad, dtype == 1 ? 1 : 0, dst);
+  hipLaunchKernelGGL(pack_kernel, dim3((unsigned)((n + bs - 1) / bs)), dim3(bs), 0, stream, raw, off, N, Nvalid,
+                     K, Kpad, dtype == 1 ? 1 : 0, dst);
   return hipGetLastError();
 }
 
-hipError_t launch_time_kv(const float* raw, uint32_t pmem0, const uint32_t* wkv, const uint32_t* bkv,
-                          int T, int L, int D, int dtype, float* rows_scratch, float* tkv,
-                          hipStream_t stream) {
+hipError_t launch_time_kv(const float* raw, uint32_t pmem0, const uint32_t* wkv, const uint32_t* bkv, int T, int L,
+                          int D, int dtype, float* rows_scratch, float* tkv, hipStream_t stream) {
   const int bs = 256;
   hipLaunchKernelGGL(time_row_kernel, dim3((T * D + bs - 1) / bs), dim3(bs), 0, stream, raw, pmem0, T, D,
                      rows_scratch);
@@ -767,12 +961,15 @@ hipError_t launch_ddpm_table(int T, float* table, hipStream_t stream) {
 
 template <class AT> constexpr int dtype_of() { return std::is_same<AT, float>::value ? 0 : 1; }
 
+#define EVO_MATCH(AT, D, DH, HZ, SPT, DFF)                                                                 \
+  (key.d == D && key.dh == DH && key.horizon == HZ && key.d_ff == DFF && key.dtype == dtype_of<AT>() && \
+   key.spt == SPT)
+
 bool kernel_available(const KernelKey& key, int* threads) {
-#define X(AT, D, DH, HZ, SPT, DFF, NW, HG, FC, SMAX)                                                     \
-  if (key.d == D && key.dh == DH && key.horizon == HZ && key.d_ff == DFF && key.dtype == dtype_of<AT>() && \
-      key.spt == SPT) {                                                                                  \
-    if (threads) *threads = NW * 64;                                                                     \
-    return true;                                                                                         \
+#define X(AT, D, DH, HZ, SPT, DFF, NW, HG, FC, SMAX) \
+  if (EVO_MATCH(AT, D, DH, HZ, SPT, DFF)) {          \
+    if (threads) *threads = NW * 64;                 \
+    return true;                                     \
   }
   EVO_SHAPES(X)
 #undef X
@@ -780,10 +977,8 @@ bool kernel_available(const KernelKey& key, int* threads) {
 }
 
 int kernel_max_obs_tokens_for(const KernelKey& key) {
-#define X(AT, D, DH, HZ, SPT, DFF, NW, HG, FC, SMAX)                                                     \
-  if (key.d == D && key.dh == DH && key.horizon == HZ && key.d_ff == DFF && key.dtype == dtype_of<AT>() && \
-      key.spt == SPT)                                                                                    \
-    return (SMAX - 1) < 16 / SPT ? (SMAX - 1) : 16 / SPT;
+#define X(AT, D, DH, HZ, SPT, DFF, NW, HG, FC, SMAX) \
+  if (EVO_MATCH(AT, D, DH, HZ, SPT, DFF)) return (SMAX - 1) < 16 / SPT ? (SMAX - 1) : 16 / SPT;
   EVO_SHAPES(X)
 #undef X
   return 0;
@@ -791,13 +986,14 @@ int kernel_max_obs_tokens_for(const KernelKey& key) {
 
 int kernel_max_action_dim() { return 16; }
 
+int kernel_max_steps_x_spt() { return kMaskEntries; }
+
 hipError_t launch_denoise(const KernelKey& key, const KParams& p, hipStream_t stream) {
-#define X(AT, D, DH, HZ, SPT, DFF, NW, HG, FC, SMAX)                                                     \
-  if (key.d == D && key.dh == DH && key.horizon == HZ && key.d_ff == DFF && key.dtype == dtype_of<AT>() && \
-      key.spt == SPT) {                                                                                  \
+#define X(AT, D, DH, HZ, SPT, DFF, NW, HG, FC, SMAX)                                                      \
+  if (EVO_MATCH(AT, D, DH, HZ, SPT, DFF)) {                                                               \
     hipLaunchKernelGGL((denoise_kernel<AT, D, DH, HZ, SPT, DFF, NW, HG, FC, SMAX>), dim3(p.n_tiles),      \
-                       dim3(NW * 64), 0, stream, p);                                                     \
-    return hipGetLastError();                                                                            \
+                       dim3(NW * 64), 0, stream, p);                                                      \
+    return hipGetLastError();                                                                             \
   }
   EVO_SHAPES(X)
 #undef X

@@ -24,12 +24,14 @@ struct KParams {
   const LayerOff* loff;      // [L]
   const PackOff* poff;       // [L]
   uint64_t pk_obs;           // fragment offset of W_obs (K padded to obs_pad)
+  uint64_t pk_win;           // fp32 fragments of W_in (K = action_dim padded to 16)
+  uint64_t pk_wout;          // fp32 fragments of W_out (rows padded to 16)
   uint32_t W_in, b_in, P_act, b_obs, P_mem, lnf_g, lnf_b, W_out, b_out, pad_;
   const float* tkv;          // [T][L][2d] time-token keys/values, indexed by timestep k
   const float* ddpm;         // [T][8] sampler constants, indexed by timestep k
   const int32_t* tile_sample;  // [n_tiles][spt] sample index or -1
   const int32_t* tile_slot;    // [n_tiles][spt] schedule slot
-  const uint8_t* codes;        // [slots][3L][T]
+  const uint64_t* masks;       // [slots][T][3] unit bitmasks {evaluate(+merged bit 63), reuse, store}
   const float* obs;          // [batch][n_obs][obs_dim]
   const float* noise;        // [T][batch][H][A]
   float* out;                // [batch][H][A]
@@ -52,8 +54,12 @@ int kernel_max_obs_tokens_for(const KernelKey& key);
 hipError_t launch_denoise(const KernelKey& key, const KParams& p, hipStream_t stream);
 
 // Creation-time kernels.
-hipError_t launch_pack(const float* raw, size_t off, int N, int K, int Kpad, int dtype,
+// Pack rows [0, N) of the [Nvalid][K] matrix at raw + off into MFMA
+// fragments (rows >= Nvalid and columns >= K are zero); dtype 1 = bf16.
+hipError_t launch_pack(const float* raw, size_t off, int N, int Nvalid, int K, int Kpad, int dtype,
                        uint4* dst, hipStream_t stream);
+// Largest T * samples-per-tile the kernels accept (schedule masks live in LDS).
+int kernel_max_steps_x_spt();
 // Time-token keys/values tkv[T][L][2d]; wkv/bkv: device arrays of the
 // layers' W_kv / b_kv float offsets; rows_scratch: device float[T][d].
 hipError_t launch_time_kv(const float* raw, uint32_t pmem0, const uint32_t* wkv, const uint32_t* bkv,

@@ -56,6 +56,10 @@ def lib() -> ctypes.CDLL:
     if _lib is None:
         if not os.path.exists(LIB_PATH):
             raise RuntimeError(f"{LIB_PATH} is not built: run __graft_entry__.build()")
+        # torch ships its own HIP runtime; loading it first makes the library
+        # bind to that same runtime (one HIP runtime per process), so torch
+        # tensors and streams are valid in the library's calls.
+        import torch  # noqa: F401
         L = ctypes.CDLL(LIB_PATH)
         P, I32, U64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_uint64
         L.evo_weight_count.argtypes = [ctypes.POINTER(PolicyDesc)]
