@@ -36,6 +36,7 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr uint64_t kMergedBit = 1ull << 63;
 constexpr int kMaskEntries = 341;  // (T x samples per tile) entries of 3 x u64 in LDS (8 KiB)
+constexpr int kMaxLayers = 21;     // 3L <= 63 units (one 64-bit mask per step)
 
 // float -> bfloat16 bits, round to nearest even (finite inputs)
 __device__ __forceinline__ uint32_t bf16_rne(float f) {
@@ -46,6 +47,29 @@ __device__ __forceinline__ uint32_t bf16_rne(float f) {
 
 __device__ __forceinline__ f32x4 mfma4(float a, float b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
+// Cross-lane moves within a row of 16 lanes (DPP): swap neighbours, swap
+// pairs, mirror within 8, mirror within 16.  Each pairs every lane with a
+// lane of the other half of its group, so four steps combine all 16 lanes
+// and every lane ends with the same value.
+template <int CTRL>
+__device__ __forceinline__ float dpp_mov(float v) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xF, 0xF, true));
+}
+__device__ __forceinline__ float row16_sum(float v) {
+  v += dpp_mov<0xB1>(v);
+  v += dpp_mov<0x4E>(v);
+  v += dpp_mov<0x141>(v);
+  v += dpp_mov<0x140>(v);
+  return v;
+}
+__device__ __forceinline__ float row16_max(float v) {
+  v = fmaxf(v, dpp_mov<0xB1>(v));
+  v = fmaxf(v, dpp_mov<0x4E>(v));
+  v = fmaxf(v, dpp_mov<0x141>(v));
+  v = fmaxf(v, dpp_mov<0x140>(v));
+  return v;
 }
 
 // Orders a wave's own LDS writes before its following LDS reads (other
@@ -191,15 +215,19 @@ __device__ __forceinline__ void ln_stats(const f32x4 (&h)[C::CBW][C::RB], float 
         const float e = h[c][rb][i] - m;
         q += e * e;
       }
+      // merge equal-count groups pairwise: mean of the two means, M2 sum
+      // plus the spread term (symmetric, so both partners agree bitwise)
       float n = (float)C::CBW;
-#pragma unroll
-      for (int off = 1; off < 16; off <<= 1) {
-        const float mo = __shfl_xor(m, off), qo = __shfl_xor(q, off);
+      const auto merge = [&](float mo, float qo) {
         const float d = mo - m;
         m = 0.5f * (m + mo);
         q = q + qo + d * d * (0.5f * n);
         n *= 2.f;
-      }
+      };
+      merge(dpp_mov<0xB1>(m), dpp_mov<0xB1>(q));
+      merge(dpp_mov<0x4E>(m), dpp_mov<0x4E>(q));
+      merge(dpp_mov<0x141>(m), dpp_mov<0x141>(q));
+      merge(dpp_mov<0x140>(m), dpp_mov<0x140>(q));
       if (lc == 0) {
         red[w][rb * 16 + lq * 4 + i][0] = m;
         red[w][rb * 16 + lq * 4 + i][1] = q;
@@ -253,6 +281,8 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
   __shared__ float red[NW][R][2];
   __shared__ __attribute__((aligned(16))) float xs[R * 16];
   __shared__ uint64_t msk[kMaskEntries * 3];
+  __shared__ LayerOff s_loff[kMaxLayers];
+  __shared__ PackOff s_poff[kMaxLayers];
   __shared__ int smp[SPT];
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, lc = lane & 15, lq = lane >> 4;
@@ -261,6 +291,10 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
   const float* raw = p.raw;
 
   if (tid < SPT) smp[tid] = p.tile_sample[tile * SPT + tid];
+  for (int it = tid; it < L * (int)(sizeof(LayerOff) / 4); it += NT)
+    reinterpret_cast<uint32_t*>(s_loff)[it] = reinterpret_cast<const uint32_t*>(p.loff)[it];
+  for (int it = tid; it < L * (int)(sizeof(PackOff) / 8); it += NT)
+    reinterpret_cast<uint64_t*>(s_poff)[it] = reinterpret_cast<const uint64_t*>(p.poff)[it];
   for (int it = tid; it < SPT * T * 3; it += NT) {
     const int j = it / (T * 3), r = it % (T * 3);
     msk[it] = p.masks[(size_t)p.tile_slot[tile * SPT + j] * T * 3 + r];
@@ -317,9 +351,9 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
       f32x4 kv[MPWK][1];
 #pragma unroll
       for (int m = 0; m < MPWK; ++m) kv[m][0] = f32x4{0.f, 0.f, 0.f, 0.f};
-      gemm_acc<AT, 1, MPWK, D / O::KF>(kv, xa, LDA, p.pk + p.poff[l].kv, D / O::KF, 0,
+      gemm_acc<AT, 1, MPWK, D / O::KF>(kv, xa, LDA, p.pk + s_poff[l].kv, D / O::KF, 0,
                                         [&](int m) { return w + NW * m; }, lane);
-      const uint32_t bkv = p.loff[l].b_kv;
+      const uint32_t bkv = s_loff[l].b_kv;
 #pragma unroll
       for (int m = 0; m < MPWK; ++m) {
         const int gcol = (w + NW * m) * 16 + lc;
@@ -373,6 +407,35 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) mac[c][rb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+  // LayerNorm gain/shift and output bias of the next unit to evaluate, for
+  // this lane's columns (loaded one unit ahead)
+  float nlg[CBW], nlb[CBW], nrb[CBW];
+  int loaded_t = -1, loaded_u = -1;  // (step, unit) the prefetched parameters belong to
+  const auto load_unit_params = [&](int tt, int unit) {
+    loaded_t = tt;
+    loaded_u = unit;
+    const int ul = unit / 3, uu = unit - 3 * ul;
+    const LayerOff& q = s_loff[ul];
+    const uint32_t go = uu == 0 ? q.ln1_g : (uu == 1 ? q.ln2_g : q.ln3_g);
+    const uint32_t bo = uu == 0 ? q.ln1_b : (uu == 1 ? q.ln2_b : q.ln3_b);
+    const uint32_t ro = uu == 0 ? q.b_o : (uu == 1 ? q.b_o2 : q.b_2);
+#pragma unroll
+    for (int c = 0; c < CBW; ++c) {
+      const int col = (w * CBW + c) * 16 + lc;
+      nlg[c] = raw[go + col];
+      nlb[c] = raw[bo + col];
+      nrb[c] = raw[ro + col];
+    }
+  };
+  // first unit any sample of the tile evaluates at step tt (U if none)
+  const auto first_eval = [&](int tt) {
+    uint64_t m = 0;
+#pragma unroll
+    for (int j = 0; j < SPT; ++j)
+      if (smp[j] >= 0) m |= msk[(j * T + tt) * 3 + 0] & ~kMergedBit;
+    return m ? __builtin_ctzll(m) : U;
+  };
+
   constexpr int ZPT = (R * 16 + NT - 1) / NT;
   constexpr int MPWQ = (3 * GW / 16) / NW, MPWC = (GW / 16) / NW, MPWF = (FC / 16) / NW;
 
@@ -410,6 +473,21 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
         const int row = it / A, a = it % A, s = smp[row / HZ];
         if (s >= 0) zpre[q] = p.noise[(((size_t)(t + 1) * p.batch + s) * HZ + (row % HZ)) * A + a];
       }
+    }
+    // parameters of this step's first evaluated unit, unless the previous
+    // step already requested them
+    {
+      const int f = evT ? __builtin_ctzll(evT) : U;
+      if (f < U && !(loaded_t == t && loaded_u == f)) load_unit_params(t, f);
+    }
+    // sampler constants and head bias of this step's update (prefetched)
+    const float* dd = p.ddpm + (size_t)k * 8;
+    const float s1 = dd[0], sa = dd[1], c0 = dd[2], ct = dd[3], sg = dd[4];
+    float bout[ZPT];
+#pragma unroll
+    for (int q = 0; q < ZPT; ++q) {
+      const int it = tid + q * NT;
+      bout[q] = it < R * A ? raw[p.b_out + it % A] : 0.f;
     }
     // ---- embedding of the current sample on fp32 MFMA: h = (b_in + P_act) + x W_in^T
     {
@@ -477,18 +555,23 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
 
       // ---- evaluate unit e for the tile
       const int l = e / 3, u = e - 3 * l;
-      const LayerOff lo = p.loff[l];
-      const PackOff po = p.poff[l];
-      const uint32_t gofs = u == 0 ? lo.ln1_g : (u == 1 ? lo.ln2_g : lo.ln3_g);
-      const uint32_t bofs = u == 0 ? lo.ln1_b : (u == 1 ? lo.ln2_b : lo.ln3_b);
-      const uint32_t r_bias = u == 0 ? lo.b_o : (u == 1 ? lo.b_o2 : lo.b_2);
+      const LayerOff lo = s_loff[l];
+      const PackOff po = s_poff[l];
       float lg[CBW], lb[CBW], rbias[CBW];
 #pragma unroll
       for (int c = 0; c < CBW; ++c) {
-        const int col = (w * CBW + c) * 16 + lc;
-        lg[c] = raw[gofs + col];
-        lb[c] = raw[bofs + col];
-        rbias[c] = raw[r_bias + col];
+        lg[c] = nlg[c];
+        lb[c] = nlb[c];
+        rbias[c] = nrb[c];
+      }
+      {
+        // request the parameters of the next evaluated unit (this step or the next)
+        const uint64_t later = (e + 1 < 64) ? (evT >> (e + 1)) : 0ull;
+        if (later) load_unit_params(t, e + 1 + __builtin_ctzll(later));
+        else if (t + 1 < T) {
+          const int f = first_eval(t + 1);
+          if (f < U) load_unit_params(t + 1, f);
+        }
       }
       const auto gcb_sa = [&](int g) {
         return [=](int m) {
@@ -573,8 +656,7 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
                 s[jj][i] = ok ? s[jj][i] * kScale : -INFINITY;
                 m = fmaxf(m, s[jj][i]);
               }
-#pragma unroll
-              for (int off = 1; off < 16; off <<= 1) m = fmaxf(m, __shfl_xor(m, off));
+              m = row16_max(m);
               float su = 0.f;
 #pragma unroll
               for (int jj = 0; jj < NJB; ++jj) {
@@ -582,9 +664,7 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
                 s[jj][i] = ev;
                 su += ev;
               }
-#pragma unroll
-              for (int off = 1; off < 16; off <<= 1) su += __shfl_xor(su, off);
-              sm[i] = su;
+              sm[i] = row16_sum(su);
             }
             float* sc = pw + w * PWN;
 #pragma unroll
@@ -621,14 +701,19 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
         gemm_pref<MPWC>(b1c, pk + po.q, D / O::KF, 0, gcb_ca(0), lane);
         layer_norm_to_xa();
         for (int g = 0; g < NH / HG; ++g) {
-          for (int it = tid; it < SPT * S * 2 * GW; it += NT) {
-            const int col = it % (2 * GW), sm_ = (it / (2 * GW)) % S, j = it / (2 * GW * S);
-            const int gcol = col < GW ? g * GW + col : D + g * GW + (col - GW);
-            float v = 0.f;
-            if (smp[j] >= 0)
-              v = sm_ == 0 ? p.tkv[((size_t)k * L + l) * (2 * D) + gcol]
-                           : p.okv[(((size_t)smp[j] * L + l) * nobs + (sm_ - 1)) * (2 * D) + gcol];
-            kvbuf[(j * SMAX + sm_) * (2 * GW) + col] = v;
+          constexpr int KVN = SPT * SMAX * 2 * GW, KVQ = (KVN + NT - 1) / NT;
+          float kvv[KVQ];
+#pragma unroll
+          for (int q = 0; q < KVQ; ++q) {
+            const int it = tid + q * NT;
+            kvv[q] = 0.f;
+            if (it < KVN) {
+              const int col = it % (2 * GW), sm_ = (it / (2 * GW)) % SMAX, j = it / (2 * GW * SMAX);
+              const int gcol = col < GW ? g * GW + col : D + g * GW + (col - GW);
+              if (sm_ < S && smp[j] >= 0)
+                kvv[q] = sm_ == 0 ? p.tkv[((size_t)k * L + l) * (2 * D) + gcol]
+                                  : p.okv[(((size_t)smp[j] * L + l) * nobs + (sm_ - 1)) * (2 * D) + gcol];
+            }
           }
           f32x4 y[MPWC][RB];
 #pragma unroll
@@ -648,6 +733,9 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
 #pragma unroll
               for (int i = 0; i < 4; ++i) ybuf[(rb * 16 + lq * 4 + i) * LDY + loc] = y[m][rb][i] + bq;
           }
+#pragma unroll
+          for (int q = 0; q < KVQ; ++q)
+            if (tid + q * NT < KVN) kvbuf[tid + q * NT] = kvv[q];
           __syncthreads();
           for (int pr = w; pr < HG * RB; pr += NW) {
             const int hh = pr % HG, ib = pr / HG;
@@ -668,15 +756,10 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
               const int gi = ib * 16 + lq * 4 + i;
               const bool ok = nok && (jn == gi / HZ);
               const float v = ok ? s[i] * kScale : -INFINITY;
-              float m = v;
-#pragma unroll
-              for (int off = 1; off < 16; off <<= 1) m = fmaxf(m, __shfl_xor(m, off));
+              const float m = row16_max(v);
               const float ev = ok ? expf(v - m) : 0.f;
-              float su = ev;
-#pragma unroll
-              for (int off = 1; off < 16; off <<= 1) su += __shfl_xor(su, off);
               s[i] = ev;
-              sm[i] = su;
+              sm[i] = row16_sum(ev);
             }
             float* sc = pw + w * PWN;
 #pragma unroll
@@ -802,8 +885,6 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) epsp[(w * R + rb * 16 + lq * 4 + i) * 16 + lc] = eacc[rb][i];
       __syncthreads();
-      const float* dd = p.ddpm + (size_t)k * 8;
-      const float s1 = dd[0], sa = dd[1], c0 = dd[2], ct = dd[3], sg = dd[4];
 #pragma unroll
       for (int q = 0; q < ZPT; ++q) {
         const int it = tid + q * NT;
@@ -812,7 +893,7 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
           float part = 0.f;
 #pragma unroll
           for (int ww = 0; ww < NW; ++ww) part += epsp[(ww * R + row) * 16 + a];
-          const float e = raw[p.b_out + a] + part;
+          const float e = bout[q] + part;
           float* xp = xs + row * 16 + OF::pcol(a);
           const float x = *xp;
           float x0 = (x - s1 * e) / sa;
@@ -954,7 +1035,7 @@ hipError_t launch_ddpm_table(int T, float* table, hipStream_t stream) {
   X(float, 64, 32, 8, 2, 256, 4, 2, 256, 8)            \
   X(__bf16, 64, 32, 8, 2, 256, 4, 2, 256, 8)           \
   X(float, 256, 64, 16, 1, 1024, 8, 4, 256, 8)         \
-  X(float, 256, 64, 16, 2, 1024, 8, 2, 256, 8)         \
+  X(float, 256, 64, 16, 2, 1024, 8, 2, 128, 8)         \
   X(__bf16, 256, 64, 16, 1, 1024, 8, 4, 512, 8)        \
   X(__bf16, 256, 64, 16, 2, 1024, 8, 2, 256, 8)        \
   X(__bf16, 768, 64, 32, 1, 3072, 8, 2, 256, 5)
