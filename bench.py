@@ -78,6 +78,7 @@ class Runner:
             e.record()
         torch.cuda.synchronize()
         wall = time.perf_counter() - t0
+        self.pol.synchronize()   # raises if a kernel reported a device-side failure
         kms = [s.elapsed_time(e) for s, e in ev]
         return wall, kms
 
@@ -93,6 +94,7 @@ class Runner:
             self.call()
             torch.cuda.synchronize()
             lat.append((time.perf_counter() - t) * 1e3)
+        self.pol.synchronize()
         return lat
 
     def close(self):

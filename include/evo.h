@@ -83,7 +83,10 @@ typedef struct {
  * those of the time token once per policy, so they are not repeated at
  * each refresh.  The byte counters are this implementation's algorithmic
  * traffic: cache reads/writes of reused/refreshed residuals, and weight
- * bytes of evaluated units summed over workgroups. */
+ * bytes of evaluated units summed over workgroups.  n_tiles counts the
+ * sample tiles, n_workgroups the workgroups launched (small batches run
+ * several workgroups per one-sample tile; each keeps its own caches, so the
+ * cache bytes scale with it, while a unit's weights are split among them). */
 typedef struct {
   uint64_t refreshes_requested;
   uint64_t refreshes_effective;
@@ -95,6 +98,7 @@ typedef struct {
   uint64_t cache_bytes_written;
   uint64_t weight_bytes;
   uint64_t n_tiles;
+  uint64_t n_workgroups;
 } evo_stats;
 
 typedef struct evo_policy evo_policy;
@@ -159,6 +163,15 @@ int evo_set_schedule_pairs(evo_policy* p, int32_t schedule_id, const int32_t* pa
  * the statistics of the call are available immediately (host computed). */
 int evo_denoise(evo_policy* p, int32_t batch, const float* obs_cond, const float* noise,
                 const int32_t* schedule_ids, float* actions_out, void* hip_stream);
+
+/* Wait for the policy's last evo_denoise and report a device-side failure.
+ * Small batches run a variant in which several workgroups share a tile and
+ * meet at bounded device-side barriers; if one of those waits ever times
+ * out, the kernel stops early, its outputs are invalid, and this call
+ * returns EVO_E_HIP (the flag is then cleared; until it is, later team
+ * launches stop at their first barrier).  Setting the environment variable
+ * EVO_TEAM=0 before evo_create_policy disables that variant. */
+int evo_synchronize(evo_policy* p);
 
 /* Statistics of the last evo_denoise call (host struct). */
 int evo_get_stats(const evo_policy* p, evo_stats* out);

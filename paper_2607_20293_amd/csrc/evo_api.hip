@@ -2,6 +2,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cstdlib>
 #include <cstring>
 #include <new>
 #include <vector>
@@ -48,7 +49,7 @@ int check_supported(const Shape& s) {
   const int n = spt_options(s.H, opts);
   bool any = false;
   for (int i = 0; i < n; ++i) {
-    KernelKey k{s.d, s.dh(), s.H, s.dff, s.dtype, opts[i]};
+    KernelKey k{s.d, s.dh(), s.H, s.dff, s.dtype, opts[i], 1};
     int th;
     if (!kernel_available(k, &th)) continue;
     if (s.A > kernel_max_action_dim()) return fail(EVO_E_UNSUPPORTED, "action_dim %d > %d", s.A, kernel_max_action_dim());
@@ -87,6 +88,13 @@ struct evo_policy {
   float* d_cache = nullptr;
   size_t cache_floats = 0;
   float* d_okv = nullptr;
+  // small-batch team variant: members per tile, largest batch it serves,
+  // partial-residual exchange, barrier counters, device error flag
+  int team = 1, team_batch = 0;
+  size_t okv_stride = 0;
+  float* d_xchg = nullptr;
+  unsigned* d_tctr = nullptr;
+  unsigned* d_derr = nullptr;
   uint8_t* d_plan = nullptr;
   size_t plan_bytes = 0, tiles_cap = 0, codes_cap = 0;
   uint8_t* h_stage[2] = {nullptr, nullptr};
@@ -101,6 +109,7 @@ struct evo_policy {
   bool has_last = false;
   Plan last_plan;
   int last_threads = 0;
+  int last_team = 1;
 };
 
 static void release(evo_policy* p) {
@@ -114,6 +123,9 @@ static void release(evo_policy* p) {
   (void)hipFree(p->d_ddpm);
   (void)hipFree(p->d_cache);
   (void)hipFree(p->d_okv);
+  (void)hipFree(p->d_xchg);
+  (void)hipFree(p->d_tctr);
+  (void)hipFree(p->d_derr);
   (void)hipFree(p->d_plan);
   for (int i = 0; i < 2; ++i) {
     if (p->h_stage[i]) (void)hipHostFree(p->h_stage[i]);
@@ -273,9 +285,30 @@ int evo_create_policy(const evo_policy_desc* desc, const float* host_weights, si
       tiles = std::max(tiles, t);
       spt_max = std::max(spt_max, opts[i]);
     }
+    // team variant (one sample per tile, `team` workgroups per tile) for
+    // batches that fill at most n_cu workgroups; it needs cooperative launch
+    const char* env = std::getenv("EVO_TEAM");
+    const bool team_on = !(env && env[0] == '0');
+    const int team = kernel_team_size(KernelKey{s.d, s.dh(), s.H, s.dff, s.dtype, 1, 0});
+    int coop = 0;
+    (void)hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, p->device);
+    if (team_on && team > 1 && coop && p->n_cu >= team) {
+      p->team = team;
+      p->team_batch = std::min(s.max_batch, p->n_cu / team);
+      rows = std::max(rows, (size_t)p->team_batch * team * s.H);
+    }
     p->cache_floats = (size_t)U * rows * d;
     CREATE_TRY(hipMalloc(&p->d_cache, p->cache_floats * sizeof(float)));
-    CREATE_TRY(hipMalloc(&p->d_okv, (size_t)s.max_batch * L * s.n_obs * 2 * d * sizeof(float)));
+    const size_t okv_per = (size_t)L * s.n_obs * 2 * d;
+    p->okv_stride = (size_t)p->team_batch * okv_per;
+    CREATE_TRY(hipMalloc(&p->d_okv,
+                         std::max((size_t)s.max_batch * okv_per, p->okv_stride * p->team) * sizeof(float)));
+    if (p->team > 1) {
+      CREATE_TRY(hipMalloc(&p->d_xchg, (size_t)p->team_batch * 2 * p->team * s.H * d * sizeof(float)));
+      CREATE_TRY(hipMalloc(&p->d_tctr, (size_t)p->team_batch * 16 * sizeof(unsigned)));
+      CREATE_TRY(hipMalloc(&p->d_derr, sizeof(unsigned)));
+      CREATE_TRY(hipMemset(p->d_derr, 0, sizeof(unsigned)));
+    }
     p->tiles_cap = tiles * spt_max;
     p->codes_cap = (size_t)std::min(s.max_sched, s.max_batch) * T * 3 * sizeof(uint64_t);
     p->plan_bytes = (2 * p->tiles_cap * sizeof(int32_t) + 255) / 256 * 256 + p->codes_cap;
@@ -343,9 +376,9 @@ int evo_denoise(evo_policy* p, int32_t batch, const float* obs_cond, const float
   // samples per tile: two when a single-sample tiling would oversubscribe the CUs
   int opts[2];
   const int nopt = spt_options(s.H, opts);
-  int spt = 0, threads = 0;
+  int spt = 0, threads = 0, team = 1;
   for (int i = 0; i < nopt; ++i) {
-    KernelKey k{s.d, s.dh(), s.H, s.dff, s.dtype, opts[i]};
+    KernelKey k{s.d, s.dh(), s.H, s.dff, s.dtype, opts[i], 1};
     int th;
     if (!kernel_available(k, &th)) continue;
     if (spt == 0 || (opts[i] > spt && batch > p->n_cu)) {
@@ -354,6 +387,16 @@ int evo_denoise(evo_policy* p, int32_t batch, const float* obs_cond, const float
     }
   }
   if (!spt) return fail(EVO_E_UNSUPPORTED, "no kernel for this shape");
+  // small batches: several workgroups per one-sample tile
+  if (p->team > 1 && batch <= p->team_batch) {
+    KernelKey k{s.d, s.dh(), s.H, s.dff, s.dtype, 1, p->team};
+    int th;
+    if (kernel_available(k, &th)) {
+      spt = 1;
+      threads = th;
+      team = p->team;
+    }
+  }
   Plan plan;
   int rc = build_plan(s, p->reg, schedule_ids, batch, spt, 8, &plan);
   if (rc) return rc;
@@ -402,16 +445,42 @@ int evo_denoise(evo_policy* p, int32_t batch, const float* obs_cond, const float
   kp.pk_wout = p->pk_wout;
   kp.obs = obs_cond; kp.noise = noise; kp.out = actions_out; kp.okv = p->d_okv; kp.cache = p->d_cache;
   kp.batch = batch;
-  KernelKey key{s.d, s.dh(), s.H, s.dff, s.dtype, spt};
+  kp.team = team;
+  if (team > 1) {
+    if ((size_t)plan.n_tiles > (size_t)p->team_batch) return fail(EVO_E_STATE, "team plan exceeds the buffers");
+    kp.xchg = p->d_xchg;
+    kp.tctr = p->d_tctr;
+    kp.derr = p->d_derr;
+    kp.okv_member_stride = p->okv_stride;
+    HIP_TRY(launch_zero_u32(p->d_tctr, plan.n_tiles * 16, stream));
+  }
+  KernelKey key{s.d, s.dh(), s.H, s.dff, s.dtype, spt, team};
   HIP_TRY(launch_denoise(key, kp, stream));
   HIP_TRY(hipEventRecord(p->ev_done, stream));
   p->last_stream = stream;
   p->launched = true;
 
-  call_stats(s, p->reg, schedule_ids, batch, &plan, &p->last);
+  call_stats(s, p->reg, schedule_ids, batch, &plan, team, &p->last);
   p->has_last = true;
   p->last_plan = std::move(plan);
   p->last_threads = threads;
+  p->last_team = team;
+  return EVO_OK;
+}
+
+int evo_synchronize(evo_policy* p) {
+  clear_error();
+  if (!p) return fail(EVO_E_INVALID, "policy is NULL");
+  DeviceGuard guard(p->device);
+  if (p->launched) HIP_TRY(hipEventSynchronize(p->ev_done));
+  if (p->d_derr) {
+    unsigned flag = 0;
+    HIP_TRY(hipMemcpy(&flag, p->d_derr, sizeof(unsigned), hipMemcpyDeviceToHost));
+    if (flag) {
+      HIP_TRY(hipMemset(p->d_derr, 0, sizeof(unsigned)));
+      return fail(EVO_E_HIP, "a team barrier timed out on the device; outputs of that call are invalid");
+    }
+  }
   return EVO_OK;
 }
 
@@ -439,7 +508,7 @@ int evo_schedule_stats(const evo_policy_desc* desc, const uint8_t* lattices, int
     const int id = ids ? ids[n] : 0;
     if (id < 0 || id >= n_lat) return fail(EVO_E_INVALID, "id %d of sample %d out of range", id, n);
   }
-  call_stats(s, reg, ids, batch, nullptr, out);
+  call_stats(s, reg, ids, batch, nullptr, 1, out);
   return EVO_OK;
 }
 
@@ -473,7 +542,8 @@ int evo_debug_read_cache(evo_policy* p, int32_t unit, int32_t sample, float* hos
   HIP_TRY(hipDeviceSynchronize());
   const int R = pl.spt * s.H, d = s.d, NW = p->last_threads / 64, RB = R / 16, CBW = d / 16 / NW;
   std::vector<float> buf((size_t)R * d);
-  HIP_TRY(hipMemcpy(buf.data(), p->d_cache + ((size_t)tile * s.U() + unit) * R * d, buf.size() * sizeof(float),
+  HIP_TRY(hipMemcpy(buf.data(), p->d_cache + ((size_t)tile * p->last_team * s.U() + unit) * R * d,
+                    buf.size() * sizeof(float),
                     hipMemcpyDeviceToHost));
   for (int i = 0; i < s.H; ++i) {
     const int row = slot * s.H + i, rb = row / 16, rr = row % 16;

@@ -225,7 +225,7 @@ int build_plan(const Shape& s, const std::vector<Schedule>& reg, const int32_t* 
 }
 
 void call_stats(const Shape& s, const std::vector<Schedule>& reg, const int32_t* ids, int batch,
-                const Plan* plan, evo_stats* out) {
+                const Plan* plan, int team, evo_stats* out) {
   evo_stats st;
   std::memset(&st, 0, sizeof(st));
   const Flops f = flops_of(s);
@@ -249,8 +249,11 @@ void call_stats(const Shape& s, const std::vector<Schedule>& reg, const int32_t*
     const uint64_t obs_pad = (uint64_t)((s.obs_dim + 31) / 32 * 32);
     const uint64_t per_query_w = obs_pad * s.d * e + (uint64_t)s.L * 2 * s.d * s.d * e;
     st.n_tiles = plan->n_tiles;
+    st.n_workgroups = (uint64_t)plan->n_tiles * team;
+    st.cache_bytes_read *= team;
+    st.cache_bytes_written *= team;
     for (int q = 0; q < plan->n_tiles; ++q) {
-      st.weight_bytes += per_query_w;
+      st.weight_bytes += per_query_w * team;
       for (int t = 0; t < s.T; ++t) {
         uint64_t mask = 0;
         for (int j = 0; j < plan->spt; ++j) {

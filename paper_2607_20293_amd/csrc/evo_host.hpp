@@ -101,8 +101,10 @@ struct Plan {
 int build_plan(const Shape& s, const std::vector<Schedule>& reg, const int32_t* ids, int batch,
                int spt, int n_xcd, Plan* out);
 
-// Bookkeeping of a call (refreshes, FLOPs, algorithmic bytes).
+// Bookkeeping of a call (refreshes, FLOPs, algorithmic bytes).  With
+// `team` workgroups per tile, every member keeps its own caches and
+// observation keys/values, while the per-unit weights are split among them.
 void call_stats(const Shape& s, const std::vector<Schedule>& reg, const int32_t* ids, int batch,
-                const Plan* plan, evo_stats* out);
+                const Plan* plan, int team, evo_stats* out);
 
 }  // namespace evo

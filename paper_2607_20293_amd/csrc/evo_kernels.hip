@@ -33,6 +33,7 @@ namespace evo {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr uint64_t kMergedBit = 1ull << 63;
 constexpr int kMaskEntries = 341;  // (T x samples per tile) entries of 3 x u64 in LDS (8 KiB)
@@ -124,13 +125,13 @@ __device__ __forceinline__ void gemm_pref(uint4 (&bc)[MPW], const uint4* W, int 
 // W: packed fragments of a matrix with KBT fragments per column block; kf0
 // is the first fragment of the k-range, NKF its length; bc holds the
 // fragments of kf0 (gemm_pref).  Weight fragments are requested PD k-steps
-// ahead of their MFMAs (about six 1 KiB fragments in flight per wave); a
+// ahead of their MFMAs (about INFL 1 KiB fragments in flight per wave); a
 // scheduling fence per step keeps the compiler from hoisting further loads.
-template <class AT, int RBk, int MPW, int NKF, class GCB>
+template <class AT, int RBk, int MPW, int NKF, int INFL, class GCB>
 __device__ __forceinline__ void gemm_run(f32x4 (&acc)[MPW][RBk], const AT* A, int lda, const uint4* W, int KBT,
                                          int kf0, GCB gcb, int lane, uint4 (&bc)[MPW]) {
   using O = Op<AT>;
-  constexpr int PD0 = 6 / MPW > 0 ? 6 / MPW : 1;
+  constexpr int PD0 = INFL / MPW > 0 ? INFL / MPW : 1;
   constexpr int PD = PD0 < NKF ? PD0 : (NKF > 1 ? NKF - 1 : 1);
   const int lc = lane & 15, lq = lane >> 4;
   const uint4* wp[MPW];
@@ -167,12 +168,12 @@ __device__ __forceinline__ void gemm_acc(f32x4 (&acc)[MPW][RBk], const AT* A, in
                                          int kf0, GCB gcb, int lane) {
   uint4 bc[MPW];
   gemm_pref<MPW>(bc, W, KBT, kf0, gcb, lane);
-  gemm_run<AT, RBk, MPW, NKF>(acc, A, lda, W, KBT, kf0, gcb, lane, bc);
+  gemm_run<AT, RBk, MPW, NKF, 6>(acc, A, lda, W, KBT, kf0, gcb, lane, bc);
 }
 
 __device__ __forceinline__ float gelu_erf(float v) { return 0.5f * v * (1.0f + erff(v * 0.70710678118654752f)); }
 
-template <int D, int DH, int HZ, int SPT, int DFF, int NW, int HG, int FC, int SMAX>
+template <int D, int DH, int HZ, int SPT, int DFF, int NW, int HG, int FC, int SMAX, int TEAM>
 struct Cfg {
   static constexpr int NWV = NW;
   static constexpr int NT = NW * 64;
@@ -253,23 +254,28 @@ __device__ __forceinline__ void ln_stats(const f32x4 (&h)[C::CBW][C::RB], float 
     }
 }
 
-template <class AT, int D, int DH, int HZ, int SPT, int DFF, int NW, int HG, int FC, int SMAX>
+template <class AT, int D, int DH, int HZ, int SPT, int DFF, int NW, int HG, int FC, int SMAX, int TEAM>
 __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
   using O = Op<AT>;
   using OF = Op<float>;
-  using C = Cfg<D, DH, HZ, SPT, DFF, NW, HG, FC, SMAX>;
+  using C = Cfg<D, DH, HZ, SPT, DFF, NW, HG, FC, SMAX, TEAM>;
   constexpr int NT = C::NT, R = C::R, RB = C::RB, NH = C::NH, CB = C::CB, CBW = C::CBW, GW = C::GW;
   constexpr int LDA = D + O::PAD, LDY = C::LDY, LDZ = C::ZW + O::PAD;
   constexpr int KOBS = C::KOBS, LDO = KOBS + O::PAD;
   constexpr int NJB = C::NJB, SLOTS = C::SLOTS, PS = C::PS, PWN = C::PWN, NB = C::NB;
   static_assert(R % 16 == 0 && CB % NW == 0 && NH % HG == 0 && DFF % FC == 0, "tile shape");
   static_assert((3 * GW / 16) % NW == 0 && (GW / 16) % NW == 0 && (FC / 16) % NW == 0, "block split");
+  static_assert((NH / HG) % TEAM == 0 && (DFF / FC) % TEAM == 0, "team members split head groups and chunks");
   static_assert(HZ % 4 == 0 && (HZ & (HZ - 1)) == 0 && HZ <= 64, "horizon must be a power of two in [4, 64]");
   static_assert(NW * R * 16 <= R * LDY, "head partials must fit the stage-1 buffer");
   static_assert(16 * LDO * (int)sizeof(AT) <= R * LDY * 4, "observation operand must fit");
   static_assert(SMAX <= SLOTS, "memory tokens per sample must fit a 16-column tile");
   static_assert(DH % 16 == 0, "head dim");
   constexpr bool KEEP_EMB = RB == 1 && CBW <= 4;  // embedding constants kept in registers across steps
+  // layer-merged residual sum accumulated in registers, else in its cache slot
+  constexpr bool MAC_REG = CBW * RB <= 4;
+  // weight fragments in flight per wave in the unit products
+  constexpr int INFL = TEAM > 1 ? 16 : (RB == 1 && CBW <= 2 ? 12 : 6);
   constexpr float kScale = (DH == 64) ? 0.125f : (DH == 32 ? 0.17677669529663688f : 0.0f);
   static_assert(DH == 64 || DH == 32, "head dim");
 
@@ -286,11 +292,18 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
   __shared__ int smp[SPT];
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, lc = lane & 15, lq = lane >> 4;
-  const int tile = blockIdx.x;
+  // a team of TEAM workgroups shares a tile: each member evaluates its share
+  // of every unit's head groups / d_ff chunks and the partial residuals are
+  // summed through HBM; everything else is replicated in every member
+  const int member = blockIdx.x % TEAM;
+  const int tile = blockIdx.x / TEAM;
+  __shared__ int s_abort;
   const int L = p.L, A = p.A, T = p.T, U = 3 * L, nobs = p.n_obs, S = 1 + nobs;
   const float* raw = p.raw;
 
   if (tid < SPT) smp[tid] = p.tile_sample[tile * SPT + tid];
+  if (tid == 0) s_abort = 0;
+  float* const okv = p.okv + (size_t)member * p.okv_member_stride;
   for (int it = tid; it < L * (int)(sizeof(LayerOff) / 4); it += NT)
     reinterpret_cast<uint32_t*>(s_loff)[it] = reinterpret_cast<const uint32_t*>(p.loff)[it];
   for (int it = tid; it < L * (int)(sizeof(PackOff) / 8); it += NT)
@@ -363,7 +376,7 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
           if (row < SPT * nobs) {
             const int j = row / nobs, o = row % nobs;
             if (smp[j] >= 0)
-              p.okv[(((size_t)smp[j] * L + l) * nobs + o) * (2 * D) + gcol] = kv[m][0][i] + raw[bkv + gcol];
+              okv[(((size_t)smp[j] * L + l) * nobs + o) * (2 * D) + gcol] = kv[m][0][i] + raw[bkv + gcol];
           }
         }
       }
@@ -375,7 +388,8 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
   int jrow[RB];
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) jrow[rb] = (rb * 16 + lq * 4) / HZ;
-  float* cbase = p.cache + (size_t)tile * U * (R * D);
+  float* cbase = p.cache + (size_t)(tile * TEAM + member) * U * (R * D);
+  int nbar = 0, xpar = 0;  // team barriers passed, exchange buffer parity
   const auto cfrag = [&](int unit, int c, int rb) {
     return reinterpret_cast<f32x4*>(cbase + (size_t)unit * (R * D) +
                                     ((size_t)((w * RB + rb) * CBW + c) * 64 + lane) * 4);
@@ -401,11 +415,11 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
     }
   }
 
-  f32x4 h[CBW][RB], mac[CBW][RB];
+  f32x4 h[CBW][RB], mac[MAC_REG ? CBW : 1][MAC_REG ? RB : 1];
 #pragma unroll
-  for (int c = 0; c < CBW; ++c)
+  for (int c = 0; c < (MAC_REG ? CBW : 1); ++c)
 #pragma unroll
-    for (int rb = 0; rb < RB; ++rb) mac[c][rb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int rb = 0; rb < (MAC_REG ? RB : 1); ++rb) mac[c][rb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   // LayerNorm gain/shift and output bias of the next unit to evaluate, for
   // this lane's columns (loaded one unit ahead)
@@ -436,6 +450,34 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
     return m ? __builtin_ctzll(m) : U;
   };
 
+  // reuse-cache loads: a batch takes the NB lowest units of a mask
+  const auto seg_mask = [](int lo, int hi) {
+    const uint64_t lo_m = (lo >= 64) ? ~0ull : ((1ull << lo) - 1);
+    const uint64_t hi_m = (hi >= 64) ? ~0ull : ((1ull << hi) - 1);
+    return hi_m & ~lo_m;
+  };
+  uint64_t mru_cur[SPT];
+  const auto issue_batch = [&](uint64_t& um, auto& ub, auto& v) {
+#pragma unroll
+    for (int q = 0; q < NB; ++q) {
+      ub[q] = um ? __builtin_ctzll(um) : -1;
+      um = um ? (um & (um - 1)) : 0ull;
+    }
+#pragma unroll
+    for (int q = 0; q < NB; ++q)
+#pragma unroll
+      for (int c = 0; c < CBW; ++c)
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) {
+          uint64_t mj = mru_cur[0];
+#pragma unroll
+          for (int jj = 1; jj < SPT; ++jj)
+            if (jrow[rb] == jj) mj = mru_cur[jj];
+          v[q][c][rb] = f32x4{0.f, 0.f, 0.f, 0.f};
+          if (ub[q] >= 0 && ((mj >> ub[q]) & 1ull)) v[q][c][rb] = *cfrag(ub[q], c, rb);
+        }
+  };
+
   constexpr int ZPT = (R * 16 + NT - 1) / NT;
   constexpr int MPWQ = (3 * GW / 16) / NW, MPWC = (GW / 16) / NW, MPWF = (FC / 16) / NW;
 
@@ -455,7 +497,9 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
       mst[j] = live ? msk[(j * T + t) * 3 + 2] : 0ull;
       evT |= mev[j];
       ruT |= mru[j];
+      mru_cur[j] = mru[j];
     }
+
     const auto pick = [&](const uint64_t (&m)[SPT], int j) {
       uint64_t v = m[0];
 #pragma unroll
@@ -521,28 +565,14 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
     while (true) {
       const uint64_t rest = evT >> b;
       const int e = rest ? b + __builtin_ctzll(rest) : U;
-      // reused residuals of the units in [b, e), in unit order
+      // reused residuals of the units in [b, e), in unit order, loaded in
+      // batches of NB units
       {
-        const uint64_t lo_m = (b >= 64) ? ~0ull : ((1ull << b) - 1);
-        const uint64_t hi_m = (e >= 64) ? ~0ull : ((1ull << e) - 1);
-        uint64_t um = ruT & hi_m & ~lo_m;
+        uint64_t um = ruT & seg_mask(b, e);
         while (um) {
           int ub[NB];
-#pragma unroll
-          for (int q = 0; q < NB; ++q) {
-            ub[q] = um ? __builtin_ctzll(um) : -1;
-            um = um ? (um & (um - 1)) : 0ull;
-          }
           f32x4 v[NB][CBW][RB];
-#pragma unroll
-          for (int q = 0; q < NB; ++q)
-#pragma unroll
-            for (int c = 0; c < CBW; ++c)
-#pragma unroll
-              for (int rb = 0; rb < RB; ++rb) {
-                v[q][c][rb] = f32x4{0.f, 0.f, 0.f, 0.f};
-                if (ub[q] >= 0 && ((pick(mru, jrow[rb]) >> ub[q]) & 1ull)) v[q][c][rb] = *cfrag(ub[q], c, rb);
-              }
+          issue_batch(um, ub, v);
 #pragma unroll
           for (int q = 0; q < NB; ++q)
 #pragma unroll
@@ -563,15 +593,6 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
         lg[c] = nlg[c];
         lb[c] = nlb[c];
         rbias[c] = nrb[c];
-      }
-      {
-        // request the parameters of the next evaluated unit (this step or the next)
-        const uint64_t later = (e + 1 < 64) ? (evT >> (e + 1)) : 0ull;
-        if (later) load_unit_params(t, e + 1 + __builtin_ctzll(later));
-        else if (t + 1 < T) {
-          const int f = first_eval(t + 1);
-          if (f < U) load_unit_params(t + 1, f);
-        }
       }
       const auto gcb_sa = [&](int g) {
         return [=](int m) {
@@ -606,16 +627,16 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
       if (u == 0) {
         // ---------------- self-attention unit (causal over the action tokens)
         uint4 b1q[MPWQ];  // stage-1 weights of the first chunk, requested before the LayerNorm
-        gemm_pref<MPWQ>(b1q, pk + po.qkv, D / O::KF, 0, gcb_sa(0), lane);
+        gemm_pref<MPWQ>(b1q, pk + po.qkv, D / O::KF, 0, gcb_sa(member), lane);
         layer_norm_to_xa();
-        for (int g = 0; g < NH / HG; ++g) {
+        for (int g = member; g < NH / HG; g += TEAM) {
           f32x4 y[MPWQ][RB];
 #pragma unroll
           for (int m = 0; m < MPWQ; ++m)
 #pragma unroll
             for (int rb = 0; rb < RB; ++rb) y[m][rb] = f32x4{0.f, 0.f, 0.f, 0.f};
-          if (g > 0) gemm_pref<MPWQ>(b1q, pk + po.qkv, D / O::KF, 0, gcb_sa(g), lane);
-          gemm_run<AT, RB, MPWQ, D / O::KF>(y, xa, LDA, pk + po.qkv, D / O::KF, 0, gcb_sa(g), lane, b1q);
+          if (g != member) gemm_pref<MPWQ>(b1q, pk + po.qkv, D / O::KF, 0, gcb_sa(g), lane);
+          gemm_run<AT, RB, MPWQ, D / O::KF, INFL>(y, xa, LDA, pk + po.qkv, D / O::KF, 0, gcb_sa(g), lane, b1q);
           uint4 b2[CBW];
           gemm_pref<CBW>(b2, pk + po.o, D / O::KF, g * (GW / O::KF), own, lane);
 #pragma unroll
@@ -693,16 +714,16 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
             wave_lds_sync();
           }
           __syncthreads();
-          gemm_run<AT, RB, CBW, GW / O::KF>(r, zbuf, LDZ, pk + po.o, D / O::KF, g * (GW / O::KF), own, lane, b2);
+          gemm_run<AT, RB, CBW, GW / O::KF, INFL>(r, zbuf, LDZ, pk + po.o, D / O::KF, g * (GW / O::KF), own, lane, b2);
         }
       } else if (u == 1) {
         // ---------------- cross-attention unit (time token + observation tokens)
         uint4 b1c[MPWC];
-        gemm_pref<MPWC>(b1c, pk + po.q, D / O::KF, 0, gcb_ca(0), lane);
-        layer_norm_to_xa();
-        for (int g = 0; g < NH / HG; ++g) {
-          constexpr int KVN = SPT * SMAX * 2 * GW, KVQ = (KVN + NT - 1) / NT;
-          float kvv[KVQ];
+        gemm_pref<MPWC>(b1c, pk + po.q, D / O::KF, 0, gcb_ca(member), lane);
+        // memory keys/values of a head group: time token + observation tokens
+        constexpr int KVN = SPT * SMAX * 2 * GW, KVQ = (KVN + NT - 1) / NT;
+        float kvv[KVQ];
+        const auto load_kv = [&](int g) {
 #pragma unroll
           for (int q = 0; q < KVQ; ++q) {
             const int it = tid + q * NT;
@@ -712,16 +733,21 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
               const int gcol = col < GW ? g * GW + col : D + g * GW + (col - GW);
               if (sm_ < S && smp[j] >= 0)
                 kvv[q] = sm_ == 0 ? p.tkv[((size_t)k * L + l) * (2 * D) + gcol]
-                                  : p.okv[(((size_t)smp[j] * L + l) * nobs + (sm_ - 1)) * (2 * D) + gcol];
+                                  : okv[(((size_t)smp[j] * L + l) * nobs + (sm_ - 1)) * (2 * D) + gcol];
             }
           }
+        };
+        load_kv(member);
+        layer_norm_to_xa();
+        for (int g = member; g < NH / HG; g += TEAM) {
+          if (g != member) load_kv(g);
           f32x4 y[MPWC][RB];
 #pragma unroll
           for (int m = 0; m < MPWC; ++m)
 #pragma unroll
             for (int rb = 0; rb < RB; ++rb) y[m][rb] = f32x4{0.f, 0.f, 0.f, 0.f};
-          if (g > 0) gemm_pref<MPWC>(b1c, pk + po.q, D / O::KF, 0, gcb_ca(g), lane);
-          gemm_run<AT, RB, MPWC, D / O::KF>(y, xa, LDA, pk + po.q, D / O::KF, 0, gcb_ca(g), lane, b1c);
+          if (g != member) gemm_pref<MPWC>(b1c, pk + po.q, D / O::KF, 0, gcb_ca(g), lane);
+          gemm_run<AT, RB, MPWC, D / O::KF, INFL>(y, xa, LDA, pk + po.q, D / O::KF, 0, gcb_ca(g), lane, b1c);
           uint4 b2[CBW];
           gemm_pref<CBW>(b2, pk + po.o2, D / O::KF, g * (GW / O::KF), own, lane);
 #pragma unroll
@@ -782,21 +808,21 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
             wave_lds_sync();
           }
           __syncthreads();
-          gemm_run<AT, RB, CBW, GW / O::KF>(r, zbuf, LDZ, pk + po.o2, D / O::KF, g * (GW / O::KF), own, lane, b2);
+          gemm_run<AT, RB, CBW, GW / O::KF, INFL>(r, zbuf, LDZ, pk + po.o2, D / O::KF, g * (GW / O::KF), own, lane, b2);
         }
       } else {
         // ---------------- feed-forward unit, d_ff streamed in chunks of FC
         uint4 b1f[MPWF];
-        gemm_pref<MPWF>(b1f, pk + po.w1, D / O::KF, 0, gcb_ff(0), lane);
+        gemm_pref<MPWF>(b1f, pk + po.w1, D / O::KF, 0, gcb_ff(member), lane);
         layer_norm_to_xa();
-        for (int ch = 0; ch < DFF / FC; ++ch) {
+        for (int ch = member; ch < DFF / FC; ch += TEAM) {
           f32x4 y[MPWF][RB];
 #pragma unroll
           for (int m = 0; m < MPWF; ++m)
 #pragma unroll
             for (int rb = 0; rb < RB; ++rb) y[m][rb] = f32x4{0.f, 0.f, 0.f, 0.f};
-          if (ch > 0) gemm_pref<MPWF>(b1f, pk + po.w1, D / O::KF, 0, gcb_ff(ch), lane);
-          gemm_run<AT, RB, MPWF, D / O::KF>(y, xa, LDA, pk + po.w1, D / O::KF, 0, gcb_ff(ch), lane, b1f);
+          if (ch != member) gemm_pref<MPWF>(b1f, pk + po.w1, D / O::KF, 0, gcb_ff(ch), lane);
+          gemm_run<AT, RB, MPWF, D / O::KF, INFL>(y, xa, LDA, pk + po.w1, D / O::KF, 0, gcb_ff(ch), lane, b1f);
           uint4 b2[CBW];
           gemm_pref<CBW>(b2, pk + po.w2, DFF / O::KF, ch * (FC / O::KF), own, lane);
 #pragma unroll
@@ -810,9 +836,83 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
                 O::store(zbuf, LDZ, rb * 16 + lq * 4 + i, loc, gelu_erf(y[m][rb][i] + b1));
           }
           __syncthreads();
-          gemm_run<AT, RB, CBW, FC / O::KF>(r, zbuf, LDZ, pk + po.w2, DFF / O::KF, ch * (FC / O::KF), own, lane, b2);
+          gemm_run<AT, RB, CBW, FC / O::KF, INFL>(r, zbuf, LDZ, pk + po.w2, DFF / O::KF, ch * (FC / O::KF), own, lane, b2);
           __syncthreads();
         }
+      }
+      // request the parameters of the next evaluated unit (this step or the
+      // next), after this unit's weight loads so they do not delay them
+      const auto request_next_params = [&]() {
+        const uint64_t later = (e + 1 < 64) ? (evT >> (e + 1)) : 0ull;
+        if (later) load_unit_params(t, e + 1 + __builtin_ctzll(later));
+        else if (t + 1 < T) {
+          const int f = first_eval(t + 1);
+          if (f < U) load_unit_params(t + 1, f);
+        }
+      };
+      if constexpr (TEAM > 1) {
+        // Sum the members' partial residuals in member order, so that every
+        // member obtains the same bits.  The partials travel through memory
+        // with device-coherent (SC1) buffer stores and loads, which do not
+        // leave stale or dirty lines in the per-XCD caches; the barrier thus
+        // needs no cache write-back or invalidation (the weight stream stays
+        // in L2).  Ordering: a member's stores have completed (vmcnt 0)
+        // before its counter increment, and the partials are loaded only
+        // after the counter has shown every member.
+        constexpr int kCoherent = 16;  // SC1 cache-policy bit
+        float* xb = p.xchg + (size_t)tile * (2 * TEAM) * (R * D);
+        const auto xr = __builtin_amdgcn_make_buffer_rsrc(xb, (short)0, 2 * TEAM * R * D * 4, 0x00020000);
+        const auto xoff = [&](int slot, int c, int rb) {
+          return (slot * (R * D) + (((w * RB + rb) * CBW + c) * 64 + lane) * 4) * 4;
+        };
+#pragma unroll
+        for (int c = 0; c < CBW; ++c)
+#pragma unroll
+          for (int rb = 0; rb < RB; ++rb)
+            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, r[c][rb]), xr,
+                                                   xoff(xpar * TEAM + member, c, rb), 0, kCoherent);
+        __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this wave's partials are written
+        request_next_params();
+        __syncthreads();
+        ++nbar;
+        if (tid == 0) {
+          unsigned* ctr = p.tctr + (size_t)tile * 16;
+          __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          const unsigned target = (unsigned)(nbar * TEAM);
+          unsigned spins = 0;
+          while (__hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
+            // bounded wait: a member that never arrives ends the whole kernel
+            if (__hip_atomic_load(p.derr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u ||
+                ++spins > (1u << 22)) {
+              __hip_atomic_store(p.derr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+              s_abort = 1;
+              break;
+            }
+            __builtin_amdgcn_s_sleep(1);
+          }
+        }
+        __syncthreads();
+        if (s_abort) return;
+        u32x4 part[TEAM][CBW][RB];
+#pragma unroll
+        for (int m = 0; m < TEAM; ++m)
+#pragma unroll
+          for (int c = 0; c < CBW; ++c)
+#pragma unroll
+            for (int rb = 0; rb < RB; ++rb)
+              part[m][c][rb] = __builtin_amdgcn_raw_buffer_load_b128(xr, xoff(xpar * TEAM + m, c, rb), 0, kCoherent);
+#pragma unroll
+        for (int c = 0; c < CBW; ++c)
+#pragma unroll
+          for (int rb = 0; rb < RB; ++rb) {
+            f32x4 acc = __builtin_bit_cast(f32x4, part[0][c][rb]);
+#pragma unroll
+            for (int m = 1; m < TEAM; ++m) acc += __builtin_bit_cast(f32x4, part[m][c][rb]);
+            r[c][rb] = acc;
+          }
+        xpar ^= 1;
+      } else {
+        request_next_params();
       }
 #pragma unroll
       for (int c = 0; c < CBW; ++c)
@@ -833,8 +933,18 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
             if (j == jj) mg = mmg[jj];
           if (pick(mev, j) & bit) {
             const f32x4 v = r[c][rb];
-            if (mg) mac[c][rb] = (u == 0) ? v : mac[c][rb] + v;
-            if (pick(mst, j) & bit) *cfrag(e, c, rb) = mg ? mac[c][rb] : v;
+            if constexpr (MAC_REG) {
+              if (mg) mac[c][rb] = (u == 0) ? v : mac[c][rb] + v;
+              if (pick(mst, j) & bit) *cfrag(e, c, rb) = mg ? mac[c][rb] : v;
+            } else {
+              // layer sum kept in the layer's cache slot (the FFN position)
+              if (mg) {
+                f32x4* slot = cfrag(3 * l + 2, c, rb);
+                *slot = (u == 0) ? v : *slot + v;
+              } else if (pick(mst, j) & bit) {
+                *cfrag(e, c, rb) = v;
+              }
+            }
             h[c][rb] += v;
           } else if (pick(mru, j) & bit) {
             h[c][rb] += *cfrag(e, c, rb);
@@ -903,7 +1013,7 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
           *xp = xn;
           if (t == T - 1) {
             const int s = smp[row / HZ];
-            if (s >= 0) p.out[((size_t)s * HZ + (row % HZ)) * A + a] = xn;
+            if (s >= 0 && member == 0) p.out[((size_t)s * HZ + (row % HZ)) * A + a] = xn;
           }
         }
       }
@@ -1025,32 +1135,45 @@ hipError_t launch_time_kv(const float* raw, uint32_t pmem0, const uint32_t* wkv,
   return hipGetLastError();
 }
 
+__global__ void zero_u32_kernel(unsigned* dst, int n) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) dst[i] = 0u;
+}
+
+hipError_t launch_zero_u32(unsigned* dst, int n, hipStream_t stream) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(zero_u32_kernel, dim3((n + 255) / 256), dim3(256), 0, stream, dst, n);
+  return hipGetLastError();
+}
+
 hipError_t launch_ddpm_table(int T, float* table, hipStream_t stream) {
   hipLaunchKernelGGL(ddpm_kernel, dim3(1), dim3(1), 0, stream, T, table);
   return hipGetLastError();
 }
 
 // ---------------------------------------------------------------- dispatch
-#define EVO_SHAPES(X)                                  \
-  X(float, 64, 32, 8, 2, 256, 4, 2, 256, 8)            \
-  X(__bf16, 64, 32, 8, 2, 256, 4, 2, 256, 8)           \
-  X(float, 256, 64, 16, 1, 1024, 8, 4, 256, 8)         \
-  X(float, 256, 64, 16, 2, 1024, 8, 2, 128, 8)         \
-  X(__bf16, 256, 64, 16, 1, 1024, 8, 4, 512, 8)        \
-  X(__bf16, 256, 64, 16, 2, 1024, 8, 2, 256, 8)        \
-  X(__bf16, 768, 64, 32, 1, 3072, 8, 2, 256, 5)
+#define EVO_SHAPES(X)                                     \
+  X(float, 64, 32, 8, 2, 256, 4, 2, 256, 8, 1)            \
+  X(__bf16, 64, 32, 8, 2, 256, 4, 2, 256, 8, 1)           \
+  X(float, 256, 64, 16, 1, 1024, 8, 4, 256, 8, 1)         \
+  X(float, 256, 64, 16, 2, 1024, 8, 2, 128, 8, 1)         \
+  X(__bf16, 256, 64, 16, 1, 1024, 8, 4, 512, 8, 1)        \
+  X(__bf16, 256, 64, 16, 2, 1024, 8, 2, 256, 8, 1)        \
+  X(__bf16, 768, 64, 32, 1, 3072, 8, 2, 256, 5, 1)        \
+  X(float, 256, 64, 16, 1, 1024, 4, 1, 256, 8, 4)         \
+  X(__bf16, 256, 64, 16, 1, 1024, 4, 1, 256, 8, 4)
 
 template <class AT> constexpr int dtype_of() { return std::is_same<AT, float>::value ? 0 : 1; }
 
-#define EVO_MATCH(AT, D, DH, HZ, SPT, DFF)                                                                 \
+#define EVO_MATCH(AT, D, DH, HZ, SPT, DFF, TEAM)                                                          \
   (key.d == D && key.dh == DH && key.horizon == HZ && key.d_ff == DFF && key.dtype == dtype_of<AT>() && \
-   key.spt == SPT)
+   key.spt == SPT && key.team == TEAM)
 
 bool kernel_available(const KernelKey& key, int* threads) {
-#define X(AT, D, DH, HZ, SPT, DFF, NW, HG, FC, SMAX) \
-  if (EVO_MATCH(AT, D, DH, HZ, SPT, DFF)) {          \
-    if (threads) *threads = NW * 64;                 \
-    return true;                                     \
+#define X(AT, D, DH, HZ, SPT, DFF, NW, HG, FC, SMAX, TEAM) \
+  if (EVO_MATCH(AT, D, DH, HZ, SPT, DFF, TEAM)) {          \
+    if (threads) *threads = NW * 64;                       \
+    return true;                                           \
   }
   EVO_SHAPES(X)
 #undef X
@@ -1058,8 +1181,8 @@ bool kernel_available(const KernelKey& key, int* threads) {
 }
 
 int kernel_max_obs_tokens_for(const KernelKey& key) {
-#define X(AT, D, DH, HZ, SPT, DFF, NW, HG, FC, SMAX) \
-  if (EVO_MATCH(AT, D, DH, HZ, SPT, DFF)) return (SMAX - 1) < 16 / SPT ? (SMAX - 1) : 16 / SPT;
+#define X(AT, D, DH, HZ, SPT, DFF, NW, HG, FC, SMAX, TEAM) \
+  if (EVO_MATCH(AT, D, DH, HZ, SPT, DFF, TEAM)) return (SMAX - 1) < 16 / SPT ? (SMAX - 1) : 16 / SPT;
   EVO_SHAPES(X)
 #undef X
   return 0;
@@ -1067,14 +1190,32 @@ int kernel_max_obs_tokens_for(const KernelKey& key) {
 
 int kernel_max_action_dim() { return 16; }
 
+int kernel_team_size(const KernelKey& key) {
+  int best = 1;
+#define X(AT, D, DH, HZ, SPT, DFF, NW, HG, FC, SMAX, TEAM) \
+  if (TEAM > 1 && key.d == D && key.dh == DH && key.horizon == HZ && key.d_ff == DFF &&      \
+      key.dtype == dtype_of<AT>() && key.spt == SPT)                                         \
+    best = TEAM;
+  EVO_SHAPES(X)
+#undef X
+  return best;
+}
+
 int kernel_max_steps_x_spt() { return kMaskEntries; }
 
 hipError_t launch_denoise(const KernelKey& key, const KParams& p, hipStream_t stream) {
-#define X(AT, D, DH, HZ, SPT, DFF, NW, HG, FC, SMAX)                                                      \
-  if (EVO_MATCH(AT, D, DH, HZ, SPT, DFF)) {                                                               \
-    hipLaunchKernelGGL((denoise_kernel<AT, D, DH, HZ, SPT, DFF, NW, HG, FC, SMAX>), dim3(p.n_tiles),      \
-                       dim3(NW * 64), 0, stream, p);                                                      \
-    return hipGetLastError();                                                                             \
+#define X(AT, D, DH, HZ, SPT, DFF, NW, HG, FC, SMAX, TEAM)                                                   \
+  if (EVO_MATCH(AT, D, DH, HZ, SPT, DFF, TEAM)) {                                                          \
+    const void* fn = reinterpret_cast<const void*>(&denoise_kernel<AT, D, DH, HZ, SPT, DFF, NW, HG, FC, SMAX, TEAM>); \
+    if (TEAM == 1) {                                                                                       \
+      hipLaunchKernelGGL((denoise_kernel<AT, D, DH, HZ, SPT, DFF, NW, HG, FC, SMAX, TEAM>), dim3(p.n_tiles), \
+                         dim3(NW * 64), 0, stream, p);                                                     \
+      return hipGetLastError();                                                                            \
+    }                                                                                                      \
+    /* team members wait for each other: all workgroups must be resident */                                \
+    KParams pc = p;                                                                                        \
+    void* args[] = {&pc};                                                                                  \
+    return hipLaunchCooperativeKernel(fn, dim3(p.n_tiles * TEAM), dim3(NW * 64), args, 0, stream);         \
   }
   EVO_SHAPES(X)
 #undef X

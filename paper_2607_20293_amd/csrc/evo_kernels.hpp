@@ -36,13 +36,17 @@ struct KParams {
   const float* noise;        // [T][batch][H][A]
   float* out;                // [batch][H][A]
   float* okv;                // [batch][L][n_obs][2d] observation-token keys/values
-  float* cache;              // [n_tiles][3L][rows*d] per-tile residual caches
-  int batch, pad2_;
+  float* cache;              // [n_tiles * team][3L][rows*d] per-workgroup residual caches
+  float* xchg;               // [n_tiles][2][team][rows*d] partial residuals of team members
+  unsigned* tctr;            // [n_tiles][16] team barrier counters (zeroed before each launch)
+  unsigned* derr;            // device error flag (team barrier timed out)
+  size_t okv_member_stride;  // floats between team members' observation key/value copies
+  int batch, team;
 };
 
 // Shape key of a compiled kernel instantiation.
 struct KernelKey {
-  int d, dh, horizon, d_ff, dtype, spt;
+  int d, dh, horizon, d_ff, dtype, spt, team;
 };
 
 // Returns true and the workgroup size if `key` is compiled.
@@ -66,5 +70,12 @@ hipError_t launch_time_kv(const float* raw, uint32_t pmem0, const uint32_t* wkv,
                           int T, int L, int D, int dtype, float* rows_scratch, float* tkv,
                           hipStream_t stream);
 hipError_t launch_ddpm_table(int T, float* table, hipStream_t stream);
+
+// team barrier counters must start at zero on every launch (a fill kernel,
+// not a memset node, so that the call may be captured into a graph)
+hipError_t launch_zero_u32(unsigned* dst, int n, hipStream_t stream);
+
+// team size of the small-batch variant for a shape (1: none compiled)
+int kernel_team_size(const KernelKey& key);
 
 }  // namespace evo

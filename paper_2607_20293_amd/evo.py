@@ -22,7 +22,8 @@ CODE_EVAL, CODE_STORE, CODE_REUSE, CODE_MERGED = 1, 2, 4, 8
 
 EXPORTED = ("evo_weight_count", "evo_check_desc", "evo_create_policy", "evo_set_schedule",
             "evo_set_schedule_pairs", "evo_denoise", "evo_get_stats", "evo_schedule_stats",
-            "evo_schedule_codes", "evo_debug_read_cache", "evo_destroy_policy", "evo_last_error")
+            "evo_schedule_codes", "evo_debug_read_cache", "evo_synchronize", "evo_destroy_policy",
+            "evo_last_error")
 
 
 class EvoError(RuntimeError):
@@ -42,7 +43,7 @@ class Stats(ctypes.Structure):
     _fields_ = [(n, ctypes.c_uint64) for n in (
         "refreshes_requested", "refreshes_effective", "flops_cacheable", "flops_always",
         "flops_full", "flops_kernel", "cache_bytes_read", "cache_bytes_written",
-        "weight_bytes", "n_tiles")]
+        "weight_bytes", "n_tiles", "n_workgroups")]
 
     def as_dict(self):
         return {n: int(getattr(self, n)) for n, _ in self._fields_}
@@ -83,6 +84,8 @@ def lib() -> ctypes.CDLL:
         L.evo_schedule_codes.restype = ctypes.c_int
         L.evo_debug_read_cache.argtypes = [P, I32, I32, P]
         L.evo_debug_read_cache.restype = ctypes.c_int
+        L.evo_synchronize.argtypes = [P]
+        L.evo_synchronize.restype = ctypes.c_int
         L.evo_destroy_policy.argtypes = [P]
         L.evo_destroy_policy.restype = None
         L.evo_last_error.argtypes = []
@@ -203,6 +206,11 @@ class Policy:
         st = torch.cuda.current_stream(obs.device) if stream is None else stream
         _check(lib().evo_denoise(self._h, B, po, pn, pid, pout, ctypes.c_void_p(st.cuda_stream)))
         return out
+
+    def synchronize(self):
+        """Wait for the last denoise call; raise if its kernel reported a
+        device-side failure (a timed-out team barrier)."""
+        _check(lib().evo_synchronize(self._h))
 
     def stats(self) -> dict:
         st = Stats()

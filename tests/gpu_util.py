@@ -32,6 +32,7 @@ def run_gpu(pol, inp_obs, inp_noise, ids):
     obs = torch.from_numpy(np.ascontiguousarray(inp_obs)).to(dev)
     noise = torch.from_numpy(np.ascontiguousarray(inp_noise)).to(dev)
     out = pol.denoise(obs, noise, ids)
+    pol.synchronize()
     torch.cuda.synchronize()
     return out.cpu().numpy().astype(np.float64), pol.stats()
 

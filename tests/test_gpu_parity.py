@@ -3,6 +3,8 @@ the same seeded inputs, plus the invariants of the cached loop that hold on
 the device (determinism, per-query reset, sample independence, cache
 contents).  Bars: fp32 max-abs <= 1e-4; bf16 normwise relative <= 3e-2;
 bookkeeping bit-exact."""
+import os
+
 import numpy as np
 import pytest
 
@@ -15,17 +17,29 @@ from tests.gpu_util import check_stats, compare, device, run_gpu, run_oracle, sa
 pytestmark = pytest.mark.gpu
 
 
-def _policy(shape, weights, dtype, max_batch, max_sched, cold=O.COLD_COMPUTE, clip=True):
+def _policy(shape, weights, dtype, max_batch, max_sched, cold=O.COLD_COMPUTE, clip=True, team=True):
+    """team=False creates the policy with the small-batch team variant
+    switched off (EVO_TEAM=0 is read at creation)."""
     device()
-    return evo.Policy(shape, weights, dtype=dtype, max_batch=max_batch, max_schedules=max_sched,
-                      cold_policy=cold, clip=clip)
+    old = os.environ.get("EVO_TEAM")
+    if not team:
+        os.environ["EVO_TEAM"] = "0"
+    try:
+        return evo.Policy(shape, weights, dtype=dtype, max_batch=max_batch, max_schedules=max_sched,
+                          cold_policy=cold, clip=clip)
+    finally:
+        if old is None:
+            os.environ.pop("EVO_TEAM", None)
+        else:
+            os.environ["EVO_TEAM"] = old
 
 
 def _case(name, shape, weights, obs, noise, lattices, ids, dtype, gran=O.GRAN_LAYER,
-          cold=O.COLD_COMPUTE, samples=None, max_batch=None, clip=True):
-    say(f"[gpu] {name}: dtype={dtype} batch={obs.shape[0]} schedules={len(lattices)} gran={gran} cold={cold}")
+          cold=O.COLD_COMPUTE, samples=None, max_batch=None, clip=True, team=True):
+    say(f"[gpu] {name}: dtype={dtype} batch={obs.shape[0]} schedules={len(lattices)} gran={gran} cold={cold} "
+        f"team={team}")
     B = obs.shape[0]
-    pol = _policy(shape, weights, dtype, max_batch or B, len(lattices), cold, clip)
+    pol = _policy(shape, weights, dtype, max_batch or B, len(lattices), cold, clip, team)
     for j, lt in enumerate(lattices):
         pol.set_schedule(j, lt, gran)
     got, gst = run_gpu(pol, obs, noise, ids)
@@ -75,6 +89,51 @@ def test_pusht_b1(name):
     inp = I.make_inputs(w)
     pol, *_ = _case(name, w.shape, inp.weights, inp.obs, inp.noise, inp.lattices, inp.ids, w.dtype)
     pol.close()
+
+
+@pytest.mark.parametrize("name", ["pusht_fp32_b1_d25", "pusht_bf16_b1_d25"])
+def test_pusht_b1_single_workgroup(name):
+    """The same batch-1 queries with the team variant switched off: one
+    workgroup per tile."""
+    w = I.WORKLOADS[name]
+    inp = I.make_inputs(w)
+    pol, got, gst, _ = _case(name + "_noteam", w.shape, inp.weights, inp.obs, inp.noise, inp.lattices, inp.ids,
+                             w.dtype, team=False)
+    assert gst["n_workgroups"] == gst["n_tiles"] == 1
+    pol.close()
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_team_variant_matches_single_workgroup(dtype):
+    """Batches of at most n_cu/4 samples run four workgroups per one-sample
+    tile (heads and d_ff chunks split among them, partial residuals summed
+    through memory).  Both variants match the oracle on a ragged batch with
+    mixed unit-granular schedules, and each other to summation order."""
+    s = I.PUSHT
+    wts = I.make_weights(s, 6, "perturbed")
+    B = 7
+    obs, noise = I.make_obs(s, B, 6), I.make_noise(s, B, 6)
+    rng = np.random.default_rng([6, 3])
+    lats = [I.lattice_bernoulli(3 * s.n_layers, s.n_steps, p, rng) for p in (0.1, 0.3, 0.6)]
+    ids = np.array([0, 1, 2, 2, 1, 0, 1], np.int32)
+    pol_t, got_t, st_t, _ = _case(f"team_{dtype}", s, wts, obs, noise, lats, ids, dtype, gran=O.GRAN_UNIT,
+                                  samples=[0, 3, 6])
+    pol_1, got_1, st_1, _ = _case(f"noteam_{dtype}", s, wts, obs, noise, lats, ids, dtype, gran=O.GRAN_UNIT,
+                                  samples=[0, 3, 6], team=False)
+    assert st_t["n_tiles"] == st_1["n_tiles"] == B
+    assert st_1["n_workgroups"] == B
+    assert st_t["n_workgroups"] in (B, 4 * B)
+    if st_t["n_workgroups"] == 4 * B:
+        assert st_t["cache_bytes_written"] == 4 * st_1["cache_bytes_written"]
+    d = float(np.max(np.abs(got_t - got_1)))
+    say(f"  team vs single workgroup: max-abs diff {d:.3e}")
+    if dtype == "fp32":
+        assert d <= 1e-4
+    # repeated team calls are bitwise reproducible
+    again, _ = run_gpu(pol_t, obs, noise, ids)
+    assert np.array_equal(again, got_t)
+    pol_t.close()
+    pol_1.close()
 
 
 @pytest.mark.parametrize("name", ["pusht_fp32_b64_d25", "pusht_bf16_b64_d25", "pusht_bf16_b64_all"])
@@ -150,7 +209,7 @@ def test_two_sample_tiles_match_single_sample_tiles():
     s = w.shape
     inp = I.make_inputs(w)
     say("[gpu] two-sample tiles vs single-sample tiles")
-    pol = _policy(s, inp.weights, "bf16", 512, 64)
+    pol = _policy(s, inp.weights, "bf16", 512, 64, team=False)
     for j, lt in enumerate(inp.lattices):
         pol.set_schedule(j, lt, O.GRAN_LAYER)
     big, st = run_gpu(pol, inp.obs, inp.noise, inp.ids)
@@ -186,7 +245,8 @@ def test_step0_only_cache_holds_step0_residuals(dtype):
         worst = max(worst, e / scale)
         assert (e <= 1e-4) if dtype == "fp32" else (e / scale <= 3e-2), (b, e)
     say(f"  cache readback worst relative error {worst:.2e}")
-    assert gst["cache_bytes_written"] == 3 * s.n_layers * s.horizon * s.d_model * 4
+    per_wg = gst["n_workgroups"] // gst["n_tiles"]
+    assert gst["cache_bytes_written"] == 3 * s.n_layers * s.horizon * s.d_model * 4 * per_wg
     pol.close()
 
 
