@@ -304,7 +304,7 @@ int evo_create_policy(const evo_policy_desc* desc, const float* host_weights, si
     CREATE_TRY(hipMalloc(&p->d_okv,
                          std::max((size_t)s.max_batch * okv_per, p->okv_stride * p->team) * sizeof(float)));
     if (p->team > 1) {
-      CREATE_TRY(hipMalloc(&p->d_xchg, (size_t)p->team_batch * 2 * p->team * s.H * d * sizeof(float)));
+      CREATE_TRY(hipMalloc(&p->d_xchg, (size_t)p->team_batch * 3 * p->team * s.H * d * sizeof(float)));
       CREATE_TRY(hipMalloc(&p->d_tctr, (size_t)p->team_batch * 16 * sizeof(unsigned)));
       CREATE_TRY(hipMalloc(&p->d_derr, sizeof(unsigned)));
       CREATE_TRY(hipMemset(p->d_derr, 0, sizeof(unsigned)));

@@ -191,7 +191,7 @@ struct Cfg {
   static constexpr int SLOTS = 16 / SPB;               // memory columns per sample in a 16-wide tile
   static constexpr int PS = 17;                        // stride of a 16x16 fp32 scratch tile
   static constexpr int PWN = (NJB > RB ? NJB : RB) * 16 * PS;
-  static constexpr int NB = (4 / (CBW * RB)) > 0 ? (4 / (CBW * RB)) : 1;  // reuse loads per batch
+  static constexpr int NB = (8 / (CBW * RB)) > 0 ? (8 / (CBW * RB)) : 1;  // reuse loads per batch
 };
 
 // LayerNorm statistics of the tile rows from the register-resident stream:
@@ -389,7 +389,48 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) jrow[rb] = (rb * 16 + lq * 4) / HZ;
   float* cbase = p.cache + (size_t)(tile * TEAM + member) * U * (R * D);
-  int nbar = 0, xpar = 0;  // team barriers passed, exchange buffer parity
+  // Team exchange slots: [tile][3][TEAM][R*D] floats, slot n % 3 carries
+  // the partials of the n-th evaluated unit.  A slot word that still holds
+  // the sentinel has not been written yet; every member resets its own slot
+  // of unit n-1 once it holds all partials of unit n (then every member has
+  // finished reading unit n-1), which is the slot's next use at unit n+2.
+  constexpr int kCoherent = 16;            // SC1 cache-policy bit: device-coherent access
+  constexpr unsigned kEmpty = 0xFFFFFFFFu;  // never produced by arithmetic (canonical NaN differs)
+  int nbar = 0;                             // evaluated units exchanged so far
+  float* const xb = TEAM > 1 ? p.xchg + (size_t)tile * (3 * TEAM) * (R * D) : nullptr;
+  const auto xr = __builtin_amdgcn_make_buffer_rsrc(xb, (short)0, TEAM > 1 ? 3 * TEAM * R * D * 4 : 0, 0x00020000);
+  const auto xoff = [&](int slot, int m, int c, int rb) {
+    return ((slot * TEAM + m) * (R * D) + (((w * RB + rb) * CBW + c) * 64 + lane) * 4) * 4;
+  };
+  if constexpr (TEAM > 1) {
+    // all three slots of this member start empty; one counter barrier makes
+    // sure no member reads a slot before its owner has emptied it
+    const u32x4 empty = {kEmpty, kEmpty, kEmpty, kEmpty};
+#pragma unroll
+    for (int sl = 0; sl < 3; ++sl)
+#pragma unroll
+      for (int c = 0; c < CBW; ++c)
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb)
+          __builtin_amdgcn_raw_buffer_store_b128(empty, xr, xoff(sl, member, c, rb), 0, kCoherent);
+    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
+    __syncthreads();
+    if (tid == 0) {
+      unsigned* ctr = p.tctr + (size_t)tile * 16;
+      __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      unsigned spins = 0;
+      while (__hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < (unsigned)TEAM) {
+        if (__hip_atomic_load(p.derr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u || ++spins > (1u << 22)) {
+          __hip_atomic_store(p.derr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          s_abort = 1;
+          break;
+        }
+        __builtin_amdgcn_s_sleep(1);
+      }
+    }
+    __syncthreads();
+    if (s_abort) return;
+  }
   const auto cfrag = [&](int unit, int c, int rb) {
     return reinterpret_cast<f32x4*>(cbase + (size_t)unit * (R * D) +
                                     ((size_t)((w * RB + rb) * CBW + c) * 64 + lane) * 4);
@@ -400,11 +441,13 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
   uint4 win[KEEP_EMB ? CBW : 1];
   f32x4 pb[KEEP_EMB ? CBW : 1][KEEP_EMB ? RB : 1];
   float lfg[KEEP_EMB ? CBW : 1], lfb[KEEP_EMB ? CBW : 1];
+  uint4 wout[KEEP_EMB ? CBW : 1];
   if constexpr (KEEP_EMB) {
 #pragma unroll
     for (int c = 0; c < CBW; ++c) {
       const int col = (w * CBW + c) * 16 + lc;
       win[c] = pk[p.pk_win + (size_t)(w * CBW + c) * 64 + lane];
+      wout[c] = pk[p.pk_wout + (size_t)(w * CBW + c) * 64 + lane];
       const float bi = raw[p.b_in + col];
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb)
@@ -457,6 +500,11 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
     return hi_m & ~lo_m;
   };
   uint64_t mru_cur[SPT];
+  // The loads of a batch are issued unconditionally (an entry that is not
+  // needed reads past the end of a buffer resource, which returns zeros
+  // without a memory access), so that they are all in flight before the
+  // first is consumed.
+  const auto crs = __builtin_amdgcn_make_buffer_rsrc(cbase, (short)0, U * (R * D) * 4, 0x00020000);
   const auto issue_batch = [&](uint64_t& um, auto& ub, auto& v) {
 #pragma unroll
     for (int q = 0; q < NB; ++q) {
@@ -473,8 +521,9 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
 #pragma unroll
           for (int jj = 1; jj < SPT; ++jj)
             if (jrow[rb] == jj) mj = mru_cur[jj];
-          v[q][c][rb] = f32x4{0.f, 0.f, 0.f, 0.f};
-          if (ub[q] >= 0 && ((mj >> ub[q]) & 1ull)) v[q][c][rb] = *cfrag(ub[q], c, rb);
+          const bool use = ub[q] >= 0 && ((mj >> ub[q]) & 1ull);
+          const int off = use ? (ub[q] * (R * D) + (((w * RB + rb) * CBW + c) * 64 + lane) * 4) * 4 : 0x7FFFFFF0;
+          v[q][c][rb] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(crs, off, 0, 0));
         }
   };
 
@@ -525,8 +574,9 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
       if (f < U && !(loaded_t == t && loaded_u == f)) load_unit_params(t, f);
     }
     // sampler constants and head bias of this step's update (prefetched)
-    const float* dd = p.ddpm + (size_t)k * 8;
-    const float s1 = dd[0], sa = dd[1], c0 = dd[2], ct = dd[3], sg = dd[4];
+    // (a lane-indexed vector load: a uniform scalar load would be waited for
+    // by the next LDS access)
+    const float ddl = lane < 5 ? p.ddpm[(size_t)k * 8 + lane] : 0.f;
     float bout[ZPT];
 #pragma unroll
     for (int q = 0; q < ZPT; ++q) {
@@ -636,17 +686,19 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
 #pragma unroll
             for (int rb = 0; rb < RB; ++rb) y[m][rb] = f32x4{0.f, 0.f, 0.f, 0.f};
           if (g != member) gemm_pref<MPWQ>(b1q, pk + po.qkv, D / O::KF, 0, gcb_sa(g), lane);
+          float bq[MPWQ];  // stage-1 biases, requested before the GEMM so their latency is hidden
+#pragma unroll
+          for (int m = 0; m < MPWQ; ++m) bq[m] = raw[lo.b_qkv + gcb_sa(g)(m) * 16 + lc];
           gemm_run<AT, RB, MPWQ, D / O::KF, INFL>(y, xa, LDA, pk + po.qkv, D / O::KF, 0, gcb_sa(g), lane, b1q);
           uint4 b2[CBW];
           gemm_pref<CBW>(b2, pk + po.o, D / O::KF, g * (GW / O::KF), own, lane);
 #pragma unroll
           for (int m = 0; m < MPWQ; ++m) {
-            const int loc = (w + NW * m) * 16 + lc, gcol = gcb_sa(g)(m) * 16 + lc;
-            const float bq = raw[lo.b_qkv + gcol];
+            const int loc = (w + NW * m) * 16 + lc;
 #pragma unroll
             for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-              for (int i = 0; i < 4; ++i) ybuf[(rb * 16 + lq * 4 + i) * LDY + loc] = y[m][rb][i] + bq;
+              for (int i = 0; i < 4; ++i) ybuf[(rb * 16 + lq * 4 + i) * LDY + loc] = y[m][rb][i] + bq[m];
           }
           __syncthreads();
           // scores, softmax and values on fp32 MFMA tiles: wave per (head, query block)
@@ -747,17 +799,19 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
 #pragma unroll
             for (int rb = 0; rb < RB; ++rb) y[m][rb] = f32x4{0.f, 0.f, 0.f, 0.f};
           if (g != member) gemm_pref<MPWC>(b1c, pk + po.q, D / O::KF, 0, gcb_ca(g), lane);
+          float bq[MPWC];
+#pragma unroll
+          for (int m = 0; m < MPWC; ++m) bq[m] = raw[lo.b_q + gcb_ca(g)(m) * 16 + lc];
           gemm_run<AT, RB, MPWC, D / O::KF, INFL>(y, xa, LDA, pk + po.q, D / O::KF, 0, gcb_ca(g), lane, b1c);
           uint4 b2[CBW];
           gemm_pref<CBW>(b2, pk + po.o2, D / O::KF, g * (GW / O::KF), own, lane);
 #pragma unroll
           for (int m = 0; m < MPWC; ++m) {
-            const int loc = (w + NW * m) * 16 + lc, gcol = gcb_ca(g)(m) * 16 + lc;
-            const float bq = raw[lo.b_q + gcol];
+            const int loc = (w + NW * m) * 16 + lc;
 #pragma unroll
             for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-              for (int i = 0; i < 4; ++i) ybuf[(rb * 16 + lq * 4 + i) * LDY + loc] = y[m][rb][i] + bq;
+              for (int i = 0; i < 4; ++i) ybuf[(rb * 16 + lq * 4 + i) * LDY + loc] = y[m][rb][i] + bq[m];
           }
 #pragma unroll
           for (int q = 0; q < KVQ; ++q)
@@ -822,18 +876,20 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
 #pragma unroll
             for (int rb = 0; rb < RB; ++rb) y[m][rb] = f32x4{0.f, 0.f, 0.f, 0.f};
           if (ch != member) gemm_pref<MPWF>(b1f, pk + po.w1, D / O::KF, 0, gcb_ff(ch), lane);
+          float b1v[MPWF];
+#pragma unroll
+          for (int m = 0; m < MPWF; ++m) b1v[m] = raw[lo.b_1 + ch * FC + (w + NW * m) * 16 + lc];
           gemm_run<AT, RB, MPWF, D / O::KF, INFL>(y, xa, LDA, pk + po.w1, D / O::KF, 0, gcb_ff(ch), lane, b1f);
           uint4 b2[CBW];
           gemm_pref<CBW>(b2, pk + po.w2, DFF / O::KF, ch * (FC / O::KF), own, lane);
 #pragma unroll
           for (int m = 0; m < MPWF; ++m) {
             const int loc = (w + NW * m) * 16 + lc;
-            const float b1 = raw[lo.b_1 + ch * FC + loc];
 #pragma unroll
             for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
               for (int i = 0; i < 4; ++i)
-                O::store(zbuf, LDZ, rb * 16 + lq * 4 + i, loc, gelu_erf(y[m][rb][i] + b1));
+                O::store(zbuf, LDZ, rb * 16 + lq * 4 + i, loc, gelu_erf(y[m][rb][i] + b1v[m]));
           }
           __syncthreads();
           gemm_run<AT, RB, CBW, FC / O::KF, INFL>(r, zbuf, LDZ, pk + po.w2, DFF / O::KF, ch * (FC / O::KF), own, lane, b2);
@@ -853,64 +909,75 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
       if constexpr (TEAM > 1) {
         // Sum the members' partial residuals in member order, so that every
         // member obtains the same bits.  The partials travel through memory
-        // with device-coherent (SC1) buffer stores and loads, which do not
-        // leave stale or dirty lines in the per-XCD caches; the barrier thus
-        // needs no cache write-back or invalidation (the weight stream stays
-        // in L2).  Ordering: a member's stores have completed (vmcnt 0)
-        // before its counter increment, and the partials are loaded only
-        // after the counter has shown every member.
-        constexpr int kCoherent = 16;  // SC1 cache-policy bit
-        float* xb = p.xchg + (size_t)tile * (2 * TEAM) * (R * D);
-        const auto xr = __builtin_amdgcn_make_buffer_rsrc(xb, (short)0, 2 * TEAM * R * D * 4, 0x00020000);
-        const auto xoff = [&](int slot, int c, int rb) {
-          return (slot * (R * D) + (((w * RB + rb) * CBW + c) * 64 + lane) * 4) * 4;
-        };
-#pragma unroll
-        for (int c = 0; c < CBW; ++c)
-#pragma unroll
-          for (int rb = 0; rb < RB; ++rb)
-            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, r[c][rb]), xr,
-                                                   xoff(xpar * TEAM + member, c, rb), 0, kCoherent);
-        __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this wave's partials are written
-        request_next_params();
-        __syncthreads();
-        ++nbar;
-        if (tid == 0) {
-          unsigned* ctr = p.tctr + (size_t)tile * 16;
-          __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          const unsigned target = (unsigned)(nbar * TEAM);
-          unsigned spins = 0;
-          while (__hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
-            // bounded wait: a member that never arrives ends the whole kernel
-            if (__hip_atomic_load(p.derr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u ||
-                ++spins > (1u << 22)) {
-              __hip_atomic_store(p.derr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-              s_abort = 1;
-              break;
-            }
-            __builtin_amdgcn_s_sleep(1);
-          }
-        }
-        __syncthreads();
-        if (s_abort) return;
-        u32x4 part[TEAM][CBW][RB];
-#pragma unroll
-        for (int m = 0; m < TEAM; ++m)
-#pragma unroll
-          for (int c = 0; c < CBW; ++c)
-#pragma unroll
-            for (int rb = 0; rb < RB; ++rb)
-              part[m][c][rb] = __builtin_amdgcn_raw_buffer_load_b128(xr, xoff(xpar * TEAM + m, c, rb), 0, kCoherent);
+        // with device-coherent (SC1) buffer stores and loads, which leave no
+        // stale or dirty lines in the per-XCD caches (the weight stream stays
+        // in L2).  Each thread waits only for the words it sums: a word is
+        // ready once it no longer holds the sentinel.  Waits are bounded;
+        // on a timeout the device error flag is set and every later wait
+        // ends at once, so the kernel always finishes.
+        const int cur = nbar % 3, prev = (nbar + 2) % 3;
+        __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): the reset of this slot (one unit ago) has landed
 #pragma unroll
         for (int c = 0; c < CBW; ++c)
 #pragma unroll
           for (int rb = 0; rb < RB; ++rb) {
-            f32x4 acc = __builtin_bit_cast(f32x4, part[0][c][rb]);
+            u32x4 v = __builtin_bit_cast(u32x4, r[c][rb]);
 #pragma unroll
-            for (int m = 1; m < TEAM; ++m) acc += __builtin_bit_cast(f32x4, part[m][c][rb]);
+            for (int q = 0; q < 4; ++q) v[q] = v[q] == kEmpty ? 0x7FC00000u : v[q];
+            __builtin_amdgcn_raw_buffer_store_b128(v, xr, xoff(cur, member, c, rb), 0, kCoherent);
+          }
+        request_next_params();
+        u32x4 part[TEAM][CBW][RB];
+        unsigned pending = ((1u << TEAM) - 1u) & ~(1u << member);
+        unsigned spins = 0;
+        while (true) {
+#pragma unroll
+          for (int m = 0; m < TEAM; ++m)
+            if (pending >> m & 1u) {
+#pragma unroll
+              for (int c = 0; c < CBW; ++c)
+#pragma unroll
+                for (int rb = 0; rb < RB; ++rb)
+                  part[m][c][rb] = __builtin_amdgcn_raw_buffer_load_b128(xr, xoff(cur, m, c, rb), 0, kCoherent);
+            }
+#pragma unroll
+          for (int m = 0; m < TEAM; ++m)
+            if (pending >> m & 1u) {
+              bool ok = true;
+#pragma unroll
+              for (int c = 0; c < CBW; ++c)
+#pragma unroll
+                for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+                  for (int q = 0; q < 4; ++q) ok = ok && part[m][c][rb][q] != kEmpty;
+              if (ok) pending &= ~(1u << m);
+            }
+          if (!pending) break;
+          if (__hip_atomic_load(p.derr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u || ++spins > (1u << 20)) {
+            __hip_atomic_store(p.derr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            break;
+          }
+          __builtin_amdgcn_s_sleep(1);
+        }
+#pragma unroll
+        for (int c = 0; c < CBW; ++c)
+#pragma unroll
+          for (int rb = 0; rb < RB; ++rb) {
+            f32x4 acc = member == 0 ? r[c][rb] : __builtin_bit_cast(f32x4, part[0][c][rb]);
+#pragma unroll
+            for (int m = 1; m < TEAM; ++m)
+              acc += member == m ? r[c][rb] : __builtin_bit_cast(f32x4, part[m][c][rb]);
             r[c][rb] = acc;
           }
-        xpar ^= 1;
+        // every member has read the partials of the previous unit: empty
+        // this member's slot of it for its next use
+        const u32x4 empty = {kEmpty, kEmpty, kEmpty, kEmpty};
+#pragma unroll
+        for (int c = 0; c < CBW; ++c)
+#pragma unroll
+          for (int rb = 0; rb < RB; ++rb)
+            __builtin_amdgcn_raw_buffer_store_b128(empty, xr, xoff(prev, member, c, rb), 0, kCoherent);
+        ++nbar;
       } else {
         request_next_params();
       }
@@ -972,7 +1039,9 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
           g_ = raw[p.lnf_g + col];
           b_ = raw[p.lnf_b + col];
         }
-        const uint4 wo = pk[p.pk_wout + (size_t)(w * CBW + c) * 64 + lane];
+        uint4 wo;
+        if constexpr (KEEP_EMB) wo = wout[c];
+        else wo = pk[p.pk_wout + (size_t)(w * CBW + c) * 64 + lane];
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
@@ -1004,6 +1073,8 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
 #pragma unroll
           for (int ww = 0; ww < NW; ++ww) part += epsp[(ww * R + row) * 16 + a];
           const float e = bout[q] + part;
+          const auto dd = [&](int i) { return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(ddl), i)); };
+          const float s1 = dd(0), sa = dd(1), c0 = dd(2), ct = dd(3), sg = dd(4);
           float* xp = xs + row * 16 + OF::pcol(a);
           const float x = *xp;
           float x0 = (x - s1 * e) / sa;

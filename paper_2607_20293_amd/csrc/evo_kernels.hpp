@@ -37,7 +37,7 @@ struct KParams {
   float* out;                // [batch][H][A]
   float* okv;                // [batch][L][n_obs][2d] observation-token keys/values
   float* cache;              // [n_tiles * team][3L][rows*d] per-workgroup residual caches
-  float* xchg;               // [n_tiles][2][team][rows*d] partial residuals of team members
+  float* xchg;               // [n_tiles][3][team][rows*d] partial residuals of team members
   unsigned* tctr;            // [n_tiles][16] team barrier counters (zeroed before each launch)
   unsigned* derr;            // device error flag (team barrier timed out)
   size_t okv_member_stride;  // floats between team members' observation key/value copies
