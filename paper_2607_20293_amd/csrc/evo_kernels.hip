@@ -113,35 +113,56 @@ template <> struct Op<float> {
   }
 };
 
-// First weight fragments of a product (issued ahead of the product).
-template <int MPW, class GCB>
-__device__ __forceinline__ void gemm_pref(uint4 (&bc)[MPW], const uint4* W, int KBT, int kf0, GCB gcb, int lane) {
+// k-steps a product keeps in flight: about INFL 1 KiB fragments per wave
+template <int MPW, int NKF, int INFL>
+constexpr int pd_of() {
+  constexpr int pd0 = INFL / MPW > 0 ? INFL / MPW : 1;
+  return pd0 < NKF ? pd0 : (NKF > 1 ? NKF - 1 : 1);
+}
+// k-steps requested ahead of a product (before the phase that precedes it):
+// about PF fragments per wave, at least one k-step, at most the in-flight depth
+template <int MPW, int NKF, int INFL, int PF>
+constexpr int np_of() {
+  constexpr int n = PF / MPW > 0 ? PF / MPW : 1;
+  constexpr int pd = pd_of<MPW, NKF, INFL>();
+  return n < pd ? n : pd;
+}
+
+// First NP k-steps of weight fragments of a product (issued ahead of it).
+template <int NP, int MPW, class GCB>
+__device__ __forceinline__ void gemm_pref(uint4 (&bc)[NP][MPW], const uint4* W, int KBT, int kf0, GCB gcb,
+                                          int lane) {
 #pragma unroll
-  for (int m = 0; m < MPW; ++m) bc[m] = W[((size_t)gcb(m) * KBT + kf0) * 64 + lane];
+  for (int d = 0; d < NP; ++d)
+#pragma unroll
+    for (int m = 0; m < MPW; ++m) bc[d][m] = W[((size_t)gcb(m) * KBT + kf0 + d) * 64 + lane];
 }
 
 // acc[m][rb] += A[rb*16 .. +16][k-range] x W[col block gcb(m)][k-range]^T
 // A: LDS operand, row stride lda elements, offset to the k-range start.
 // W: packed fragments of a matrix with KBT fragments per column block; kf0
 // is the first fragment of the k-range, NKF its length; bc holds the
-// fragments of kf0 (gemm_pref).  Weight fragments are requested PD k-steps
-// ahead of their MFMAs (about INFL 1 KiB fragments in flight per wave); a
-// scheduling fence per step keeps the compiler from hoisting further loads.
-template <class AT, int RBk, int MPW, int NKF, int INFL, class GCB>
+// fragments of the first NP k-steps (gemm_pref).  Weight fragments are
+// requested PD k-steps ahead of their MFMAs (about INFL 1 KiB fragments in
+// flight per wave); a scheduling fence per step keeps the compiler from
+// hoisting further loads.
+template <class AT, int RBk, int MPW, int NKF, int INFL, int NP, class GCB>
 __device__ __forceinline__ void gemm_run(f32x4 (&acc)[MPW][RBk], const AT* A, int lda, const uint4* W, int KBT,
-                                         int kf0, GCB gcb, int lane, uint4 (&bc)[MPW]) {
+                                         int kf0, GCB gcb, int lane, uint4 (&bc)[NP][MPW]) {
   using O = Op<AT>;
-  constexpr int PD0 = INFL / MPW > 0 ? INFL / MPW : 1;
-  constexpr int PD = PD0 < NKF ? PD0 : (NKF > 1 ? NKF - 1 : 1);
+  constexpr int PD = pd_of<MPW, NKF, INFL>();
+  static_assert(NP >= 1 && NP <= PD, "prefetched k-steps");
   const int lc = lane & 15, lq = lane >> 4;
   const uint4* wp[MPW];
 #pragma unroll
   for (int m = 0; m < MPW; ++m) wp[m] = W + ((size_t)gcb(m) * KBT + kf0) * 64 + lane;
   uint4 buf[PD + 1][MPW];
 #pragma unroll
-  for (int m = 0; m < MPW; ++m) buf[0][m] = bc[m];
+  for (int d = 0; d < NP; ++d)
 #pragma unroll
-  for (int d = 1; d < PD; ++d)
+    for (int m = 0; m < MPW; ++m) buf[d][m] = bc[d][m];
+#pragma unroll
+  for (int d = NP; d < PD; ++d)
 #pragma unroll
     for (int m = 0; m < MPW; ++m)
       if (d < NKF) buf[d][m] = wp[m][d * 64];
@@ -166,12 +187,33 @@ __device__ __forceinline__ void gemm_run(f32x4 (&acc)[MPW][RBk], const AT* A, in
 template <class AT, int RBk, int MPW, int NKF, class GCB>
 __device__ __forceinline__ void gemm_acc(f32x4 (&acc)[MPW][RBk], const AT* A, int lda, const uint4* W, int KBT,
                                          int kf0, GCB gcb, int lane) {
-  uint4 bc[MPW];
-  gemm_pref<MPW>(bc, W, KBT, kf0, gcb, lane);
-  gemm_run<AT, RBk, MPW, NKF, 6>(acc, A, lda, W, KBT, kf0, gcb, lane, bc);
+  uint4 bc[1][MPW];
+  gemm_pref<1, MPW>(bc, W, KBT, kf0, gcb, lane);
+  gemm_run<AT, RBk, MPW, NKF, 6, 1>(acc, A, lda, W, KBT, kf0, gcb, lane, bc);
 }
 
-__device__ __forceinline__ float gelu_erf(float v) { return 0.5f * v * (1.0f + erff(v * 0.70710678118654752f)); }
+// Hardware transcendental approximations (v_rsq_f32, v_exp_f32, v_rcp_f32;
+// about 1 ulp).  The phases around the matrix products run at one or two
+// waves per SIMD, where every dependent instruction is exposed latency; the
+// correctly rounded library sequences cost tens of instructions each.
+__device__ __forceinline__ float fast_rsqrt(float x) { return __builtin_amdgcn_rsqf(x); }
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+__device__ __forceinline__ float fast_rcp(float x) { return __builtin_amdgcn_rcpf(x); }
+constexpr float kLog2e = 1.4426950408889634f;
+
+// GELU with the error function (0.5 v (1 + erf(v / sqrt 2))).  erfc(x) for
+// x >= 0 uses the rational-exponential approximation of Abramowitz and
+// Stegun, Handbook of Mathematical Functions, formula 7.1.26 (absolute error
+// below 1.5e-7); 1 + erf(v/sqrt2) is then erfc(|x|) for v < 0 and
+// 2 - erfc(|x|) for v >= 0, which avoids cancellation on the negative side.
+__device__ __forceinline__ float gelu_erf(float v) {
+  const float x = fabsf(v) * 0.70710678118654752f;
+  const float t = fast_rcp(1.0f + 0.3275911f * x);
+  const float poly =
+      t * (0.254829592f + t * (-0.284496736f + t * (1.421413741f + t * (-1.453152027f + t * 1.061405429f))));
+  const float q = poly * fast_exp2(-x * x * kLog2e);  // erfc(x)
+  return 0.5f * v * (v >= 0.f ? 2.0f - q : q);
+}
 
 template <int D, int DH, int HZ, int SPT, int DFF, int NW, int HG, int FC, int SMAX, int TEAM>
 struct Cfg {
@@ -250,7 +292,7 @@ __device__ __forceinline__ void ln_stats(const f32x4 (&h)[C::CBW][C::RB], float 
         n = tot;
       }
       mu[rb][i] = M;
-      rs[rb][i] = 1.0f / sqrtf(Q * (1.0f / D) + 1e-5f);
+      rs[rb][i] = fast_rsqrt(Q * (1.0f / D) + 1e-5f);
     }
 }
 
@@ -271,7 +313,11 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
   static_assert(16 * LDO * (int)sizeof(AT) <= R * LDY * 4, "observation operand must fit");
   static_assert(SMAX <= SLOTS, "memory tokens per sample must fit a 16-column tile");
   static_assert(DH % 16 == 0, "head dim");
-  constexpr bool KEEP_EMB = RB == 1 && CBW <= 4;  // embedding constants kept in registers across steps
+  // embedding / head constants of the lane's columns, kept across steps in
+  // LDS (EMB_LDS, where it fits) or in registers (KEEP_EMB), else re-read
+  constexpr bool EMB_LDS = RB == 1 && CBW <= 4 && (sizeof(AT) == 2 || TEAM > 1 || D <= 64);
+  constexpr bool KEEP_EMB = RB == 1 && CBW <= 4 && !EMB_LDS;
+  constexpr bool PB_LDS = EMB_LDS && (TEAM > 1 || D <= 64);  // else the row biases stay in registers
   // layer-merged residual sum accumulated in registers, else in its cache slot
   constexpr bool MAC_REG = CBW * RB <= 4;
   // weight fragments in flight per wave in the unit products
@@ -291,7 +337,14 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
   __shared__ PackOff s_poff[kMaxLayers];
   __shared__ int smp[SPT];
 
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, lc = lane & 15, lq = lane >> 4;
+  const int tid = threadIdx.x, w = tid >> 6;
+  // lane indices are made opaque to the optimiser (an empty asm) once per
+  // step, unit, head group and d_ff chunk, so that the address arithmetic
+  // derived from them is recomputed inside the loops instead of being
+  // hoisted into registers held for the whole kernel (which spilled); the
+  // one-wave-per-SIMD team variant has accumulation registers to spare and
+  // keeps the hoisted form
+  int lane = tid & 63, lc = lane & 15, lq = lane >> 4;
   // a team of TEAM workgroups shares a tile: each member evaluates its share
   // of every unit's head groups / d_ff chunks and the partial residuals are
   // summed through HBM; everything else is replicated in every member
@@ -437,24 +490,42 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
   };
   const uint4* pk = p.pk;
 
-  // embedding / head constants of this lane's columns
-  uint4 win[KEEP_EMB ? CBW : 1];
-  f32x4 pb[KEEP_EMB ? CBW : 1][KEEP_EMB ? RB : 1];
-  float lfg[KEEP_EMB ? CBW : 1], lfb[KEEP_EMB ? CBW : 1];
-  uint4 wout[KEEP_EMB ? CBW : 1];
-  if constexpr (KEEP_EMB) {
+  // embedding / head constants of this lane's columns (each lane writes and
+  // later reads only its own LDS entries, so no barrier is needed)
+  __shared__ uint4 s_win[EMB_LDS ? CB * 64 : 1], s_wout[EMB_LDS ? CB * 64 : 1];
+  __shared__ f32x4 s_pb[PB_LDS ? CB * 64 : 1];
+  __shared__ float s_lf[EMB_LDS ? 2 * D : 1];
+  constexpr int KE = KEEP_EMB ? CBW : 1, KP = (KEEP_EMB || (EMB_LDS && !PB_LDS)) ? CBW : 1;
+  uint4 win[KE], wout[KE];
+  f32x4 pb[KP][KP > 1 ? RB : 1];
+  float lfg[KE], lfb[KE];
+  if constexpr (KEEP_EMB || EMB_LDS) {
 #pragma unroll
     for (int c = 0; c < CBW; ++c) {
-      const int col = (w * CBW + c) * 16 + lc;
-      win[c] = pk[p.pk_win + (size_t)(w * CBW + c) * 64 + lane];
-      wout[c] = pk[p.pk_wout + (size_t)(w * CBW + c) * 64 + lane];
+      const int col = (w * CBW + c) * 16 + lc, fi = (w * CBW + c) * 64 + lane;
+      const uint4 wi = pk[p.pk_win + (size_t)fi], wo = pk[p.pk_wout + (size_t)fi];
       const float bi = raw[p.b_in + col];
+      f32x4 pv[RB];
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) pb[c][rb][i] = bi + raw[p.P_act + (size_t)((rb * 16 + lq * 4 + i) % HZ) * D + col];
-      lfg[c] = raw[p.lnf_g + col];
-      lfb[c] = raw[p.lnf_b + col];
+        for (int i = 0; i < 4; ++i) pv[rb][i] = bi + raw[p.P_act + (size_t)((rb * 16 + lq * 4 + i) % HZ) * D + col];
+      const float g_ = raw[p.lnf_g + col], b_ = raw[p.lnf_b + col];
+      if constexpr (EMB_LDS) {
+        s_win[fi] = wi;
+        s_wout[fi] = wo;
+        if constexpr (PB_LDS) s_pb[fi] = pv[0];
+        else pb[c][0] = pv[0];
+        s_lf[col] = g_;
+        s_lf[D + col] = b_;
+      } else {
+        win[c] = wi;
+        wout[c] = wo;
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) pb[c][rb] = pv[rb];
+        lfg[c] = g_;
+        lfb[c] = b_;
+      }
     }
   }
 
@@ -529,8 +600,16 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
 
   constexpr int ZPT = (R * 16 + NT - 1) / NT;
   constexpr int MPWQ = (3 * GW / 16) / NW, MPWC = (GW / 16) / NW, MPWF = (FC / 16) / NW;
+  // fragments per wave requested ahead of each product (where registers allow)
+  constexpr int PF = ((RB == 1 && CBW <= 2 && sizeof(AT) == 2) || TEAM > 1) ? 8 : 1;
+  constexpr int NPQ = np_of<MPWQ, D / O::KF, INFL, PF>();
+  constexpr int NPC = np_of<MPWC, D / O::KF, INFL, PF>();
+  constexpr int NPF = np_of<MPWF, D / O::KF, INFL, PF>();
+  constexpr int NP2A = np_of<CBW, GW / O::KF, INFL, PF>();
+  constexpr int NP2F = np_of<CBW, FC / O::KF, INFL, PF>();
 
   for (int t = 0; t < T; ++t) {
+    if constexpr (TEAM == 1) asm volatile("" : "+v"(lane), "+v"(lc), "+v"(lq));
     const int k = T - 1 - t;
     // schedule of this step for every sample slot
     uint64_t mev[SPT], mru[SPT], mst[SPT];
@@ -591,13 +670,16 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
 #pragma unroll
       for (int c = 0; c < CBW; ++c) {
         uint4 wv;
-        if constexpr (KEEP_EMB) wv = win[c];
+        if constexpr (EMB_LDS) wv = s_win[(w * CBW + c) * 64 + lane];
+        else if constexpr (KEEP_EMB) wv = win[c];
         else wv = pk[p.pk_win + (size_t)(w * CBW + c) * 64 + lane];
         const int col = (w * CBW + c) * 16 + lc;
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb) {
           f32x4 acc;
-          if constexpr (KEEP_EMB) {
+          if constexpr (PB_LDS) {
+            acc = s_pb[(w * CBW + c) * 64 + lane];
+          } else if constexpr (KEEP_EMB || EMB_LDS) {
             acc = pb[c][rb];
           } else {
             const float bi = raw[p.b_in + col];
@@ -634,6 +716,7 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
       if (e >= U) break;
 
       // ---- evaluate unit e for the tile
+      if constexpr (TEAM == 1) asm volatile("" : "+v"(lane), "+v"(lc), "+v"(lq));
       const int l = e / 3, u = e - 3 * l;
       const LayerOff lo = s_loff[l];
       const PackOff po = s_poff[l];
@@ -644,6 +727,17 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
         lb[c] = nlb[c];
         rbias[c] = nrb[c];
       }
+      // request the parameters of the next evaluated unit (this step or the
+      // next) now, so that they have the whole unit to arrive
+      const auto request_next_params = [&]() {
+        const uint64_t later = (e + 1 < 64) ? (evT >> (e + 1)) : 0ull;
+        if (later) load_unit_params(t, e + 1 + __builtin_ctzll(later));
+        else if (t + 1 < T) {
+          const int f = first_eval(t + 1);
+          if (f < U) load_unit_params(t + 1, f);
+        }
+      };
+      request_next_params();
       const auto gcb_sa = [&](int g) {
         return [=](int m) {
           const int iloc = w + NW * m, part = iloc / (GW / 16), within = iloc % (GW / 16);
@@ -676,22 +770,23 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
 
       if (u == 0) {
         // ---------------- self-attention unit (causal over the action tokens)
-        uint4 b1q[MPWQ];  // stage-1 weights of the first chunk, requested before the LayerNorm
-        gemm_pref<MPWQ>(b1q, pk + po.qkv, D / O::KF, 0, gcb_sa(member), lane);
+        uint4 b1q[NPQ][MPWQ];  // stage-1 weights of the first chunk, requested before the LayerNorm
+        gemm_pref<NPQ, MPWQ>(b1q, pk + po.qkv, D / O::KF, 0, gcb_sa(member), lane);
         layer_norm_to_xa();
         for (int g = member; g < NH / HG; g += TEAM) {
+          if constexpr (TEAM == 1) asm volatile("" : "+v"(lane), "+v"(lc), "+v"(lq));
           f32x4 y[MPWQ][RB];
 #pragma unroll
           for (int m = 0; m < MPWQ; ++m)
 #pragma unroll
             for (int rb = 0; rb < RB; ++rb) y[m][rb] = f32x4{0.f, 0.f, 0.f, 0.f};
-          if (g != member) gemm_pref<MPWQ>(b1q, pk + po.qkv, D / O::KF, 0, gcb_sa(g), lane);
+          if (g != member) gemm_pref<NPQ, MPWQ>(b1q, pk + po.qkv, D / O::KF, 0, gcb_sa(g), lane);
           float bq[MPWQ];  // stage-1 biases, requested before the GEMM so their latency is hidden
 #pragma unroll
           for (int m = 0; m < MPWQ; ++m) bq[m] = raw[lo.b_qkv + gcb_sa(g)(m) * 16 + lc];
-          gemm_run<AT, RB, MPWQ, D / O::KF, INFL>(y, xa, LDA, pk + po.qkv, D / O::KF, 0, gcb_sa(g), lane, b1q);
-          uint4 b2[CBW];
-          gemm_pref<CBW>(b2, pk + po.o, D / O::KF, g * (GW / O::KF), own, lane);
+          gemm_run<AT, RB, MPWQ, D / O::KF, INFL, NPQ>(y, xa, LDA, pk + po.qkv, D / O::KF, 0, gcb_sa(g), lane, b1q);
+          uint4 b2[NP2A][CBW];
+          gemm_pref<NP2A, CBW>(b2, pk + po.o, D / O::KF, g * (GW / O::KF), own, lane);
 #pragma unroll
           for (int m = 0; m < MPWQ; ++m) {
             const int loc = (w + NW * m) * 16 + lc;
@@ -726,14 +821,14 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
               for (int jj = 0; jj < NJB; ++jj) {
                 const int gj = (jb0 + jj) * 16 + lc;
                 const bool ok = (gj <= gi) && (gj / HZ == gi / HZ);
-                s[jj][i] = ok ? s[jj][i] * kScale : -INFINITY;
+                s[jj][i] = ok ? s[jj][i] * (kScale * kLog2e) : -INFINITY;
                 m = fmaxf(m, s[jj][i]);
               }
               m = row16_max(m);
               float su = 0.f;
 #pragma unroll
               for (int jj = 0; jj < NJB; ++jj) {
-                const float ev = (s[jj][i] == -INFINITY) ? 0.f : expf(s[jj][i] - m);
+                const float ev = (s[jj][i] == -INFINITY) ? 0.f : fast_exp2(s[jj][i] - m);
                 s[jj][i] = ev;
                 su += ev;
               }
@@ -743,7 +838,7 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
 #pragma unroll
             for (int jj = 0; jj < NJB; ++jj)
 #pragma unroll
-              for (int i = 0; i < 4; ++i) sc[(jj * 16 + lq * 4 + i) * PS + lc] = s[jj][i] / sm[i];
+              for (int i = 0; i < 4; ++i) sc[(jj * 16 + lq * 4 + i) * PS + lc] = s[jj][i] * fast_rcp(sm[i]);
             wave_lds_sync();
 #pragma unroll
             for (int cb = 0; cb < DH / 16; ++cb) {
@@ -766,12 +861,13 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
             wave_lds_sync();
           }
           __syncthreads();
-          gemm_run<AT, RB, CBW, GW / O::KF, INFL>(r, zbuf, LDZ, pk + po.o, D / O::KF, g * (GW / O::KF), own, lane, b2);
+          gemm_run<AT, RB, CBW, GW / O::KF, INFL, NP2A>(r, zbuf, LDZ, pk + po.o, D / O::KF, g * (GW / O::KF), own, lane,
+                                                       b2);
         }
       } else if (u == 1) {
         // ---------------- cross-attention unit (time token + observation tokens)
-        uint4 b1c[MPWC];
-        gemm_pref<MPWC>(b1c, pk + po.q, D / O::KF, 0, gcb_ca(member), lane);
+        uint4 b1c[NPC][MPWC];
+        gemm_pref<NPC, MPWC>(b1c, pk + po.q, D / O::KF, 0, gcb_ca(member), lane);
         // memory keys/values of a head group: time token + observation tokens
         constexpr int KVN = SPT * SMAX * 2 * GW, KVQ = (KVN + NT - 1) / NT;
         float kvv[KVQ];
@@ -792,19 +888,20 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
         load_kv(member);
         layer_norm_to_xa();
         for (int g = member; g < NH / HG; g += TEAM) {
+          if constexpr (TEAM == 1) asm volatile("" : "+v"(lane), "+v"(lc), "+v"(lq));
           if (g != member) load_kv(g);
           f32x4 y[MPWC][RB];
 #pragma unroll
           for (int m = 0; m < MPWC; ++m)
 #pragma unroll
             for (int rb = 0; rb < RB; ++rb) y[m][rb] = f32x4{0.f, 0.f, 0.f, 0.f};
-          if (g != member) gemm_pref<MPWC>(b1c, pk + po.q, D / O::KF, 0, gcb_ca(g), lane);
+          if (g != member) gemm_pref<NPC, MPWC>(b1c, pk + po.q, D / O::KF, 0, gcb_ca(g), lane);
           float bq[MPWC];
 #pragma unroll
           for (int m = 0; m < MPWC; ++m) bq[m] = raw[lo.b_q + gcb_ca(g)(m) * 16 + lc];
-          gemm_run<AT, RB, MPWC, D / O::KF, INFL>(y, xa, LDA, pk + po.q, D / O::KF, 0, gcb_ca(g), lane, b1c);
-          uint4 b2[CBW];
-          gemm_pref<CBW>(b2, pk + po.o2, D / O::KF, g * (GW / O::KF), own, lane);
+          gemm_run<AT, RB, MPWC, D / O::KF, INFL, NPC>(y, xa, LDA, pk + po.q, D / O::KF, 0, gcb_ca(g), lane, b1c);
+          uint4 b2[NP2A][CBW];
+          gemm_pref<NP2A, CBW>(b2, pk + po.o2, D / O::KF, g * (GW / O::KF), own, lane);
 #pragma unroll
           for (int m = 0; m < MPWC; ++m) {
             const int loc = (w + NW * m) * 16 + lc;
@@ -835,15 +932,15 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
             for (int i = 0; i < 4; ++i) {
               const int gi = ib * 16 + lq * 4 + i;
               const bool ok = nok && (jn == gi / HZ);
-              const float v = ok ? s[i] * kScale : -INFINITY;
+              const float v = ok ? s[i] * (kScale * kLog2e) : -INFINITY;
               const float m = row16_max(v);
-              const float ev = ok ? expf(v - m) : 0.f;
+              const float ev = ok ? fast_exp2(v - m) : 0.f;
               s[i] = ev;
               sm[i] = row16_sum(ev);
             }
             float* sc = pw + w * PWN;
 #pragma unroll
-            for (int i = 0; i < 4; ++i) sc[(lq * 4 + i) * PS + lc] = s[i] / sm[i];
+            for (int i = 0; i < 4; ++i) sc[(lq * 4 + i) * PS + lc] = s[i] * fast_rcp(sm[i]);
             wave_lds_sync();
 #pragma unroll
             for (int cb = 0; cb < DH / 16; ++cb) {
@@ -862,26 +959,28 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
             wave_lds_sync();
           }
           __syncthreads();
-          gemm_run<AT, RB, CBW, GW / O::KF, INFL>(r, zbuf, LDZ, pk + po.o2, D / O::KF, g * (GW / O::KF), own, lane, b2);
+          gemm_run<AT, RB, CBW, GW / O::KF, INFL, NP2A>(r, zbuf, LDZ, pk + po.o2, D / O::KF, g * (GW / O::KF), own,
+                                                       lane, b2);
         }
       } else {
         // ---------------- feed-forward unit, d_ff streamed in chunks of FC
-        uint4 b1f[MPWF];
-        gemm_pref<MPWF>(b1f, pk + po.w1, D / O::KF, 0, gcb_ff(member), lane);
+        uint4 b1f[NPF][MPWF];
+        gemm_pref<NPF, MPWF>(b1f, pk + po.w1, D / O::KF, 0, gcb_ff(member), lane);
         layer_norm_to_xa();
         for (int ch = member; ch < DFF / FC; ch += TEAM) {
+          if constexpr (TEAM == 1) asm volatile("" : "+v"(lane), "+v"(lc), "+v"(lq));
           f32x4 y[MPWF][RB];
 #pragma unroll
           for (int m = 0; m < MPWF; ++m)
 #pragma unroll
             for (int rb = 0; rb < RB; ++rb) y[m][rb] = f32x4{0.f, 0.f, 0.f, 0.f};
-          if (ch != member) gemm_pref<MPWF>(b1f, pk + po.w1, D / O::KF, 0, gcb_ff(ch), lane);
+          if (ch != member) gemm_pref<NPF, MPWF>(b1f, pk + po.w1, D / O::KF, 0, gcb_ff(ch), lane);
           float b1v[MPWF];
 #pragma unroll
           for (int m = 0; m < MPWF; ++m) b1v[m] = raw[lo.b_1 + ch * FC + (w + NW * m) * 16 + lc];
-          gemm_run<AT, RB, MPWF, D / O::KF, INFL>(y, xa, LDA, pk + po.w1, D / O::KF, 0, gcb_ff(ch), lane, b1f);
-          uint4 b2[CBW];
-          gemm_pref<CBW>(b2, pk + po.w2, DFF / O::KF, ch * (FC / O::KF), own, lane);
+          gemm_run<AT, RB, MPWF, D / O::KF, INFL, NPF>(y, xa, LDA, pk + po.w1, D / O::KF, 0, gcb_ff(ch), lane, b1f);
+          uint4 b2[NP2F][CBW];
+          gemm_pref<NP2F, CBW>(b2, pk + po.w2, DFF / O::KF, ch * (FC / O::KF), own, lane);
 #pragma unroll
           for (int m = 0; m < MPWF; ++m) {
             const int loc = (w + NW * m) * 16 + lc;
@@ -892,20 +991,11 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
                 O::store(zbuf, LDZ, rb * 16 + lq * 4 + i, loc, gelu_erf(y[m][rb][i] + b1v[m]));
           }
           __syncthreads();
-          gemm_run<AT, RB, CBW, FC / O::KF, INFL>(r, zbuf, LDZ, pk + po.w2, DFF / O::KF, ch * (FC / O::KF), own, lane, b2);
+          gemm_run<AT, RB, CBW, FC / O::KF, INFL, NP2F>(r, zbuf, LDZ, pk + po.w2, DFF / O::KF, ch * (FC / O::KF), own,
+                                                        lane, b2);
           __syncthreads();
         }
       }
-      // request the parameters of the next evaluated unit (this step or the
-      // next), after this unit's weight loads so they do not delay them
-      const auto request_next_params = [&]() {
-        const uint64_t later = (e + 1 < 64) ? (evT >> (e + 1)) : 0ull;
-        if (later) load_unit_params(t, e + 1 + __builtin_ctzll(later));
-        else if (t + 1 < T) {
-          const int f = first_eval(t + 1);
-          if (f < U) load_unit_params(t + 1, f);
-        }
-      };
       if constexpr (TEAM > 1) {
         // Sum the members' partial residuals in member order, so that every
         // member obtains the same bits.  The partials travel through memory
@@ -926,7 +1016,6 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
             for (int q = 0; q < 4; ++q) v[q] = v[q] == kEmpty ? 0x7FC00000u : v[q];
             __builtin_amdgcn_raw_buffer_store_b128(v, xr, xoff(cur, member, c, rb), 0, kCoherent);
           }
-        request_next_params();
         u32x4 part[TEAM][CBW][RB];
         unsigned pending = ((1u << TEAM) - 1u) & ~(1u << member);
         unsigned spins = 0;
@@ -978,8 +1067,6 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
           for (int rb = 0; rb < RB; ++rb)
             __builtin_amdgcn_raw_buffer_store_b128(empty, xr, xoff(prev, member, c, rb), 0, kCoherent);
         ++nbar;
-      } else {
-        request_next_params();
       }
 #pragma unroll
       for (int c = 0; c < CBW; ++c)
@@ -1031,7 +1118,10 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
 #pragma unroll
       for (int c = 0; c < CBW; ++c) {
         float g_, b_;
-        if constexpr (KEEP_EMB) {
+        if constexpr (EMB_LDS) {
+          g_ = s_lf[(w * CBW + c) * 16 + lc];
+          b_ = s_lf[D + (w * CBW + c) * 16 + lc];
+        } else if constexpr (KEEP_EMB) {
           g_ = lfg[c];
           b_ = lfb[c];
         } else {
@@ -1040,7 +1130,8 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
           b_ = raw[p.lnf_b + col];
         }
         uint4 wo;
-        if constexpr (KEEP_EMB) wo = wout[c];
+        if constexpr (EMB_LDS) wo = s_wout[(w * CBW + c) * 64 + lane];
+        else if constexpr (KEEP_EMB) wo = wout[c];
         else wo = pk[p.pk_wout + (size_t)(w * CBW + c) * 64 + lane];
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb)
@@ -1074,10 +1165,10 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
           for (int ww = 0; ww < NW; ++ww) part += epsp[(ww * R + row) * 16 + a];
           const float e = bout[q] + part;
           const auto dd = [&](int i) { return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(ddl), i)); };
-          const float s1 = dd(0), sa = dd(1), c0 = dd(2), ct = dd(3), sg = dd(4);
+          const float s1 = dd(0), rsa = dd(1), c0 = dd(2), ct = dd(3), sg = dd(4);
           float* xp = xs + row * 16 + OF::pcol(a);
           const float x = *xp;
-          float x0 = (x - s1 * e) / sa;
+          float x0 = (x - s1 * e) * rsa;
           if (p.clip) x0 = fminf(fmaxf(x0, -1.f), 1.f);
           float xn = c0 * x0 + ct * x;
           if (k > 0) xn += sg * zpre[q];
@@ -1177,7 +1268,7 @@ __global__ void ddpm_kernel(int T, float* tab) {
     const double var = fmax((1.0 - abar_prev) / (1.0 - abar) * beta, 1e-20);
     float* r = tab + (size_t)i * 8;
     r[0] = (float)sqrt(1.0 - abar);
-    r[1] = (float)sqrt(abar);
+    r[1] = (float)(1.0 / sqrt(abar));  // stored as a reciprocal: the update multiplies
     r[2] = (float)c0;
     r[3] = (float)ct;
     r[4] = (float)sqrt(var);

@@ -28,7 +28,7 @@ struct KParams {
   uint64_t pk_wout;          // fp32 fragments of W_out (rows padded to 16)
   uint32_t W_in, b_in, P_act, b_obs, P_mem, lnf_g, lnf_b, W_out, b_out, pad_;
   const float* tkv;          // [T][L][2d] time-token keys/values, indexed by timestep k
-  const float* ddpm;         // [T][8] sampler constants, indexed by timestep k
+  const float* ddpm;         // [T][8] sampler constants by timestep k: sqrt(1-abar), 1/sqrt(abar), c0, ct, sigma
   const int32_t* tile_sample;  // [n_tiles][spt] sample index or -1
   const int32_t* tile_slot;    // [n_tiles][spt] schedule slot
   const uint64_t* masks;       // [slots][T][3] unit bitmasks {evaluate(+merged bit 63), reuse, store}
