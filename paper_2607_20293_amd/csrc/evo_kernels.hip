@@ -321,7 +321,7 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
   // layer-merged residual sum accumulated in registers, else in its cache slot
   constexpr bool MAC_REG = CBW * RB <= 4;
   // weight fragments in flight per wave in the unit products
-  constexpr int INFL = TEAM > 1 ? 16 : (RB == 1 && CBW <= 2 ? 12 : 6);
+  constexpr int INFL = (TEAM > 1 && RB == 1) ? 16 : (RB == 1 && CBW <= 2 ? 12 : 6);
   constexpr float kScale = (DH == 64) ? 0.125f : (DH == 32 ? 0.17677669529663688f : 0.0f);
   static_assert(DH == 64 || DH == 32, "head dim");
 
@@ -341,9 +341,7 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
   // lane indices are made opaque to the optimiser (an empty asm) once per
   // step, unit, head group and d_ff chunk, so that the address arithmetic
   // derived from them is recomputed inside the loops instead of being
-  // hoisted into registers held for the whole kernel (which spilled); the
-  // one-wave-per-SIMD team variant has accumulation registers to spare and
-  // keeps the hoisted form
+  // hoisted into registers held for the whole kernel (which spilled)
   int lane = tid & 63, lc = lane & 15, lq = lane >> 4;
   // a team of TEAM workgroups shares a tile: each member evaluates its share
   // of every unit's head groups / d_ff chunks and the partial residuals are
@@ -601,7 +599,7 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
   constexpr int ZPT = (R * 16 + NT - 1) / NT;
   constexpr int MPWQ = (3 * GW / 16) / NW, MPWC = (GW / 16) / NW, MPWF = (FC / 16) / NW;
   // fragments per wave requested ahead of each product (where registers allow)
-  constexpr int PF = ((RB == 1 && CBW <= 2 && sizeof(AT) == 2) || TEAM > 1) ? 8 : 1;
+  constexpr int PF = ((sizeof(AT) == 4 && RB > 1) || D > 256) ? 1 : 8;
   constexpr int NPQ = np_of<MPWQ, D / O::KF, INFL, PF>();
   constexpr int NPC = np_of<MPWC, D / O::KF, INFL, PF>();
   constexpr int NPF = np_of<MPWF, D / O::KF, INFL, PF>();
@@ -609,7 +607,7 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
   constexpr int NP2F = np_of<CBW, FC / O::KF, INFL, PF>();
 
   for (int t = 0; t < T; ++t) {
-    if constexpr (TEAM == 1) asm volatile("" : "+v"(lane), "+v"(lc), "+v"(lq));
+    asm volatile("" : "+v"(lane), "+v"(lc), "+v"(lq));
     const int k = T - 1 - t;
     // schedule of this step for every sample slot
     uint64_t mev[SPT], mru[SPT], mst[SPT];
@@ -716,7 +714,7 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
       if (e >= U) break;
 
       // ---- evaluate unit e for the tile
-      if constexpr (TEAM == 1) asm volatile("" : "+v"(lane), "+v"(lc), "+v"(lq));
+      asm volatile("" : "+v"(lane), "+v"(lc), "+v"(lq));
       const int l = e / 3, u = e - 3 * l;
       const LayerOff lo = s_loff[l];
       const PackOff po = s_poff[l];
@@ -774,7 +772,7 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
         gemm_pref<NPQ, MPWQ>(b1q, pk + po.qkv, D / O::KF, 0, gcb_sa(member), lane);
         layer_norm_to_xa();
         for (int g = member; g < NH / HG; g += TEAM) {
-          if constexpr (TEAM == 1) asm volatile("" : "+v"(lane), "+v"(lc), "+v"(lq));
+          asm volatile("" : "+v"(lane), "+v"(lc), "+v"(lq));
           f32x4 y[MPWQ][RB];
 #pragma unroll
           for (int m = 0; m < MPWQ; ++m)
@@ -888,7 +886,7 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
         load_kv(member);
         layer_norm_to_xa();
         for (int g = member; g < NH / HG; g += TEAM) {
-          if constexpr (TEAM == 1) asm volatile("" : "+v"(lane), "+v"(lc), "+v"(lq));
+          asm volatile("" : "+v"(lane), "+v"(lc), "+v"(lq));
           if (g != member) load_kv(g);
           f32x4 y[MPWC][RB];
 #pragma unroll
@@ -968,7 +966,7 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
         gemm_pref<NPF, MPWF>(b1f, pk + po.w1, D / O::KF, 0, gcb_ff(member), lane);
         layer_norm_to_xa();
         for (int ch = member; ch < DFF / FC; ch += TEAM) {
-          if constexpr (TEAM == 1) asm volatile("" : "+v"(lane), "+v"(lc), "+v"(lq));
+          asm volatile("" : "+v"(lane), "+v"(lc), "+v"(lq));
           f32x4 y[MPWF][RB];
 #pragma unroll
           for (int m = 0; m < MPWF; ++m)
@@ -1016,48 +1014,93 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
             for (int q = 0; q < 4; ++q) v[q] = v[q] == kEmpty ? 0x7FC00000u : v[q];
             __builtin_amdgcn_raw_buffer_store_b128(v, xr, xoff(cur, member, c, rb), 0, kCoherent);
           }
-        u32x4 part[TEAM][CBW][RB];
-        unsigned pending = ((1u << TEAM) - 1u) & ~(1u << member);
-        unsigned spins = 0;
-        while (true) {
-#pragma unroll
-          for (int m = 0; m < TEAM; ++m)
-            if (pending >> m & 1u) {
-#pragma unroll
-              for (int c = 0; c < CBW; ++c)
-#pragma unroll
-                for (int rb = 0; rb < RB; ++rb)
-                  part[m][c][rb] = __builtin_amdgcn_raw_buffer_load_b128(xr, xoff(cur, m, c, rb), 0, kCoherent);
+        // bounded wait for every word of `v` (loaded by `load`) to be written
+        const auto poll = [&](auto& v, auto load, auto ready) {
+          unsigned spins = 0;
+          while (true) {
+            load(v);
+            if (ready(v)) break;
+            if (__hip_atomic_load(p.derr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u || ++spins > (1u << 20)) {
+              __hip_atomic_store(p.derr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+              break;
             }
-#pragma unroll
-          for (int m = 0; m < TEAM; ++m)
-            if (pending >> m & 1u) {
-              bool ok = true;
-#pragma unroll
-              for (int c = 0; c < CBW; ++c)
-#pragma unroll
-                for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-                  for (int q = 0; q < 4; ++q) ok = ok && part[m][c][rb][q] != kEmpty;
-              if (ok) pending &= ~(1u << m);
-            }
-          if (!pending) break;
-          if (__hip_atomic_load(p.derr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u || ++spins > (1u << 20)) {
-            __hip_atomic_store(p.derr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            break;
+            __builtin_amdgcn_s_sleep(1);
           }
-          __builtin_amdgcn_s_sleep(1);
+        };
+        const auto full = [&](const u32x4& x) {
+          return x[0] != kEmpty && x[1] != kEmpty && x[2] != kEmpty && x[3] != kEmpty;
+        };
+        if constexpr (TEAM == 2) {
+          // two operands: r + other is the same sum on both members
+          // (commutative), so only the other member's partial is held, a few
+          // column blocks at a time
+          constexpr int XC = (CBW * RB > 4) ? (4 / RB > 0 ? 4 / RB : 1) : CBW;
+          static_assert(CBW % XC == 0, "exchange chunks");
+          const int other = 1 - member;
+#pragma unroll
+          for (int c0 = 0; c0 < CBW; c0 += XC) {
+            u32x4 part[XC][RB];
+            poll(part,
+                 [&](u32x4 (&v)[XC][RB]) {
+#pragma unroll
+                   for (int c = 0; c < XC; ++c)
+#pragma unroll
+                     for (int rb = 0; rb < RB; ++rb)
+                       v[c][rb] = __builtin_amdgcn_raw_buffer_load_b128(xr, xoff(cur, other, c0 + c, rb), 0, kCoherent);
+                 },
+                 [&](const u32x4 (&v)[XC][RB]) {
+                   bool ok = true;
+#pragma unroll
+                   for (int c = 0; c < XC; ++c)
+#pragma unroll
+                     for (int rb = 0; rb < RB; ++rb) ok = ok && full(v[c][rb]);
+                   return ok;
+                 });
+#pragma unroll
+            for (int c = 0; c < XC; ++c)
+#pragma unroll
+              for (int rb = 0; rb < RB; ++rb) r[c0 + c][rb] += __builtin_bit_cast(f32x4, part[c][rb]);
+          }
+        } else {
+          // more operands: every member sums the partials in member order
+          u32x4 part[TEAM][CBW][RB];
+          unsigned pending = ((1u << TEAM) - 1u) & ~(1u << member);
+          poll(part,
+               [&](u32x4 (&v)[TEAM][CBW][RB]) {
+#pragma unroll
+                 for (int m = 0; m < TEAM; ++m)
+                   if (pending >> m & 1u) {
+#pragma unroll
+                     for (int c = 0; c < CBW; ++c)
+#pragma unroll
+                       for (int rb = 0; rb < RB; ++rb)
+                         v[m][c][rb] = __builtin_amdgcn_raw_buffer_load_b128(xr, xoff(cur, m, c, rb), 0, kCoherent);
+                   }
+               },
+               [&](const u32x4 (&v)[TEAM][CBW][RB]) {
+#pragma unroll
+                 for (int m = 0; m < TEAM; ++m)
+                   if (pending >> m & 1u) {
+                     bool ok = true;
+#pragma unroll
+                     for (int c = 0; c < CBW; ++c)
+#pragma unroll
+                       for (int rb = 0; rb < RB; ++rb) ok = ok && full(v[m][c][rb]);
+                     if (ok) pending &= ~(1u << m);
+                   }
+                 return pending == 0u;
+               });
+#pragma unroll
+          for (int c = 0; c < CBW; ++c)
+#pragma unroll
+            for (int rb = 0; rb < RB; ++rb) {
+              f32x4 acc = member == 0 ? r[c][rb] : __builtin_bit_cast(f32x4, part[0][c][rb]);
+#pragma unroll
+              for (int m = 1; m < TEAM; ++m)
+                acc += member == m ? r[c][rb] : __builtin_bit_cast(f32x4, part[m][c][rb]);
+              r[c][rb] = acc;
+            }
         }
-#pragma unroll
-        for (int c = 0; c < CBW; ++c)
-#pragma unroll
-          for (int rb = 0; rb < RB; ++rb) {
-            f32x4 acc = member == 0 ? r[c][rb] : __builtin_bit_cast(f32x4, part[0][c][rb]);
-#pragma unroll
-            for (int m = 1; m < TEAM; ++m)
-              acc += member == m ? r[c][rb] : __builtin_bit_cast(f32x4, part[m][c][rb]);
-            r[c][rb] = acc;
-          }
         // every member has read the partials of the previous unit: empty
         // this member's slot of it for its next use
         const u32x4 empty = {kEmpty, kEmpty, kEmpty, kEmpty};
@@ -1323,7 +1366,8 @@ hipError_t launch_ddpm_table(int T, float* table, hipStream_t stream) {
   X(__bf16, 256, 64, 16, 2, 1024, 8, 2, 256, 8, 1)        \
   X(__bf16, 768, 64, 32, 1, 3072, 8, 2, 256, 5, 1)        \
   X(float, 256, 64, 16, 1, 1024, 4, 1, 256, 8, 4)         \
-  X(__bf16, 256, 64, 16, 1, 1024, 4, 1, 256, 8, 4)
+  X(__bf16, 256, 64, 16, 1, 1024, 4, 1, 256, 8, 4)        \
+  X(__bf16, 768, 64, 32, 1, 3072, 8, 2, 256, 5, 2)
 
 template <class AT> constexpr int dtype_of() { return std::is_same<AT, float>::value ? 0 : 1; }
 
