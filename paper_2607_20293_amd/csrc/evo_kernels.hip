@@ -50,6 +50,35 @@ __device__ __forceinline__ f32x4 mfma4(float a, float b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
 }
 
+// 16x16 tile of q · kᵀ over a DH-long dot product on fp32 MFMA.  The K order
+// is permuted (any bijection of k works when both operands use it): lane
+// group lq takes k = 16·lq + j at step j, so each lane reads 16 contiguous
+// floats of its row (four 16-byte LDS reads) instead of 16 strided ones, and
+// four independent accumulators shorten the dependent MFMA chain.
+template <int DH>
+__device__ __forceinline__ f32x4 qk_tile(const float* qrow, const float* krow, bool kvalid, int lq) {
+  static_assert(DH % 64 == 0 || DH == 32, "head size");
+  f32x4 acc[4] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
+  constexpr int KPL = DH / 4;  // k per lane group
+#pragma unroll
+  for (int j4 = 0; j4 < KPL / 4; ++j4) {
+    const f32x4 qv = *reinterpret_cast<const f32x4*>(qrow + lq * KPL + 4 * j4);
+    f32x4 kv = *reinterpret_cast<const f32x4*>(krow + lq * KPL + 4 * j4);
+    if (!kvalid) kv = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) acc[e] = mfma4(qv[e], kv[e], acc[e]);
+  }
+  return (acc[0] + acc[1]) + (acc[2] + acc[3]);
+}
+
+// waves sharing one (head, 16-query block) of attention: each repeats the
+// scores and computes its share of the DH / 16 value column blocks
+constexpr int attn_waves_per_pair(int nw, int npair, int ncb) {
+  int wpp = 1;
+  while (wpp * 2 <= nw / (npair > 0 ? npair : 1) && ncb % (wpp * 2) == 0) wpp *= 2;
+  return wpp;
+}
+
 // Cross-lane moves within a row of 16 lanes (DPP): swap neighbours, swap
 // pairs, mirror within 8, mirror within 16.  Each pairs every lane with a
 // lane of the other half of its group, so four steps combine all 16 lanes
@@ -598,6 +627,7 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
 
   constexpr int ZPT = (R * 16 + NT - 1) / NT;
   constexpr int MPWQ = (3 * GW / 16) / NW, MPWC = (GW / 16) / NW, MPWF = (FC / 16) / NW;
+  constexpr int WPP = attn_waves_per_pair(NW, HG * RB, DH / 16);
   // fragments per wave requested ahead of each product (where registers allow)
   constexpr int PF = ((sizeof(AT) == 4 && RB > 1) || D > 256) ? 1 : 8;
   constexpr int NPQ = np_of<MPWQ, D / O::KF, INFL, PF>();
@@ -794,8 +824,10 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
               for (int i = 0; i < 4; ++i) ybuf[(rb * 16 + lq * 4 + i) * LDY + loc] = y[m][rb][i] + bq[m];
           }
           __syncthreads();
-          // scores, softmax and values on fp32 MFMA tiles: wave per (head, query block)
-          for (int pr = w; pr < HG * RB; pr += NW) {
+          // scores, softmax and values on fp32 MFMA tiles: WPP waves per
+          // (head, query block), each with DH / 16 / WPP value column blocks
+          for (int it = w; it < HG * RB * WPP; it += NW) {
+            const int pr = it / WPP, part = it % WPP;
             const int hh = pr % HG, ib = pr / HG;
             const int jb0 = (HZ >= 16) ? ((ib * 16) / HZ) * (HZ / 16) : ib;
             f32x4 s[NJB];
@@ -803,12 +835,9 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
             for (int jj = 0; jj < NJB; ++jj) {
               s[jj] = f32x4{0.f, 0.f, 0.f, 0.f};
               const int jb = jb0 + jj;
-              if (jb <= ib) {
-                const float* qp = ybuf + (ib * 16 + lc) * LDY + hh * DH + lq;
-                const float* kp = ybuf + (jb * 16 + lc) * LDY + GW + hh * DH + lq;
-#pragma unroll
-                for (int kk = 0; kk < DH / 4; ++kk) s[jj] = mfma4(qp[4 * kk], kp[4 * kk], s[jj]);
-              }
+              if (jb <= ib)
+                s[jj] = qk_tile<DH>(ybuf + (ib * 16 + lc) * LDY + hh * DH, ybuf + (jb * 16 + lc) * LDY + GW + hh * DH,
+                                    true, lq);
             }
             float sm[4];
 #pragma unroll
@@ -839,7 +868,8 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
               for (int i = 0; i < 4; ++i) sc[(jj * 16 + lq * 4 + i) * PS + lc] = s[jj][i] * fast_rcp(sm[i]);
             wave_lds_sync();
 #pragma unroll
-            for (int cb = 0; cb < DH / 16; ++cb) {
+            for (int cbi = 0; cbi < DH / 16 / WPP; ++cbi) {
+              const int cb = part * (DH / 16 / WPP) + cbi;
               f32x4 o = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
               for (int jj = 0; jj < NJB; ++jj) {
@@ -912,19 +942,15 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
           for (int q = 0; q < KVQ; ++q)
             if (tid + q * NT < KVN) kvbuf[tid + q * NT] = kvv[q];
           __syncthreads();
-          for (int pr = w; pr < HG * RB; pr += NW) {
+          for (int it = w; it < HG * RB * WPP; it += NW) {
+            const int pr = it / WPP, part = it % WPP;
             const int hh = pr % HG, ib = pr / HG;
             const int js0 = (ib * 16) / HZ;  // first sample slot of this row block
             // memory column n of the tile: sample js0 + n / SLOTS, token n % SLOTS
             const int jn = js0 + lc / SLOTS, sn = lc % SLOTS;
             const bool nok = sn < S && jn < SPT;
-            f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f};
-            {
-              const float* qp = ybuf + (ib * 16 + lc) * LDY + hh * DH + lq;
-              const float* kp = kvbuf + ((nok ? jn : 0) * SMAX + (nok ? sn : 0)) * (2 * GW) + hh * DH + lq;
-#pragma unroll
-              for (int kk = 0; kk < DH / 4; ++kk) s = mfma4(qp[4 * kk], nok ? kp[4 * kk] : 0.f, s);
-            }
+            f32x4 s = qk_tile<DH>(ybuf + (ib * 16 + lc) * LDY + hh * DH,
+                                  kvbuf + ((nok ? jn : 0) * SMAX + (nok ? sn : 0)) * (2 * GW) + hh * DH, nok, lq);
             float sm[4];
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
@@ -941,7 +967,8 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
             for (int i = 0; i < 4; ++i) sc[(lq * 4 + i) * PS + lc] = s[i] * fast_rcp(sm[i]);
             wave_lds_sync();
 #pragma unroll
-            for (int cb = 0; cb < DH / 16; ++cb) {
+            for (int cbi = 0; cbi < DH / 16 / WPP; ++cbi) {
+              const int cb = part * (DH / 16 / WPP) + cbi;
               f32x4 o = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
               for (int kk = 0; kk < 4; ++kk) {
