@@ -942,46 +942,52 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
           for (int q = 0; q < KVQ; ++q)
             if (tid + q * NT < KVN) kvbuf[tid + q * NT] = kvv[q];
           __syncthreads();
+          // Each row attends to the S = 1 + n_obs memory tokens of its own
+          // sample: few keys, so the products run on the vector ALUs (fp32
+          // MFMA tiles would be mostly padding).  Lane = (row, quarter of the
+          // head's dims); a row's four lanes are adjacent, so the score
+          // reduction is two quad shuffles.  WPP waves per (head, row block)
+          // each produce DH / WPP output dims.
           for (int it = w; it < HG * RB * WPP; it += NW) {
             const int pr = it / WPP, part = it % WPP;
             const int hh = pr % HG, ib = pr / HG;
-            const int js0 = (ib * 16) / HZ;  // first sample slot of this row block
-            // memory column n of the tile: sample js0 + n / SLOTS, token n % SLOTS
-            const int jn = js0 + lc / SLOTS, sn = lc % SLOTS;
-            const bool nok = sn < S && jn < SPT;
-            f32x4 s = qk_tile<DH>(ybuf + (ib * 16 + lc) * LDY + hh * DH,
-                                  kvbuf + ((nok ? jn : 0) * SMAX + (nok ? sn : 0)) * (2 * GW) + hh * DH, nok, lq);
-            float sm[4];
+            const int qr = lane >> 2, qg = lane & 3;  // row in the block, dim quarter
+            const int row = ib * 16 + qr, js = row / HZ;
+            constexpr int DQ = DH / 4, OD = DH / 4 / WPP;
+            const float* qrow = ybuf + row * LDY + hh * DH + qg * DQ;
+            const int c0 = hh * DH + part * (DH / WPP) + qg * OD;  // first output column of this lane
+            // one pass over the keys with a running maximum (online softmax)
+            float mx = -INFINITY, den = 0.f, o[OD];
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-              const int gi = ib * 16 + lq * 4 + i;
-              const bool ok = nok && (jn == gi / HZ);
-              const float v = ok ? s[i] * (kScale * kLog2e) : -INFINITY;
-              const float m = row16_max(v);
-              const float ev = ok ? fast_exp2(v - m) : 0.f;
-              s[i] = ev;
-              sm[i] = row16_sum(ev);
-            }
-            float* sc = pw + w * PWN;
+            for (int d = 0; d < OD; ++d) o[d] = 0.f;
+#pragma unroll 1
+            for (int j = 0; j < S; ++j) {
+              const float* kr = kvbuf + (js * SMAX + j) * (2 * GW) + hh * DH + qg * DQ;
+              float a = 0.f;
 #pragma unroll
-            for (int i = 0; i < 4; ++i) sc[(lq * 4 + i) * PS + lc] = s[i] * fast_rcp(sm[i]);
-            wave_lds_sync();
-#pragma unroll
-            for (int cbi = 0; cbi < DH / 16 / WPP; ++cbi) {
-              const int cb = part * (DH / 16 / WPP) + cbi;
-              f32x4 o = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-              for (int kk = 0; kk < 4; ++kk) {
-                const int n = 4 * kk + lq, jv = js0 + n / SLOTS, sv = n % SLOTS;
-                const bool vok = sv < S && jv < SPT;
-                const float a = sc[lc * PS + n];
-                const float v = vok ? kvbuf[(jv * SMAX + sv) * (2 * GW) + GW + hh * DH + cb * 16 + lc] : 0.f;
-                o = mfma4(a, v, o);
+              for (int d4 = 0; d4 < DQ / 4; ++d4) {
+                const f32x4 kv = *reinterpret_cast<const f32x4*>(kr + 4 * d4);
+                const f32x4 qv = *reinterpret_cast<const f32x4*>(qrow + 4 * d4);
+                a += qv[0] * kv[0] + qv[1] * kv[1] + qv[2] * kv[2] + qv[3] * kv[3];
               }
+              a += dpp_mov<0xB1>(a);  // sum over the row's four lanes
+              a += dpp_mov<0x4E>(a);
+              a *= kScale * kLog2e;
+              const float mn = fmaxf(mx, a);
+              const float sc = fast_exp2(mx - mn), pj = fast_exp2(a - mn);
+              den = den * sc + pj;
+              mx = mn;
+              const float* vr = kvbuf + (js * SMAX + j) * (2 * GW) + GW + c0;
 #pragma unroll
-              for (int i = 0; i < 4; ++i) O::store(zbuf, LDZ, ib * 16 + lq * 4 + i, hh * DH + cb * 16 + lc, o[i]);
+              for (int d4 = 0; d4 < OD / 4; ++d4) {
+                const f32x4 vv = *reinterpret_cast<const f32x4*>(vr + 4 * d4);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) o[4 * d4 + e] = o[4 * d4 + e] * sc + pj * vv[e];
+              }
             }
-            wave_lds_sync();
+            const float inv = fast_rcp(den);
+#pragma unroll
+            for (int d = 0; d < OD; ++d) O::store(zbuf, LDZ, row, c0 + d, o[d] * inv);
           }
           __syncthreads();
           gemm_run<AT, RB, CBW, GW / O::KF, INFL, NP2A>(r, zbuf, LDZ, pk + po.o2, D / O::KF, g * (GW / O::KF), own,
