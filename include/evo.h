@@ -169,8 +169,12 @@ int evo_denoise(evo_policy* p, int32_t batch, const float* obs_cond, const float
  * meet at bounded device-side barriers; if one of those waits ever times
  * out, the kernel stops early, its outputs are invalid, and this call
  * returns EVO_E_HIP (the flag is then cleared; until it is, later team
- * launches stop at their first barrier).  Setting the environment variable
- * EVO_TEAM=0 before evo_create_policy disables that variant. */
+ * launches stop at their first barrier).  Environment variables read by
+ * evo_create_policy: EVO_TEAM=0 disables that variant; EVO_TEAM_SPIN_LIMIT
+ * sets the number of polls before a wait gives up (default 2^20, about a
+ * second); EVO_TEAM_TEST_WITHHOLD=1 is a test hook that makes team member 0
+ * withhold its partial residuals, so that the other members' waits time out
+ * and this error path can be exercised (outputs are then invalid). */
 int evo_synchronize(evo_policy* p);
 
 /* Statistics of the last evo_denoise call (host struct). */

@@ -91,6 +91,8 @@ struct evo_policy {
   // small-batch team variant: members per tile, largest batch it serves,
   // partial-residual exchange, barrier counters, device error flag
   int team = 1, team_batch = 0;
+  unsigned team_spin_limit = 1u << 20;  // EVO_TEAM_SPIN_LIMIT
+  int team_withhold = 0;                // EVO_TEAM_TEST_WITHHOLD (test hook)
   size_t okv_stride = 0;
   float* d_xchg = nullptr;
   unsigned* d_tctr = nullptr;
@@ -289,6 +291,9 @@ int evo_create_policy(const evo_policy_desc* desc, const float* host_weights, si
     // batches that fill at most n_cu workgroups; it needs cooperative launch
     const char* env = std::getenv("EVO_TEAM");
     const bool team_on = !(env && env[0] == '0');
+    if (const char* e = std::getenv("EVO_TEAM_SPIN_LIMIT"))
+      p->team_spin_limit = (unsigned)std::min(std::strtoul(e, nullptr, 10), 1ul << 28);
+    if (const char* e = std::getenv("EVO_TEAM_TEST_WITHHOLD")) p->team_withhold = e[0] == '1';
     const int team = kernel_team_size(KernelKey{s.d, s.dh(), s.H, s.dff, s.dtype, 1, 0});
     int coop = 0;
     (void)hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, p->device);
@@ -452,6 +457,8 @@ int evo_denoise(evo_policy* p, int32_t batch, const float* obs_cond, const float
     kp.tctr = p->d_tctr;
     kp.derr = p->d_derr;
     kp.okv_member_stride = p->okv_stride;
+    kp.spin_limit = p->team_spin_limit;
+    kp.withhold = p->team_withhold;
     HIP_TRY(launch_zero_u32(p->d_tctr, plan.n_tiles * 16, stream));
   }
   KernelKey key{s.d, s.dh(), s.H, s.dff, s.dtype, spt, team};

@@ -500,7 +500,7 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
       __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       unsigned spins = 0;
       while (__hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < (unsigned)TEAM) {
-        if (__hip_atomic_load(p.derr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u || ++spins > (1u << 22)) {
+        if (__hip_atomic_load(p.derr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u || ++spins > 4u * p.spin_limit) {
           __hip_atomic_store(p.derr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
           s_abort = 1;
           break;
@@ -1045,7 +1045,8 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
             u32x4 v = __builtin_bit_cast(u32x4, r[c][rb]);
 #pragma unroll
             for (int q = 0; q < 4; ++q) v[q] = v[q] == kEmpty ? 0x7FC00000u : v[q];
-            __builtin_amdgcn_raw_buffer_store_b128(v, xr, xoff(cur, member, c, rb), 0, kCoherent);
+            if (!(p.withhold && member == 0))
+              __builtin_amdgcn_raw_buffer_store_b128(v, xr, xoff(cur, member, c, rb), 0, kCoherent);
           }
         // bounded wait for every word of `v` (loaded by `load`) to be written
         const auto poll = [&](auto& v, auto load, auto ready) {
@@ -1053,7 +1054,7 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
           while (true) {
             load(v);
             if (ready(v)) break;
-            if (__hip_atomic_load(p.derr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u || ++spins > (1u << 20)) {
+            if (__hip_atomic_load(p.derr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u || ++spins > p.spin_limit) {
               __hip_atomic_store(p.derr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
               break;
             }

@@ -42,6 +42,8 @@ struct KParams {
   unsigned* derr;            // device error flag (team barrier timed out)
   size_t okv_member_stride;  // floats between team members' observation key/value copies
   int batch, team;
+  unsigned spin_limit;       // polls before a team wait gives up (sets *derr)
+  int withhold;              // test hook: team member 0 never publishes its partials
 };
 
 // Shape key of a compiled kernel instantiation.

@@ -17,21 +17,25 @@ from tests.gpu_util import check_stats, compare, device, run_gpu, run_oracle, sa
 pytestmark = pytest.mark.gpu
 
 
-def _policy(shape, weights, dtype, max_batch, max_sched, cold=O.COLD_COMPUTE, clip=True, team=True):
+def _policy(shape, weights, dtype, max_batch, max_sched, cold=O.COLD_COMPUTE, clip=True, team=True, env=None):
     """team=False creates the policy with the small-batch team variant
-    switched off (EVO_TEAM=0 is read at creation)."""
+    switched off (EVO_TEAM=0 is read at creation); env: further variables
+    set only while the policy is created."""
     device()
-    old = os.environ.get("EVO_TEAM")
+    env = dict(env or {})
     if not team:
-        os.environ["EVO_TEAM"] = "0"
+        env["EVO_TEAM"] = "0"
+    old = {k: os.environ.get(k) for k in env}
+    os.environ.update(env)
     try:
         return evo.Policy(shape, weights, dtype=dtype, max_batch=max_batch, max_schedules=max_sched,
                           cold_policy=cold, clip=clip)
     finally:
-        if old is None:
-            os.environ.pop("EVO_TEAM", None)
-        else:
-            os.environ["EVO_TEAM"] = old
+        for k, v in old.items():
+            if v is None:
+                os.environ.pop(k, None)
+            else:
+                os.environ[k] = v
 
 
 def _case(name, shape, weights, obs, noise, lattices, ids, dtype, gran=O.GRAN_LAYER,
@@ -134,6 +138,40 @@ def test_team_variant_matches_single_workgroup(dtype):
     assert np.array_equal(again, got_t)
     pol_t.close()
     pol_1.close()
+
+
+def test_team_wait_timeout_is_reported():
+    """Error path of the team variant, forced from the host: team member 0
+    withholds its partial residuals (test hook) and the other members' waits
+    give up after 64 polls.  The kernel still finishes; evo_synchronize
+    reports the failure once and clears it; a policy created normally
+    afterwards is unaffected."""
+    import torch
+    s = I.PUSHT
+    wts = I.make_weights(s, 7, "perturbed")
+    obs, noise = I.make_obs(s, 1, 7), I.make_noise(s, 1, 7)
+    lat = I.lattice_bernoulli(3 * s.n_layers, s.n_steps, 0.2, np.random.default_rng(7))
+    say("[gpu] team wait timeout, forced from the host")
+    pol = _policy(s, wts, "bf16", 1, 1, env={"EVO_TEAM_TEST_WITHHOLD": "1", "EVO_TEAM_SPIN_LIMIT": "64"})
+    pol.set_schedule(0, lat, O.GRAN_UNIT)
+    dev = device()
+    pol.denoise(torch.from_numpy(obs).to(dev), torch.from_numpy(noise).to(dev), None)
+    st = pol.stats()
+    if st["n_workgroups"] == st["n_tiles"]:
+        pol.synchronize()
+        pol.close()
+        pytest.skip("the team variant is not used on this device")
+    with pytest.raises(evo.EvoError) as e:
+        pol.synchronize()
+    assert e.value.code == -4 and "team barrier" in str(e.value)
+    pol.synchronize()  # reported once, then cleared
+    pol.close()
+    pol2 = _policy(s, wts, "bf16", 1, 1)
+    pol2.set_schedule(0, lat, O.GRAN_UNIT)
+    got, st2 = run_gpu(pol2, obs, noise, np.zeros(1, np.int32))
+    ref, _ = run_oracle(s, wts, obs, noise, [lat], np.zeros(1, np.int32), O.GRAN_UNIT, O.COLD_COMPUTE, "bf16")
+    compare(got, ref, "bf16", "after a forced timeout")
+    pol2.close()
 
 
 @pytest.mark.parametrize("name", ["pusht_fp32_b64_d25", "pusht_bf16_b64_d25", "pusht_bf16_b64_all"])
