@@ -177,6 +177,51 @@ int evo_denoise(evo_policy* p, int32_t batch, const float* obs_cond, const float
  * and this error path can be exercised (outputs are then invalid). */
 int evo_synchronize(evo_policy* p);
 
+/* ---- Redundancy-aware initialisation of the schedule search (Sec. 3.3,
+ * Eq. 6 and Eq. 7).  Offline tooling around the cached loop: activations of
+ * the uncached policy, their cross-step cosine dissimilarity, and the guided
+ * sampling distribution over block x step positions. */
+
+/* evo_denoise that also records, for every sample n, unit b (3L units,
+ * row 3l+u, u = 0 SA, 1 CA, 2 FFN) and step t that is evaluated, the unit's
+ * residual a_{n,b,t} (the branch output after its bias, before the residual
+ * add) into acts_out: device float [batch][3L][T][H][d], caller-owned,
+ * 3L*T*H*d floats per sample.  Positions that are not evaluated are left
+ * untouched, so Sec. 3.3's activations of the uncached policy come from an
+ * all-refresh schedule.  Each sample is one query r of Eq. 6.  Other
+ * arguments, errors and asynchrony as evo_denoise. */
+int evo_collect_activations(evo_policy* p, int32_t batch, const float* obs_cond, const float* noise,
+                            const int32_t* schedule_ids, float* actions_out, float* acts_out, void* hip_stream);
+
+/* Eq. 6: scores_out[b][t] = mean over the queries r < rollouts of
+ * 1/(T-1) sum_{t' != t} (1 - cos(a_{r,b,t}, a_{r,b,t'})), the cosine of a
+ * zero vector taken as 0.  acts: device float [rollouts][3L][T][H][d] as
+ * written by evo_collect_activations; scores_out: device float [3L][T].
+ * Computed in fp32 (step x step Gram matrices on fp32 MFMA, queries averaged
+ * in order, deterministic).  rollouts in [1, max_batch]; 2 <= T <= 128 else
+ * EVO_E_UNSUPPORTED.  Asynchronous on hip_stream; uses a per-policy
+ * workspace, so calls on one policy must not overlap. */
+int evo_redundancy_scores(evo_policy* p, int32_t rollouts, const float* acts, float* scores_out,
+                          void* hip_stream);
+
+/* Eq. 7 on the host: the scores (host float [rows][n_steps]) are normalised
+ * to w in [0, 1] by min-max over all positions (all zeros if constant), and
+ * probs_out[i] = (eps + w_i)^gamma / sum_j (eps + w_j)^gamma (host double,
+ * same shape).  eps, gamma >= 0; the paper gives no values for them. */
+int evo_guided_probabilities(const float* scores, int32_t rows, int32_t n_steps, double eps, double gamma,
+                             double* probs_out);
+
+/* K distinct positions drawn one after another without replacement from
+ * probs (host double [rows][n_steps]), as for an initial individual of the
+ * search (Sec. 3.3).  Implemented as the K largest keys log p - log(-log u)
+ * (Gumbel-top-K, which has exactly that law) with the caller's uniforms
+ * (host double [rows][n_steps], each in (0, 1)); equal keys go to the lower
+ * flat index.  pairs_out: host int32 [K][2] = (row, step), in flat order;
+ * feed it to evo_set_schedule_pairs.  K larger than the number of positions
+ * with p > 0 -> EVO_E_INVALID. */
+int evo_guided_sample(const double* probs, int32_t rows, int32_t n_steps, int32_t K, const double* uniforms,
+                      int32_t* pairs_out);
+
 /* Statistics of the last evo_denoise call (host struct). */
 int evo_get_stats(const evo_policy* p, evo_stats* out);
 

@@ -88,6 +88,7 @@ struct evo_policy {
   float* d_cache = nullptr;
   size_t cache_floats = 0;
   float* d_okv = nullptr;
+  float* d_rpart = nullptr;  // per-query Eq. 6 terms [max_batch][3L][T]
   // small-batch team variant: members per tile, largest batch it serves,
   // partial-residual exchange, barrier counters, device error flag
   int team = 1, team_batch = 0;
@@ -125,6 +126,7 @@ static void release(evo_policy* p) {
   (void)hipFree(p->d_ddpm);
   (void)hipFree(p->d_cache);
   (void)hipFree(p->d_okv);
+  (void)hipFree(p->d_rpart);
   (void)hipFree(p->d_xchg);
   (void)hipFree(p->d_tctr);
   (void)hipFree(p->d_derr);
@@ -308,6 +310,7 @@ int evo_create_policy(const evo_policy_desc* desc, const float* host_weights, si
     p->okv_stride = (size_t)p->team_batch * okv_per;
     CREATE_TRY(hipMalloc(&p->d_okv,
                          std::max((size_t)s.max_batch * okv_per, p->okv_stride * p->team) * sizeof(float)));
+    CREATE_TRY(hipMalloc(&p->d_rpart, (size_t)s.max_batch * U * T * sizeof(float)));
     if (p->team > 1) {
       CREATE_TRY(hipMalloc(&p->d_xchg, (size_t)p->team_batch * 3 * p->team * s.H * d * sizeof(float)));
       CREATE_TRY(hipMalloc(&p->d_tctr, (size_t)p->team_batch * 16 * sizeof(unsigned)));
@@ -364,8 +367,8 @@ int evo_set_schedule_pairs(evo_policy* p, int32_t schedule_id, const int32_t* pa
   return evo_set_schedule(p, schedule_id, lat.data(), rows, T, granularity);
 }
 
-int evo_denoise(evo_policy* p, int32_t batch, const float* obs_cond, const float* noise, const int32_t* schedule_ids,
-                float* actions_out, void* hip_stream) {
+static int denoise_impl(evo_policy* p, int32_t batch, const float* obs_cond, const float* noise,
+                        const int32_t* schedule_ids, float* actions_out, float* acts_out, void* hip_stream) {
   clear_error();
   if (!p) return fail(EVO_E_INVALID, "policy is NULL");
   const Shape& s = p->s;
@@ -449,6 +452,7 @@ int evo_denoise(evo_policy* p, int32_t batch, const float* obs_cond, const float
   kp.pk_win = p->pk_win;
   kp.pk_wout = p->pk_wout;
   kp.obs = obs_cond; kp.noise = noise; kp.out = actions_out; kp.okv = p->d_okv; kp.cache = p->d_cache;
+  kp.acts = acts_out;
   kp.batch = batch;
   kp.team = team;
   if (team > 1) {
@@ -489,6 +493,52 @@ int evo_synchronize(evo_policy* p) {
     }
   }
   return EVO_OK;
+}
+
+int evo_denoise(evo_policy* p, int32_t batch, const float* obs_cond, const float* noise, const int32_t* schedule_ids,
+                float* actions_out, void* hip_stream) {
+  return denoise_impl(p, batch, obs_cond, noise, schedule_ids, actions_out, nullptr, hip_stream);
+}
+
+int evo_collect_activations(evo_policy* p, int32_t batch, const float* obs_cond, const float* noise,
+                            const int32_t* schedule_ids, float* actions_out, float* acts_out, void* hip_stream) {
+  clear_error();
+  if (!acts_out) return fail(EVO_E_INVALID, "acts_out is NULL");
+  return denoise_impl(p, batch, obs_cond, noise, schedule_ids, actions_out, acts_out, hip_stream);
+}
+
+int evo_redundancy_scores(evo_policy* p, int32_t rollouts, const float* acts, float* scores_out, void* hip_stream) {
+  clear_error();
+  if (!p) return fail(EVO_E_INVALID, "policy is NULL");
+  const Shape& s = p->s;
+  if (!acts || !scores_out) return fail(EVO_E_INVALID, "NULL device pointer");
+  if (rollouts < 1 || rollouts > s.max_batch)
+    return fail(EVO_E_INVALID, "rollouts %d outside [1, %d]", rollouts, s.max_batch);
+  if (s.T < 2 || s.T > kGramMaxSteps)
+    return fail(EVO_E_UNSUPPORTED, "redundancy scores need 2 <= n_steps <= %d", kGramMaxSteps);
+  DeviceGuard guard(p->device);
+  hipStream_t stream = (hipStream_t)hip_stream;
+  if (p->launched && stream != p->last_stream) HIP_TRY(hipStreamWaitEvent(stream, p->ev_done, 0));
+  HIP_TRY(launch_redundancy(acts, rollouts, s.U(), s.T, (long long)s.H * s.d, p->d_rpart, scores_out, stream));
+  HIP_TRY(hipEventRecord(p->ev_done, stream));
+  p->last_stream = stream;
+  p->launched = true;
+  return EVO_OK;
+}
+
+int evo_guided_probabilities(const float* scores, int32_t rows, int32_t n_steps, double eps, double gamma,
+                             double* probs_out) {
+  clear_error();
+  if (!scores || !probs_out || rows < 1 || n_steps < 1) return fail(EVO_E_INVALID, "bad arguments");
+  if (!(eps >= 0.0) || !(gamma >= 0.0)) return fail(EVO_E_INVALID, "eps and gamma must be >= 0");
+  return guided_probabilities(scores, (size_t)rows * n_steps, eps, gamma, probs_out);
+}
+
+int evo_guided_sample(const double* probs, int32_t rows, int32_t n_steps, int32_t K, const double* uniforms,
+                      int32_t* pairs_out) {
+  clear_error();
+  if (!probs || !uniforms || !pairs_out || rows < 1 || n_steps < 1) return fail(EVO_E_INVALID, "bad arguments");
+  return guided_sample(probs, rows, n_steps, K, uniforms, pairs_out);
 }
 
 int evo_get_stats(const evo_policy* p, evo_stats* out) {

@@ -2,10 +2,12 @@
 #include "evo_host.hpp"
 
 #include <algorithm>
+#include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
 #include <numeric>
+#include <vector>
 
 namespace evo {
 
@@ -221,6 +223,51 @@ int build_plan(const Shape& s, const std::vector<Schedule>& reg, const int32_t* 
     }
   }
   *out = std::move(p);
+  return EVO_OK;
+}
+
+int guided_probabilities(const float* scores, size_t n, double eps, double gamma, double* p_out) {
+  double lo = scores[0], hi = scores[0];
+  for (size_t i = 0; i < n; ++i) {
+    const double v = scores[i];
+    if (!std::isfinite(v)) return fail(EVO_E_INVALID, "score %zu is not finite", i);
+    lo = std::min(lo, v);
+    hi = std::max(hi, v);
+  }
+  double tot = 0.0;
+  for (size_t i = 0; i < n; ++i) {
+    const double w = hi > lo ? ((double)scores[i] - lo) / (hi - lo) : 0.0;
+    p_out[i] = std::pow(eps + w, gamma);
+    tot += p_out[i];
+  }
+  if (!(tot > 0.0)) return fail(EVO_E_INVALID, "all weights are zero (eps = 0 and constant scores?)");
+  for (size_t i = 0; i < n; ++i) p_out[i] /= tot;
+  return EVO_OK;
+}
+
+int guided_sample(const double* p, int rows, int T, int K, const double* u, int32_t* pairs_out) {
+  const size_t n = (size_t)rows * T;
+  size_t positive = 0;
+  for (size_t i = 0; i < n; ++i) {
+    if (!(p[i] >= 0.0) || !std::isfinite(p[i])) return fail(EVO_E_INVALID, "probability %zu invalid", i);
+    if (!(u[i] > 0.0 && u[i] < 1.0)) return fail(EVO_E_INVALID, "uniform %zu not in (0, 1)", i);
+    positive += p[i] > 0.0;
+  }
+  if (K < 0 || (size_t)K > positive) return fail(EVO_E_INVALID, "K = %d exceeds the %zu positions with p > 0", K, positive);
+  std::vector<std::pair<double, size_t>> key(n);
+  for (size_t i = 0; i < n; ++i)
+    key[i] = {p[i] > 0.0 ? std::log(p[i]) - std::log(-std::log(u[i])) : -HUGE_VAL, i};
+  // K largest keys; equal keys: the lower flat index first
+  std::partial_sort(key.begin(), key.begin() + K, key.end(), [](const auto& a, const auto& b) {
+    return a.first != b.first ? a.first > b.first : a.second < b.second;
+  });
+  std::vector<size_t> chosen(K);
+  for (int k = 0; k < K; ++k) chosen[k] = key[k].second;
+  std::sort(chosen.begin(), chosen.end());
+  for (int k = 0; k < K; ++k) {
+    pairs_out[2 * k] = (int32_t)(chosen[k] / T);
+    pairs_out[2 * k + 1] = (int32_t)(chosen[k] % T);
+  }
   return EVO_OK;
 }
 

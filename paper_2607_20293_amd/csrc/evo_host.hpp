@@ -101,6 +101,15 @@ struct Plan {
 int build_plan(const Shape& s, const std::vector<Schedule>& reg, const int32_t* ids, int batch,
                int spt, int n_xcd, Plan* out);
 
+// Eq. 7 (Sec. 3.3): min-max normalise n scores into w and return
+// p_i = (eps + w_i)^gamma / sum_j (eps + w_j)^gamma in fp64.
+int guided_probabilities(const float* scores, size_t n, double eps, double gamma, double* p_out);
+// K distinct positions of the [rows][T] lattice drawn one after another
+// without replacement from p, by the Gumbel-top-K construction with one
+// given uniform per position in (0, 1) (ties to the lower flat index);
+// pairs_out [K][2] = (row, step) in flat order.
+int guided_sample(const double* p, int rows, int T, int K, const double* u, int32_t* pairs_out);
+
 // Bookkeeping of a call (refreshes, FLOPs, algorithmic bytes).  With
 // `team` workgroups per tile, every member keeps its own caches and
 // observation keys/values, while the per-unit weights are split among them.

@@ -1177,6 +1177,12 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
               }
             }
             h[c][rb] += v;
+            if (p.acts != nullptr && member == 0) {
+              // activation record of the uncached policy (Sec. 3.3): a[sample][unit][step][H][d]
+              float* ap = p.acts + (((size_t)smp[j] * U + e) * T + t) * (HZ * D) + (w * CBW + c) * 16 + lc;
+#pragma unroll
+              for (int i = 0; i < 4; ++i) ap[(size_t)((rb * 16 + lq * 4 + i) % HZ) * D] = v[i];
+            }
           } else if (pick(mru, j) & bit) {
             h[c][rb] += *cfrag(e, c, rb);
           }

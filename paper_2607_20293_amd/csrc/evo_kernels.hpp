@@ -37,6 +37,7 @@ struct KParams {
   float* out;                // [batch][H][A]
   float* okv;                // [batch][L][n_obs][2d] observation-token keys/values
   float* cache;              // [n_tiles * team][3L][rows*d] per-workgroup residual caches
+  float* acts;               // optional [batch][3L][T][H][d] record of evaluated residuals (else null)
   float* xchg;               // [n_tiles][3][team][rows*d] partial residuals of team members
   unsigned* tctr;            // [n_tiles][16] team barrier counters (zeroed before each launch)
   unsigned* derr;            // device error flag (team barrier timed out)
@@ -79,5 +80,12 @@ hipError_t launch_zero_u32(unsigned* dst, int n, hipStream_t stream);
 
 // team size of the small-batch variant for a shape (1: none compiled)
 int kernel_team_size(const KernelKey& key);
+
+// Eq. 6 dissimilarity scores from recorded activations acts [R][U][T][V]:
+// part [R][U][T] receives each query's term, d [U][T] their mean over R
+// (in query order).  T <= kGramMaxSteps.
+constexpr int kGramMaxSteps = 128;
+hipError_t launch_redundancy(const float* acts, int R, int U, int T, long long V, float* part, float* d,
+                             hipStream_t stream);
 
 }  // namespace evo

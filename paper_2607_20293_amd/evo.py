@@ -23,7 +23,30 @@ CODE_EVAL, CODE_STORE, CODE_REUSE, CODE_MERGED = 1, 2, 4, 8
 EXPORTED = ("evo_weight_count", "evo_check_desc", "evo_create_policy", "evo_set_schedule",
             "evo_set_schedule_pairs", "evo_denoise", "evo_get_stats", "evo_schedule_stats",
             "evo_schedule_codes", "evo_debug_read_cache", "evo_synchronize", "evo_destroy_policy",
-            "evo_last_error")
+            "evo_last_error", "evo_collect_activations", "evo_redundancy_scores", "evo_guided_probabilities",
+            "evo_guided_sample")
+
+
+def guided_probabilities(scores, eps: float, gamma: float) -> np.ndarray:
+    """Eq. 7 (host): scores [rows][T] -> probabilities (float64)."""
+    sc = np.ascontiguousarray(np.asarray(scores, np.float32))
+    rows, T = sc.shape
+    out = np.zeros((rows, T), np.float64)
+    _check(lib().evo_guided_probabilities(sc.ctypes.data, rows, T, float(eps), float(gamma), out.ctypes.data))
+    return out
+
+
+def guided_sample(probs, K: int, uniforms) -> np.ndarray:
+    """K distinct (row, step) positions from probs [rows][T] with the given
+    uniforms (same shape, in (0, 1)); int32 [K][2] in flat order."""
+    pr = np.ascontiguousarray(np.asarray(probs, np.float64))
+    u = np.ascontiguousarray(np.asarray(uniforms, np.float64))
+    if u.shape != pr.shape:
+        raise ValueError("uniforms must have the shape of probs")
+    rows, T = pr.shape
+    out = np.zeros((K, 2), np.int32)
+    _check(lib().evo_guided_sample(pr.ctypes.data, rows, T, int(K), u.ctypes.data, out.ctypes.data))
+    return out
 
 
 class EvoError(RuntimeError):
@@ -84,6 +107,14 @@ def lib() -> ctypes.CDLL:
         L.evo_schedule_codes.restype = ctypes.c_int
         L.evo_debug_read_cache.argtypes = [P, I32, I32, P]
         L.evo_debug_read_cache.restype = ctypes.c_int
+        L.evo_collect_activations.argtypes = [P, I32, P, P, P, P, P, P]
+        L.evo_collect_activations.restype = ctypes.c_int
+        L.evo_redundancy_scores.argtypes = [P, I32, P, P, P]
+        L.evo_redundancy_scores.restype = ctypes.c_int
+        L.evo_guided_probabilities.argtypes = [P, I32, I32, ctypes.c_double, ctypes.c_double, P]
+        L.evo_guided_probabilities.restype = ctypes.c_int
+        L.evo_guided_sample.argtypes = [P, I32, I32, I32, P, P]
+        L.evo_guided_sample.restype = ctypes.c_int
         L.evo_synchronize.argtypes = [P]
         L.evo_synchronize.restype = ctypes.c_int
         L.evo_destroy_policy.argtypes = [P]
@@ -185,9 +216,11 @@ class Policy:
         pr = np.ascontiguousarray(np.asarray(pairs, np.int32).reshape(-1, 2))
         _check(lib().evo_set_schedule_pairs(self._h, sid, pr.ctypes.data, pr.shape[0], granularity))
 
-    def denoise(self, obs, noise, ids=None, out=None, stream=None):
+    def denoise(self, obs, noise, ids=None, out=None, stream=None, acts=None):
         """obs: float32 [B][n_obs][obs_dim], noise: float32 [T][B][H][A]
-        (HIP tensors); ids: host int32 [B] or None.  Returns out [B][H][A]."""
+        (HIP tensors); ids: host int32 [B] or None.  Returns out [B][H][A].
+        acts (optional HIP tensor [B][3L][T][H][d]) receives the residuals of
+        the evaluated units (evo_collect_activations)."""
         import torch
         s = self.shape
         B = int(obs.shape[0])
@@ -204,7 +237,33 @@ class Policy:
         else:
             ids_np, pid = None, None
         st = torch.cuda.current_stream(obs.device) if stream is None else stream
-        _check(lib().evo_denoise(self._h, B, po, pn, pid, pout, ctypes.c_void_p(st.cuda_stream)))
+        if acts is None:
+            _check(lib().evo_denoise(self._h, B, po, pn, pid, pout, ctypes.c_void_p(st.cuda_stream)))
+        else:
+            pa = _dev_ptr(acts, "float32", (B, 3 * s.n_layers, s.n_steps, s.horizon, s.d_model))
+            _check(lib().evo_collect_activations(self._h, B, po, pn, pid, pout, pa, ctypes.c_void_p(st.cuda_stream)))
+        return out
+
+    def collect_activations(self, obs, noise, ids=None, stream=None):
+        """denoise that also records every evaluated unit's residual:
+        returns (out [B][H][A], acts [B][3L][T][H][d]) as HIP tensors."""
+        import torch
+        s = self.shape
+        B = int(obs.shape[0])
+        acts = torch.zeros((B, 3 * s.n_layers, s.n_steps, s.horizon, s.d_model), dtype=torch.float32,
+                           device=obs.device)
+        out = self.denoise(obs, noise, ids, stream=stream, acts=acts)
+        return out, acts
+
+    def redundancy_scores(self, acts, rollouts=None, stream=None):
+        """Eq. 6 scores [3L][T] (HIP tensor) from acts [R][3L][T][H][d]."""
+        import torch
+        s = self.shape
+        R = int(acts.shape[0]) if rollouts is None else int(rollouts)
+        pa = _dev_ptr(acts, "float32", (acts.shape[0], 3 * s.n_layers, s.n_steps, s.horizon, s.d_model))
+        out = torch.empty((3 * s.n_layers, s.n_steps), dtype=torch.float32, device=acts.device)
+        st = torch.cuda.current_stream(acts.device) if stream is None else stream
+        _check(lib().evo_redundancy_scores(self._h, R, pa, out.data_ptr(), ctypes.c_void_p(st.cuda_stream)))
         return out
 
     def synchronize(self):

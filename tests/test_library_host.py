@@ -135,3 +135,50 @@ def test_schedule_validation():
     assert e.value.code == -1
     with pytest.raises(evo.EvoError):
         evo.schedule_codes(desc, np.ones((5, s.n_steps), np.uint8), O.GRAN_LAYER)
+
+
+# ---------------------------------------------------------------- Eq. 7 host helpers
+def test_guided_probabilities_match_oracle():
+    from oracle import evo_redundancy as RD
+    rng = np.random.default_rng(11)
+    for shape, eps, gamma in [((24, 100), 0.05, 2.0), ((6, 10), 0.0, 1.0), ((3, 7), 0.5, 0.0)]:
+        d = rng.uniform(0.0, 1.5, size=shape).astype(np.float32)
+        got = evo.guided_probabilities(d, eps, gamma)
+        want = RD.guided_probabilities(d.astype(np.float64), eps, gamma)
+        assert np.allclose(got, want, rtol=1e-12, atol=0.0)
+    flat = np.full((2, 5), 0.3, np.float32)
+    assert np.allclose(evo.guided_probabilities(flat, 0.1, 3.0), 0.1)
+
+
+def test_guided_sample_matches_oracle_bit_exact():
+    from oracle import evo_redundancy as RD
+    rng = np.random.default_rng(12)
+    d = rng.uniform(0.0, 1.0, size=(24, 100)).astype(np.float32)
+    p = RD.guided_probabilities(d.astype(np.float64), 0.05, 2.0)
+    for K in (1, 24, 240, 600):
+        u = rng.uniform(size=p.shape)
+        got = evo.guided_sample(p, K, u)
+        want = RD.guided_sample(p, K, u)
+        assert got.shape == (K, 2) and np.array_equal(got, want), K
+    # zero-probability positions are never drawn; too large K is rejected
+    p0 = np.zeros((2, 4))
+    p0[0, 1], p0[1, 3] = 0.25, 0.75
+    assert np.array_equal(evo.guided_sample(p0, 2, rng.uniform(size=(2, 4))), [[0, 1], [1, 3]])
+    with pytest.raises(evo.EvoError):
+        evo.guided_sample(p0, 3, rng.uniform(size=(2, 4)))
+    with pytest.raises(evo.EvoError):
+        evo.guided_sample(p0, 1, np.ones((2, 4)))          # uniforms must lie in (0, 1)
+
+
+def test_guided_pairs_register_as_a_schedule():
+    """An initial individual from Eq. 7 is a K-pair schedule (Eq. 3)."""
+    s = I.PUSHT
+    desc = evo.make_desc(s, "bf16", max_batch=1, max_schedules=1)
+    rng = np.random.default_rng(13)
+    p = evo.guided_probabilities(rng.uniform(size=(3 * s.n_layers, s.n_steps)).astype(np.float32), 0.05, 2.0)
+    pairs = evo.guided_sample(p, 240, rng.uniform(size=p.shape))
+    lat = np.zeros((3 * s.n_layers, s.n_steps), np.uint8)
+    lat[pairs[:, 0], pairs[:, 1]] = 1
+    assert lat.sum() == 240
+    st = evo.schedule_stats(desc, [lat], np.zeros(1, np.int32), evo.GRAN_UNIT)
+    assert st["refreshes_requested"] == 240
