@@ -260,7 +260,8 @@ class Policy:
         import torch
         s = self.shape
         R = int(acts.shape[0]) if rollouts is None else int(rollouts)
-        pa = _dev_ptr(acts, "float32", (acts.shape[0], 3 * s.n_layers, s.n_steps, s.horizon, s.d_model))
+        acts = acts.reshape(acts.shape[0], 3 * s.n_layers, s.n_steps, s.horizon, s.d_model)
+        pa = _dev_ptr(acts, "float32", tuple(acts.shape))
         out = torch.empty((3 * s.n_layers, s.n_steps), dtype=torch.float32, device=acts.device)
         st = torch.cuda.current_stream(acts.device) if stream is None else stream
         _check(lib().evo_redundancy_scores(self._h, R, pa, out.data_ptr(), ctypes.c_void_p(st.cuda_stream)))
