@@ -219,6 +219,41 @@ def main():
             log(f"[bench] {name}: {extras[name]}")
             del ip
 
+        # ---------------- redundancy statistics (Sec. 3.3): 8 uncached queries of the
+        # Push-T-shaped policy, activations recorded, Eq. 6 scores on the GPU
+        s = I.PUSHT
+        R = 8
+        pol = evo.Policy(s, I.make_weights(s, 0), dtype="fp32", max_batch=R, max_schedules=1)
+        pol.set_schedule(0, np.ones((3 * s.n_layers, s.n_steps), np.uint8), evo.GRAN_UNIT)
+        dev = torch.device("cuda:0")
+        obs_r = torch.from_numpy(I.make_obs(s, R, 0)).to(dev)
+        noise_r = torch.from_numpy(I.make_noise(s, R, 0)).to(dev)
+        _, acts = pol.collect_activations(obs_r, noise_r)
+        sc = pol.redundancy_scores(acts)
+        torch.cuda.synchronize()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        reps = 5
+        ev[0].record()
+        for _ in range(reps):
+            pol.denoise(obs_r, noise_r, acts=acts)
+        ev[1].record()
+        for _ in range(reps):
+            sc = pol.redundancy_scores(acts)
+        ev[2].record()
+        torch.cuda.synchronize()
+        pol.synchronize()
+        pol.close()
+        collect_ms = ev[0].elapsed_time(ev[1]) / reps
+        scores_ms = ev[1].elapsed_time(ev[2]) / reps
+        U, T, V = 3 * s.n_layers, s.n_steps, s.horizon * s.d_model
+        gram_flops = 2.0 * R * U * T * T * V
+        extras["redundancy_pusht_fp32_r8"] = {
+            "collect_ms": round(collect_ms, 4), "scores_ms": round(scores_ms, 4),
+            "gram_TFLOPs": round(gram_flops / (scores_ms * 1e-3) / 1e12, 2),
+            "frac_fp32_peak": round(gram_flops / (scores_ms * 1e-3) / 1e12 / PEAK["fp32"], 4)}
+        log(f"[bench] redundancy_pusht_fp32_r8: {extras['redundancy_pusht_fp32_r8']}")
+        del acts
+
     cpu = None
     if not args.no_cpu_baseline:
         log("[bench] oracle CPU baseline ...")
