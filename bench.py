@@ -200,6 +200,33 @@ def main():
                 log(f"[bench] pusht b1 {dtype} density {dens}: p50 {row[str(dens)]['p50_ms']:.3f} ms "
                     f"kernel {row[str(dens)]['kernel_ms']:.3f} ms")
             lat[dtype] = row
+        # ---------------- comparison schedule families at batch 1 (Push-T-shaped, bf16):
+        # fixed-interval synchronous refresh (EfficientVLA, M = 8, 10), a block-wise
+        # fixed budget (M = 10 per unit) and the printed BAC / EVO Push-T schedules;
+        # FLOP speed-up (full / cached-path FLOPs) next to the measured one
+        gold = os.path.join(ROOT, "tests", "golden", "schedules_pusht.txt")
+        U = 3 * s.n_layers
+        fams = {"full": I.lattice_all(U, s.n_steps),
+                "efficientvla_M8": I.lattice_fixed_interval(U, s.n_steps, 8),
+                "efficientvla_M10": I.lattice_fixed_interval(U, s.n_steps, 10),
+                "blockwise_M10": I.lattice_blockwise_budget(U, s.n_steps, 10, np.random.default_rng(10)),
+                "printed_bac": I.printed_lattice(gold, "BAC", s.n_layers, s.n_steps),
+                "printed_evo": I.printed_lattice(gold, "EVO", s.n_layers, s.n_steps)}
+        fam = {}
+        for fname, lt in fams.items():
+            r = Runner(f"pusht_bf16_b1_{fname}", s, wts, "bf16", [lt], np.zeros(1, np.int32), obs1, noise1,
+                       gran=1)
+            ls = r.latency(30, 3)
+            sx = r.pol.stats()
+            r.close()
+            fam[fname] = {"p50_ms": round(statistics.median(ls), 4),
+                          "refreshes": int(sx["refreshes_effective"]),
+                          "flop_speedup": round(sx["flops_full"] / (sx["flops_cacheable"] + sx["flops_always"]), 3)}
+        for fname in fam:
+            fam[fname]["measured_speedup"] = round(fam["full"]["p50_ms"] / fam[fname]["p50_ms"], 3)
+            log(f"[bench] schedule family {fname}: {fam[fname]}")
+        extras["schedule_families_pusht_bf16_b1"] = fam
+
         # ---------------- other workloads
         for name in ("tiny_fp32_b1", "pusht_bf16_b64_d25", "population_bf16_b512", "bimanual_bf16_b128_d20",
                      "bimanual_bf16_b128_all"):

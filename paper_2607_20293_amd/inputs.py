@@ -244,6 +244,56 @@ def lattice_dirichlet_k(rows: int, T: int, K: int, rng) -> np.ndarray:
     return lat
 
 
+def lattice_fixed_interval(rows: int, T: int, M: int) -> np.ndarray:
+    """The comparison schedule the paper attributes to EfficientVLA (Sec. 1,
+    Sec. 4.1): every unit refreshed synchronously, M times per query at a
+    fixed interval: steps floor(i * T / M), i = 0 .. M-1 (step 0 included)."""
+    assert 1 <= M <= T
+    lat = np.zeros((rows, T), np.uint8)
+    lat[:, [(i * T) // M for i in range(M)]] = 1
+    return lat
+
+
+def lattice_blockwise_budget(rows: int, T: int, M: int, rng) -> np.ndarray:
+    """A block-wise fixed budget (the search space the paper attributes to
+    BAC, Sec. 2): exactly M refreshes per unit, step 0 and M-1 further steps
+    drawn without replacement per unit."""
+    assert 1 <= M <= T
+    lat = np.zeros((rows, T), np.uint8)
+    lat[:, 0] = 1
+    for r in range(rows):
+        lat[r, rng.choice(np.arange(1, T), size=M - 1, replace=False)] = 1
+    return lat
+
+
+def read_printed_schedules(path: str) -> Dict[str, Dict[str, List[int]]]:
+    """{method: {unit name: [steps]}} from a text file of printed refresh
+    schedules, one line per (unit, method): unit name, method, comma-separated
+    refreshed steps."""
+    out: Dict[str, Dict[str, List[int]]] = {}
+    with open(path) as f:
+        for line in f:
+            line = line.strip()
+            if not line or line.startswith("#"):
+                continue
+            parts = line.split()
+            steps = [int(x) for x in parts[2].split(",")] if len(parts) > 2 else []
+            out.setdefault(parts[1], {})[parts[0]] = steps
+    return out
+
+
+def printed_lattice(path: str, method: str, n_layers: int, T: int) -> np.ndarray:
+    """Unit-granular lattice [3L][T] (rows layer-major SA, CA, FFN) of one
+    method's printed schedule."""
+    sch = read_printed_schedules(path)[method]
+    lat = np.zeros((3 * n_layers, T), np.uint8)
+    for l in range(n_layers):
+        for u, nm in enumerate(("SA", "CA", "FFN")):
+            for t in sch[f"layers.{l}.{nm}"]:
+                lat[3 * l + u, t] = 1
+    return lat
+
+
 def make_lattice(kind: str, rows: int, T: int, density: float, seed: int, j: int = 0) -> np.ndarray:
     rng = np.random.default_rng([seed, 3, j])
     if kind == "all":

@@ -304,6 +304,25 @@ def test_printed_schedules(cold):
         pol.close()
 
 
+def test_comparison_schedule_families():
+    """Fixed-interval synchronous refresh (EfficientVLA, M = 8 and 10) and
+    block-wise fixed budgets (M = 10 per unit), unit- and layer-granular, on
+    the 8-layer policy, one sample per schedule."""
+    s = I.PUSHT
+    wts = I.make_weights(s, 5, "perturbed")
+    U, T = 3 * s.n_layers, s.n_steps
+    rng = np.random.default_rng(5)
+    for gran, rows in ((O.GRAN_UNIT, U), (O.GRAN_LAYER, s.n_layers)):
+        lats = [I.lattice_fixed_interval(rows, T, 8), I.lattice_fixed_interval(rows, T, 10),
+                I.lattice_blockwise_budget(rows, T, 10, rng)]
+        B = len(lats)
+        obs, noise = I.make_obs(s, B, 5), I.make_noise(s, B, 5)
+        ids = np.arange(B, dtype=np.int32)
+        for dtype in ("fp32", "bf16"):
+            pol, *_ = _case(f"families_{dtype}_gran{gran}", s, wts, obs, noise, lats, ids, dtype, gran=gran)
+            pol.close()
+
+
 def test_hand_lattice_most_recent_unit():
     """One unit refreshed at steps {0, 2, 6} only, every other unit always."""
     s = I.TINY

@@ -182,3 +182,27 @@ def test_guided_pairs_register_as_a_schedule():
     assert lat.sum() == 240
     st = evo.schedule_stats(desc, [lat], np.zeros(1, np.int32), evo.GRAN_UNIT)
     assert st["refreshes_requested"] == 240
+
+
+# ---------------------------------------------------------------- comparison schedule families
+def test_fixed_interval_and_blockwise_families():
+    """EfficientVLA-style fixed-interval lattices (every unit M times,
+    synchronously) and block-wise fixed budgets (M per unit): refresh counts
+    and the FLOP identity flops_cacheable = M x rows x per-unit FLOPs."""
+    s = I.PUSHT
+    rows, T = 3 * s.n_layers, s.n_steps
+    desc = evo.make_desc(s, "bf16", max_batch=1, max_schedules=1)
+    F = O.unit_flops(s)
+    per_layer = F["SA"] + F["CA"] + F["FFN"]
+    for M in (8, 10):
+        lat = I.lattice_fixed_interval(rows, T, M)
+        assert (lat.sum(axis=1) == M).all() and lat[:, 0].all()
+        assert (lat == lat[0]).all()                                   # synchronous
+        st = evo.schedule_stats(desc, [lat], np.zeros(1, np.int32), evo.GRAN_UNIT)
+        assert st["refreshes_requested"] == M * rows
+        assert st["flops_cacheable"] == M * s.n_layers * per_layer
+        blk = I.lattice_blockwise_budget(rows, T, M, np.random.default_rng(M))
+        assert (blk.sum(axis=1) == M).all() and blk[:, 0].all()
+        st2 = evo.schedule_stats(desc, [blk], np.zeros(1, np.int32), evo.GRAN_UNIT)
+        assert st2["flops_cacheable"] == st["flops_cacheable"]
+    assert I.lattice_fixed_interval(2, 100, 8)[0].nonzero()[0].tolist() == [0, 12, 25, 37, 50, 62, 75, 87]
