@@ -281,6 +281,35 @@ def main():
         log(f"[bench] redundancy_pusht_fp32_r8: {extras['redundancy_pusht_fp32_r8']}")
         del acts
 
+        # ---------------- schedule search (Sec. 3.2, Sec. 4.1 settings): K = 240 on the
+        # Push-T-shaped policy in bf16, population 30, 10 elites, 30 generations, 16 quick
+        # episodes per schedule (one batched call of up to 480 episodes per generation),
+        # guided individuals from the Eq. 6 scores above, synthetic success fitness
+        s = I.PUSHT
+        rows, T = 3 * s.n_layers, s.n_steps
+        probs = evo.guided_probabilities(sc.cpu().numpy(), 0.05, 2.0)
+        nq, P = 16, 30
+        pol = evo.Policy(s, I.make_weights(s, 0), dtype="bf16", max_batch=P * nq, max_schedules=P)
+        obs_q = torch.from_numpy(I.make_obs(s, nq, 91)).to(dev)
+        noise_q = torch.from_numpy(I.make_noise(s, nq, 91)).to(dev)
+        obs_f = torch.from_numpy(I.make_obs(s, 64, 92)).to(dev)
+        noise_f = torch.from_numpy(I.make_noise(s, 64, 92)).to(dev)
+        cfg = evo.GAConfig.make(240, pop_size=P, n_elite=10, max_generations=30, n_guided=15, seed=0)
+        t0 = time.perf_counter()
+        res = pol.search(cfg, obs_q, noise_q, obs_f, noise_f, probs=probs, tau=0.4, q_base=1.0, delta_acc=0.125)
+        wall = time.perf_counter() - t0
+        pol.close()
+        fits = res["fitness"]
+        extras["search_pusht_bf16_K240"] = {
+            "seconds": round(wall, 3), "generations": res["generations"], "evaluations": res["evaluations"],
+            "formal_evaluations": res["formal_evaluations"], "accepted": res["accepted"],
+            "ms_per_generation": round(wall / res["generations"] * 1e3, 2),
+            "episodes_per_s": round((res["evaluations"] * nq + res["formal_evaluations"] * 64) / wall, 1),
+            "best_quick_initial": float(np.max(fits[0])), "best_quick": res["best_quick"],
+            "mean_quick_initial": round(float(np.mean(fits[0])), 4),
+            "mean_quick_last": round(float(np.mean(fits[-1])), 4)}
+        log(f"[bench] search_pusht_bf16_K240: {extras['search_pusht_bf16_K240']}")
+
     cpu = None
     if not args.no_cpu_baseline:
         log("[bench] oracle CPU baseline ...")

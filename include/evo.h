@@ -222,6 +222,124 @@ int evo_guided_probabilities(const float* scores, int32_t rows, int32_t n_steps,
 int evo_guided_sample(const double* probs, int32_t rows, int32_t n_steps, int32_t K, const double* uniforms,
                       int32_t* pairs_out);
 
+/* ---- Schedule search (Sec. 3.2 with Eq. 4 and Eq. 5; Sec. 3.3 with Eq. 7,
+ * Eq. 8 and Eq. 9; population settings of Sec. 4.1).  Offline: finds a
+ * fixed-budget schedule for the cached loop by evolutionary search.
+ *
+ * A schedule (individual) is K distinct flat positions p = b*T + t of the
+ * rows x T lattice (rows = 3L units or L layers), sorted ascending; that
+ * array is its signature.  Randomness: Philox4x64-10 (Salmon et al., SC
+ * 2011), key (seed, 0), counter (generation, purpose << 32 | slot, index, 0),
+ * first output word w; uniform (0, 1) = ((w >> 12) + 1/2) 2^-52, integer
+ * [0, n) = ((w >> 32) n) >> 32, coin = top bit.  Purposes: 1 initial
+ * individual, 2 tournament, 3 crossover, 4 mutation test, 5 mutation target,
+ * 6 repair drop, 7 repair fill; slot = individual or child index, index =
+ * lattice position or entrant number.
+ *
+ * Operators (the paper names them without parameters; these are the
+ * readings):
+ *  - initial population: individuals 0 .. n_guided-1 take K positions from
+ *    Eq. 7's probabilities (evo_guided_sample with uniforms of purpose 1),
+ *    the others the K positions with the largest purpose-1 words (a uniform
+ *    K-subset);
+ *  - ranking: fitness descending, ties to the lower population index; the
+ *    next population is the n_elite best in that order, then the children;
+ *  - tournament: `tournament` entrants drawn with replacement, highest
+ *    fitness wins, ties to the lower index; two tournaments per child;
+ *  - set-level crossover: positions of both parents kept, each position of
+ *    one parent kept on a coin;
+ *  - mutation: each position replaced, with probability mutation_rate, by a
+ *    position drawn uniformly from the whole lattice;
+ *  - repair: duplicates merge; above K keep the K positions with the largest
+ *    purpose-6 words; below K add the missing positions (not yet in the
+ *    child) with the largest purpose-7 words. */
+typedef struct {
+  int32_t K;                /* refreshes per schedule, 1 <= K <= rows*T (Eq. 5) */
+  int32_t pop_size;         /* population size (Sec. 4.1: 30) */
+  int32_t n_elite;          /* elites carried over, 0 .. pop_size (Sec. 4.1: 10) */
+  int32_t max_generations;  /* evaluated populations, the initial one included (Sec. 4.1: 30) */
+  int32_t tournament;       /* entrants per tournament, >= 1 */
+  int32_t n_guided;         /* initial individuals drawn from Eq. 7, 0 .. pop_size */
+  double mutation_rate;     /* in [0, 1] */
+  uint64_t seed;            /* generator key */
+} evo_ga_config;
+
+typedef struct {
+  int32_t generations;         /* populations evaluated */
+  int32_t evaluations;         /* distinct schedules given a quick evaluation */
+  int32_t memo_hits;           /* population members whose signature was already evaluated */
+  int32_t formal_evaluations;  /* schedules given a formal evaluation (Eq. 8 trigger) */
+  int32_t accepted;            /* 1: a schedule passed Eq. 9 and ended the search */
+  int32_t reserved;
+  double best_quick;           /* quick fitness of the returned schedule */
+  double best_formal;          /* its formal score, NaN if it had none */
+} evo_search_result;
+
+/* Quick fitness of n schedules (host int32 [n][K]) into fitness_out (host
+ * double [n]); formal score of one schedule (host int32 [K]).  Return 0, or
+ * nonzero to abort the search (EVO_E_STATE). */
+typedef int (*evo_quick_fn)(void* user, int32_t n, const int32_t* schedules, double* fitness_out);
+typedef int (*evo_formal_fn)(void* user, const int32_t* schedule, double* score_out);
+
+/* The initial population (host int32 [pop_size][K]).  probs: Eq. 7
+ * probabilities, host double [rows][n_steps], needed when n_guided > 0
+ * (else may be NULL); K must not exceed the positions with p > 0. */
+int evo_ga_initial_population(const evo_ga_config* cfg, int32_t rows, int32_t n_steps, const double* probs,
+                              int32_t* pop_out);
+
+/* Population `generation` (>= 1) from population generation-1 (host int32
+ * [pop_size][K], each sorted and duplicate-free) and its fitness (host
+ * double [pop_size], no NaN): elites, then children by tournament,
+ * crossover, mutation and repair. */
+int evo_ga_next_generation(const evo_ga_config* cfg, int32_t rows, int32_t n_steps, int32_t generation,
+                           const int32_t* pop, const double* fitness, int32_t* next_out);
+
+/* The search loop on the host with caller-supplied fitness.  Each
+ * generation, the schedules whose signature has no fitness yet are passed to
+ * `quick` once (in population order, duplicates once); results are
+ * memoised.  Early stopping (formal != NULL): after a generation is
+ * evaluated, its members with quick fitness >= q_base (Eq. 8) that were not
+ * formally evaluated before get `formal`, best first; the first with score
+ * >= q_base - delta_acc (Eq. 9) is returned with accepted = 1.  Otherwise
+ * the best member of the last population is returned.  best_out: host int32
+ * [K].  pop_history (host int32 [max_generations][pop_size][K]) and
+ * fit_history (host double [max_generations][pop_size]) may be NULL; the
+ * first `generations` entries are written. */
+int evo_ga_search(const evo_ga_config* cfg, int32_t rows, int32_t n_steps, const double* probs,
+                  evo_quick_fn quick, evo_formal_fn formal, void* user, double q_base, double delta_acc,
+                  evo_search_result* result, int32_t* best_out, int32_t* pop_history, double* fit_history);
+
+/* Fitness on the GPU for evo_search: a synthetic stand-in for Eq. 4's
+ * rollout success rate (no simulator): episode n of a schedule succeeds when
+ * its action chunk stays within tau (max-abs over H x A, decided in fp32) of
+ * the chunk of the uncached policy (every unit evaluated at every step) for
+ * the same observation and noise; the fitness is the fraction of successes.
+ * The uncached policy scores 1, so q_base = 1 is Eq. 8's target. */
+typedef struct {
+  int32_t granularity;  /* EVO_GRAN_UNIT (rows 3L) or EVO_GRAN_LAYER (rows L) */
+  int32_t n_quick;      /* quick episodes, >= 1; pop_size * n_quick <= max_batch */
+  int32_t n_formal;     /* formal episodes (independent seeds), 0 = no early stopping; <= max_batch */
+  float tau;            /* success threshold, >= 0 */
+  double q_base;        /* Eq. 8 target */
+  double delta_acc;     /* Eq. 9 allowed drop, >= 0 */
+} evo_search_options;
+
+/* The search with GPU fitness: every generation's new schedules are
+ * evaluated in one evo_denoise call (schedule j on episodes j*n_quick ..
+ * (j+1)*n_quick-1, the same n_quick observations and noises for every
+ * schedule), deviations from the uncached chunks reduced on the device.
+ * obs_quick, noise_quick: device, [n_quick][n_obs][obs_dim] and
+ * [T][n_quick][H][A] as for evo_denoise; obs_formal, noise_formal the same
+ * for n_formal episodes (NULL if n_formal == 0).  probs, result, best_out,
+ * histories as evo_ga_search.  Needs pop_size <= max_schedules; the search
+ * overwrites schedule ids 0 .. pop_size-1 (their contents afterwards are
+ * unspecified).  Allocates and frees its own device workspace; synchronous
+ * (returns when the search is done); runs on hip_stream. */
+int evo_search(evo_policy* p, const evo_ga_config* cfg, const evo_search_options* opt, const float* obs_quick,
+               const float* noise_quick, const float* obs_formal, const float* noise_formal, const double* probs,
+               evo_search_result* result, int32_t* best_out, int32_t* pop_history, double* fit_history,
+               void* hip_stream);
+
 /* Statistics of the last evo_denoise call (host struct). */
 int evo_get_stats(const evo_policy* p, evo_stats* out);
 

@@ -18,18 +18,6 @@ using namespace evo;
 
 namespace {
 
-// Makes the policy's device current for the duration of a call.
-struct DeviceGuard {
-  int prev = -1, want = -1;
-  explicit DeviceGuard(int dev) : want(dev) {
-    if (hipGetDevice(&prev) != hipSuccess) prev = -1;
-    if (prev != want) (void)hipSetDevice(want);
-  }
-  ~DeviceGuard() {
-    if (prev >= 0 && prev != want) (void)hipSetDevice(prev);
-  }
-};
-
 #define HIP_TRY(expr)                                                                        \
   do {                                                                                       \
     hipError_t e_ = (expr);                                                                  \
@@ -114,6 +102,11 @@ struct evo_policy {
   int last_threads = 0;
   int last_team = 1;
 };
+
+namespace evo {
+const Shape& policy_shape(const evo_policy* p) { return p->s; }
+int policy_device(const evo_policy* p) { return p->device; }
+}  // namespace evo
 
 static void release(evo_policy* p) {
   if (!p) return;

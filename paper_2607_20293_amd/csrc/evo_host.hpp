@@ -6,6 +6,7 @@
 
 #include <cstdint>
 #include <string>
+#include <functional>
 #include <vector>
 
 #include "evo.h"
@@ -113,6 +114,22 @@ int guided_sample(const double* p, int rows, int T, int K, const double* u, int3
 // Bookkeeping of a call (refreshes, FLOPs, algorithmic bytes).  With
 // `team` workgroups per tile, every member keeps its own caches and
 // observation keys/values, while the per-unit weights are split among them.
+// shape and device of a policy (evo_api.hip)
+const Shape& policy_shape(const evo_policy* p);
+int policy_device(const evo_policy* p);
+
+// schedule search (evo_ga.cpp)
+struct SearchEval {
+  std::function<int(int, const int32_t*, double*)> quick;  // n schedules [n][K] -> fitness [n]
+  std::function<int(const int32_t*, double*)> formal;      // one schedule -> formal score (empty: none)
+};
+int ga_check(const evo_ga_config* c, int rows, int T, const double* probs, bool initial);
+int ga_check_population(const int32_t* pop, int P, int K, int N);
+int ga_initial(const evo_ga_config& c, int rows, int T, const double* probs, int32_t* pop);
+int ga_next(const evo_ga_config& c, int rows, int T, int gen, const int32_t* pop, const double* fit, int32_t* next);
+int ga_search(const evo_ga_config& c, int rows, int T, const double* probs, const SearchEval& ev, double q_base,
+              double delta_acc, evo_search_result* res, int32_t* best_out, int32_t* pop_hist, double* fit_hist);
+
 void call_stats(const Shape& s, const std::vector<Schedule>& reg, const int32_t* ids, int batch,
                 const Plan* plan, int team, evo_stats* out);
 

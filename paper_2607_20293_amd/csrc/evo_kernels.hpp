@@ -6,6 +6,18 @@
 
 namespace evo {
 
+// Makes a device current for the duration of a scope.
+struct DeviceGuard {
+  int prev = -1, want = -1;
+  explicit DeviceGuard(int dev) : want(dev) {
+    if (hipGetDevice(&prev) != hipSuccess) prev = -1;
+    if (prev != want) (void)hipSetDevice(want);
+  }
+  ~DeviceGuard() {
+    if (prev >= 0 && prev != want) (void)hipSetDevice(prev);
+  }
+};
+
 // Float offsets (into the fp32 parameter copy) of one layer's small tensors.
 struct LayerOff {
   uint32_t ln1_g, ln1_b, b_qkv, b_o, ln2_g, ln2_b, b_q, b_kv, b_o2, ln3_g, ln3_b, b_1, b_2;

@@ -24,7 +24,8 @@ EXPORTED = ("evo_weight_count", "evo_check_desc", "evo_create_policy", "evo_set_
             "evo_set_schedule_pairs", "evo_denoise", "evo_get_stats", "evo_schedule_stats",
             "evo_schedule_codes", "evo_debug_read_cache", "evo_synchronize", "evo_destroy_policy",
             "evo_last_error", "evo_collect_activations", "evo_redundancy_scores", "evo_guided_probabilities",
-            "evo_guided_sample")
+            "evo_guided_sample", "evo_ga_initial_population", "evo_ga_next_generation", "evo_ga_search",
+            "evo_search")
 
 
 def guided_probabilities(scores, eps: float, gamma: float) -> np.ndarray:
@@ -47,6 +48,117 @@ def guided_sample(probs, K: int, uniforms) -> np.ndarray:
     out = np.zeros((K, 2), np.int32)
     _check(lib().evo_guided_sample(pr.ctypes.data, rows, T, int(K), u.ctypes.data, out.ctypes.data))
     return out
+
+
+class GAConfig(ctypes.Structure):
+    """evo_ga_config (Sec. 3.2 / Sec. 4.1 defaults: population 30, 10 elites,
+    30 generations)."""
+    _fields_ = [("K", ctypes.c_int32), ("pop_size", ctypes.c_int32), ("n_elite", ctypes.c_int32),
+                ("max_generations", ctypes.c_int32), ("tournament", ctypes.c_int32),
+                ("n_guided", ctypes.c_int32), ("mutation_rate", ctypes.c_double), ("seed", ctypes.c_uint64)]
+
+    @classmethod
+    def make(cls, K, pop_size=30, n_elite=10, max_generations=30, tournament=2, n_guided=15,
+             mutation_rate=0.05, seed=0):
+        return cls(int(K), int(pop_size), int(n_elite), int(max_generations), int(tournament), int(n_guided),
+                   float(mutation_rate), int(seed))
+
+
+class SearchResult(ctypes.Structure):
+    _fields_ = [("generations", ctypes.c_int32), ("evaluations", ctypes.c_int32), ("memo_hits", ctypes.c_int32),
+                ("formal_evaluations", ctypes.c_int32), ("accepted", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("best_quick", ctypes.c_double), ("best_formal", ctypes.c_double)]
+
+    def as_dict(self):
+        return {n: (float(getattr(self, n)) if n.startswith("best") else int(getattr(self, n)))
+                for n, _ in self._fields_ if n != "reserved"}
+
+
+class SearchOptions(ctypes.Structure):
+    _fields_ = [("granularity", ctypes.c_int32), ("n_quick", ctypes.c_int32), ("n_formal", ctypes.c_int32),
+                ("tau", ctypes.c_float), ("q_base", ctypes.c_double), ("delta_acc", ctypes.c_double)]
+
+
+QUICK_FN = ctypes.CFUNCTYPE(ctypes.c_int, ctypes.c_void_p, ctypes.c_int32, ctypes.POINTER(ctypes.c_int32),
+                            ctypes.POINTER(ctypes.c_double))
+FORMAL_FN = ctypes.CFUNCTYPE(ctypes.c_int, ctypes.c_void_p, ctypes.POINTER(ctypes.c_int32),
+                             ctypes.POINTER(ctypes.c_double))
+
+
+def _probs_ptr(probs, rows, T):
+    if probs is None:
+        return None, None
+    pr = np.ascontiguousarray(np.asarray(probs, np.float64))
+    if pr.size != rows * T:
+        raise ValueError(f"probs must have {rows} x {T} entries")
+    return pr, pr.ctypes.data
+
+
+def ga_initial_population(cfg: GAConfig, rows: int, T: int, probs=None) -> np.ndarray:
+    """Initial population int32 [pop_size][K] (sorted flat positions)."""
+    pr, pp = _probs_ptr(probs, rows, T)
+    out = np.zeros((cfg.pop_size, cfg.K), np.int32)
+    _check(lib().evo_ga_initial_population(ctypes.byref(cfg), rows, T, pp, out.ctypes.data))
+    return out
+
+
+def ga_next_generation(cfg: GAConfig, rows: int, T: int, generation: int, pop, fitness) -> np.ndarray:
+    pop = np.ascontiguousarray(np.asarray(pop, np.int32).reshape(cfg.pop_size, cfg.K))
+    fit = np.ascontiguousarray(np.asarray(fitness, np.float64).reshape(cfg.pop_size))
+    out = np.zeros_like(pop)
+    _check(lib().evo_ga_next_generation(ctypes.byref(cfg), rows, T, int(generation), pop.ctypes.data,
+                                        fit.ctypes.data, out.ctypes.data))
+    return out
+
+
+def _search_out(cfg, res, best, ph, fh):
+    d = res.as_dict()
+    g = d["generations"]
+    d["best"] = best
+    d["populations"] = ph[:g]
+    d["fitness"] = fh[:g]
+    return d
+
+
+def ga_search(cfg: GAConfig, rows: int, T: int, quick, formal=None, probs=None, q_base: float = 1.0,
+              delta_acc: float = 0.0) -> dict:
+    """The host search loop with Python fitness callbacks: quick(int32
+    [n][K]) -> n floats; formal(int32 [K]) -> float."""
+    pr, pp = _probs_ptr(probs, rows, T)
+    K = cfg.K
+    err = []
+
+    def _quick(user, n, sch, out):
+        try:
+            a = np.ctypeslib.as_array(sch, shape=(n, K)).copy()
+            v = np.asarray(quick(a), np.float64).reshape(n)
+            for i in range(n):
+                out[i] = float(v[i])
+            return 0
+        except Exception as e:          # reported after the call returns
+            err.append(e)
+            return 1
+
+    def _formal(user, sch, out):
+        try:
+            out[0] = float(formal(np.ctypeslib.as_array(sch, shape=(K,)).copy()))
+            return 0
+        except Exception as e:
+            err.append(e)
+            return 1
+
+    qf = QUICK_FN(_quick)
+    ff = FORMAL_FN(_formal) if formal is not None else FORMAL_FN()
+    res = SearchResult()
+    best = np.zeros(K, np.int32)
+    ph = np.zeros((cfg.max_generations, cfg.pop_size, K), np.int32)
+    fh = np.zeros((cfg.max_generations, cfg.pop_size), np.float64)
+    rc = lib().evo_ga_search(ctypes.byref(cfg), rows, T, pp, qf, ff, None, float(q_base), float(delta_acc),
+                             ctypes.byref(res), best.ctypes.data, ph.ctypes.data, fh.ctypes.data)
+    if err:
+        raise err[0]
+    _check(rc)
+    return _search_out(cfg, res, best, ph, fh)
 
 
 class EvoError(RuntimeError):
@@ -115,6 +227,16 @@ def lib() -> ctypes.CDLL:
         L.evo_guided_probabilities.restype = ctypes.c_int
         L.evo_guided_sample.argtypes = [P, I32, I32, I32, P, P]
         L.evo_guided_sample.restype = ctypes.c_int
+        L.evo_ga_initial_population.argtypes = [ctypes.POINTER(GAConfig), I32, I32, P, P]
+        L.evo_ga_initial_population.restype = ctypes.c_int
+        L.evo_ga_next_generation.argtypes = [ctypes.POINTER(GAConfig), I32, I32, I32, P, P, P]
+        L.evo_ga_next_generation.restype = ctypes.c_int
+        L.evo_ga_search.argtypes = [ctypes.POINTER(GAConfig), I32, I32, P, QUICK_FN, FORMAL_FN, P,
+                                    ctypes.c_double, ctypes.c_double, ctypes.POINTER(SearchResult), P, P, P]
+        L.evo_ga_search.restype = ctypes.c_int
+        L.evo_search.argtypes = [P, ctypes.POINTER(GAConfig), ctypes.POINTER(SearchOptions), P, P, P, P, P,
+                                 ctypes.POINTER(SearchResult), P, P, P, P]
+        L.evo_search.restype = ctypes.c_int
         L.evo_synchronize.argtypes = [P]
         L.evo_synchronize.restype = ctypes.c_int
         L.evo_destroy_policy.argtypes = [P]
@@ -266,6 +388,38 @@ class Policy:
         st = torch.cuda.current_stream(acts.device) if stream is None else stream
         _check(lib().evo_redundancy_scores(self._h, R, pa, out.data_ptr(), ctypes.c_void_p(st.cuda_stream)))
         return out
+
+    def search(self, cfg: GAConfig, obs_quick, noise_quick, obs_formal=None, noise_formal=None, probs=None,
+               granularity: int = GRAN_UNIT, tau: float = 0.1, q_base: float = 1.0, delta_acc: float = 0.0,
+               stream=None) -> dict:
+        """evo_search: GA over fixed-budget schedules with the GPU fitness
+        (fraction of episodes whose chunk stays within tau of the uncached
+        chunk).  obs/noise: HIP tensors as for denoise with n_quick / n_formal
+        episodes.  Returns the result fields, 'best' (flat positions) and the
+        per-generation 'populations' and 'fitness'."""
+        import torch
+        s = self.shape
+        nq = int(obs_quick.shape[0])
+        pq = _dev_ptr(obs_quick, "float32", (nq, s.n_obs, s.obs_dim))
+        pnq = _dev_ptr(noise_quick, "float32", (s.n_steps, nq, s.horizon, s.action_dim))
+        nf, pf, pnf = 0, None, None
+        if obs_formal is not None:
+            nf = int(obs_formal.shape[0])
+            pf = _dev_ptr(obs_formal, "float32", (nf, s.n_obs, s.obs_dim))
+            pnf = _dev_ptr(noise_formal, "float32", (s.n_steps, nf, s.horizon, s.action_dim))
+        rows = 3 * s.n_layers if granularity == GRAN_UNIT else s.n_layers
+        pr, pp = _probs_ptr(probs, rows, s.n_steps)
+        opt = SearchOptions(int(granularity), nq, nf, float(tau), float(q_base), float(delta_acc))
+        res = SearchResult()
+        K = cfg.K
+        best = np.zeros(K, np.int32)
+        ph = np.zeros((cfg.max_generations, cfg.pop_size, K), np.int32)
+        fh = np.zeros((cfg.max_generations, cfg.pop_size), np.float64)
+        st = torch.cuda.current_stream(obs_quick.device) if stream is None else stream
+        _check(lib().evo_search(self._h, ctypes.byref(cfg), ctypes.byref(opt), pq, pnq, pf, pnf, pp,
+                                ctypes.byref(res), best.ctypes.data, ph.ctypes.data, fh.ctypes.data,
+                                ctypes.c_void_p(st.cuda_stream)))
+        return _search_out(cfg, res, best, ph, fh)
 
     def synchronize(self):
         """Wait for the last denoise call; raise if its kernel reported a
