@@ -131,6 +131,8 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--only-main", action="store_true", help="headline workload only (profiling runs)")
+    ap.add_argument("--workload", default="image_bf16_b256_d12",
+                    help="workload timed for the main line (profiling runs of other workloads)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calib-copy", action="store_true", help="also run one 256 MiB device copy (counter scale)")
     args = ap.parse_args()
@@ -153,7 +155,7 @@ def main():
         del x, y
 
     # ---------------- headline: batch 256, shared 12.5% lattice
-    w = I.WORKLOADS["image_bf16_b256_d12"]
+    w = I.WORKLOADS[args.workload]
     inp = I.make_inputs(w)
     log(f"[bench] {w.name}: setup")
     run = Runner(w.name, w.shape, inp.weights, w.dtype, inp.lattices, inp.ids, inp.obs, inp.noise)
@@ -166,16 +168,17 @@ def main():
     k_avg_ms = float(np.mean(kms))
     log(f"[bench] {w.name}: {value:.1f} chunks/s, {ms_per_step:.3f} ms/call, kernel {k_avg_ms:.3f} ms")
     achieved = st["flops_kernel"] / (k_avg_ms * 1e-3) / 1e12
-    roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK["bf16"], "unit": "TFLOP/s",
-            "frac": round(achieved / PEAK["bf16"], 4), "traffic": None,
+    roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK[w.dtype], "unit": "TFLOP/s",
+            "frac": round(achieved / PEAK[w.dtype], 4), "traffic": None,
             "kernel": "denoise_kernel", "kernel_ms": round(k_avg_ms, 4),
             "flops_per_launch": st["flops_kernel"],
             "weight_stream_GBps": round(st["weight_bytes"] / (k_avg_ms * 1e-3) / 1e9, 1)}
     if os.path.exists(COUNTERS):
         try:
             c = json.load(open(COUNTERS))
-            if c.get("source_sha") == kernel_source_sha():
+            if c.get("source_sha") == kernel_source_sha() and c.get("workload") == w.name:
                 roof["traffic"] = c["hbm_bytes_per_launch"]
+                roof["mfma_util_pct_counter"] = c.get("mfma_util_pct")
         except Exception:
             pass
 
@@ -319,7 +322,7 @@ def main():
     res = {
         "metric": METRIC, "value": round(value, 2), "unit": "chunks/s", "n_gpus": 1, "steps": K,
         "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4), "higher_is_better": True,
-        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "scaling": "weak", "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
         "config": {"workload": w.name, "batch": w.batch, "density": w.density, "n_layers": w.shape.n_layers,
                    "d_model": w.shape.d_model, "horizon": w.shape.horizon, "action_dim": w.shape.action_dim,
                    "n_steps": w.shape.n_steps, "parallelism": "none (one GPU)"},
