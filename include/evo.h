@@ -170,7 +170,8 @@ int evo_denoise(evo_policy* p, int32_t batch, const float* obs_cond, const float
  * out, the kernel stops early, its outputs are invalid, and this call
  * returns EVO_E_HIP (the flag is then cleared; until it is, later team
  * launches stop at their first barrier).  Environment variables read by
- * evo_create_policy: EVO_TEAM=0 disables that variant; EVO_TEAM_SPIN_LIMIT
+ * evo_create_policy: EVO_TEAM=0 disables that variant, EVO_TEAM=<n> keeps
+ * only teams of n workgroups (of those compiled); EVO_TEAM_SPIN_LIMIT
  * sets the number of polls before a wait gives up (default 2^20, about a
  * second); EVO_TEAM_TEST_WITHHOLD=1 is a test hook that makes team member 0
  * withhold its partial residuals, so that the other members' waits time out

@@ -77,12 +77,17 @@ struct evo_policy {
   size_t cache_floats = 0;
   float* d_okv = nullptr;
   float* d_rpart = nullptr;  // per-query Eq. 6 terms [max_batch][3L][T]
-  // small-batch team variant: members per tile, largest batch it serves,
-  // partial-residual exchange, barrier counters, device error flag
-  int team = 1, team_batch = 0;
+  // small-batch team variants: workgroups per one-sample tile, the largest
+  // batch each serves and its per-member observation K/V stride, in the
+  // order they are tried (smallest max_batch first); partial-residual
+  // exchange, barrier counters and the device error flag are shared
+  struct TeamCfg {
+    int team = 1, max_batch = 0;
+    size_t okv_stride = 0;
+  };
+  std::vector<TeamCfg> teams;
   unsigned team_spin_limit = 1u << 20;  // EVO_TEAM_SPIN_LIMIT
   int team_withhold = 0;                // EVO_TEAM_TEST_WITHHOLD (test hook)
-  size_t okv_stride = 0;
   float* d_xchg = nullptr;
   unsigned* d_tctr = nullptr;
   unsigned* d_derr = nullptr;
@@ -282,31 +287,52 @@ int evo_create_policy(const evo_policy_desc* desc, const float* host_weights, si
       tiles = std::max(tiles, t);
       spt_max = std::max(spt_max, opts[i]);
     }
-    // team variant (one sample per tile, `team` workgroups per tile) for
-    // batches that fill at most n_cu workgroups; it needs cooperative launch
+    // team variants (one sample per tile, `team` workgroups per tile) for
+    // batches that fill at most n_cu workgroups; they need cooperative
+    // launch.  With teams of 4 and 2 compiled, teams of 4 serve batches up to
+    // n_cu / 16 (latency-bound, the most parallel split wins) and teams of 2
+    // up to n_cu / 2; a single compiled size serves up to n_cu / team.
+    // EVO_TEAM=0 switches teams off, EVO_TEAM=<size> keeps only that size.
     const char* env = std::getenv("EVO_TEAM");
-    const bool team_on = !(env && env[0] == '0');
+    const int team_only = env ? std::atoi(env) : -1;
     if (const char* e = std::getenv("EVO_TEAM_SPIN_LIMIT"))
       p->team_spin_limit = (unsigned)std::min(std::strtoul(e, nullptr, 10), 1ul << 28);
     if (const char* e = std::getenv("EVO_TEAM_TEST_WITHHOLD")) p->team_withhold = e[0] == '1';
-    const int team = kernel_team_size(KernelKey{s.d, s.dh(), s.H, s.dff, s.dtype, 1, 0});
+    int sizes[4];
+    int nsz = kernel_team_sizes(KernelKey{s.d, s.dh(), s.H, s.dff, s.dtype, 1, 0}, sizes);
+    if (team_only >= 0) {
+      int k = 0;
+      for (int i = 0; i < nsz; ++i)
+        if (sizes[i] == team_only) sizes[k++] = sizes[i];
+      nsz = k;
+    }
     int coop = 0;
     (void)hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, p->device);
-    if (team_on && team > 1 && coop && p->n_cu >= team) {
-      p->team = team;
-      p->team_batch = std::min(s.max_batch, p->n_cu / team);
-      rows = std::max(rows, (size_t)p->team_batch * team * s.H);
+    const size_t okv_per = (size_t)L * s.n_obs * 2 * d;
+    size_t okv_floats = (size_t)s.max_batch * okv_per, xchg_rows = 0, ctr_tiles = 0;
+    if (coop) {
+      for (int i = nsz - 1; i >= 0; --i) {  // smallest team (largest batches) last in `teams`
+        const int t = sizes[i];
+        if (p->n_cu < t) continue;
+        const int cap = (nsz > 1 && t == sizes[0]) ? p->n_cu / (t * t) : p->n_cu / t;
+        evo_policy::TeamCfg tc;
+        tc.team = t;
+        tc.max_batch = std::min(s.max_batch, std::max(cap, 1));
+        tc.okv_stride = (size_t)tc.max_batch * okv_per;
+        p->teams.insert(p->teams.begin(), tc);
+        rows = std::max(rows, (size_t)tc.max_batch * t * s.H);
+        okv_floats = std::max(okv_floats, tc.okv_stride * t);
+        xchg_rows = std::max(xchg_rows, (size_t)tc.max_batch * t * s.H);
+        ctr_tiles = std::max(ctr_tiles, (size_t)tc.max_batch);
+      }
     }
     p->cache_floats = (size_t)U * rows * d;
     CREATE_TRY(hipMalloc(&p->d_cache, p->cache_floats * sizeof(float)));
-    const size_t okv_per = (size_t)L * s.n_obs * 2 * d;
-    p->okv_stride = (size_t)p->team_batch * okv_per;
-    CREATE_TRY(hipMalloc(&p->d_okv,
-                         std::max((size_t)s.max_batch * okv_per, p->okv_stride * p->team) * sizeof(float)));
+    CREATE_TRY(hipMalloc(&p->d_okv, okv_floats * sizeof(float)));
     CREATE_TRY(hipMalloc(&p->d_rpart, (size_t)s.max_batch * U * T * sizeof(float)));
-    if (p->team > 1) {
-      CREATE_TRY(hipMalloc(&p->d_xchg, (size_t)p->team_batch * 3 * p->team * s.H * d * sizeof(float)));
-      CREATE_TRY(hipMalloc(&p->d_tctr, (size_t)p->team_batch * 16 * sizeof(unsigned)));
+    if (!p->teams.empty()) {
+      CREATE_TRY(hipMalloc(&p->d_xchg, xchg_rows * 3 * d * sizeof(float)));
+      CREATE_TRY(hipMalloc(&p->d_tctr, ctr_tiles * 16 * sizeof(unsigned)));
       CREATE_TRY(hipMalloc(&p->d_derr, sizeof(unsigned)));
       CREATE_TRY(hipMemset(p->d_derr, 0, sizeof(unsigned)));
     }
@@ -389,13 +415,17 @@ static int denoise_impl(evo_policy* p, int32_t batch, const float* obs_cond, con
   }
   if (!spt) return fail(EVO_E_UNSUPPORTED, "no kernel for this shape");
   // small batches: several workgroups per one-sample tile
-  if (p->team > 1 && batch <= p->team_batch) {
-    KernelKey k{s.d, s.dh(), s.H, s.dff, s.dtype, 1, p->team};
+  const evo_policy::TeamCfg* tc = nullptr;
+  for (const auto& c : p->teams) {
+    if (batch > c.max_batch) continue;
+    KernelKey k{s.d, s.dh(), s.H, s.dff, s.dtype, 1, c.team};
     int th;
     if (kernel_available(k, &th)) {
       spt = 1;
       threads = th;
-      team = p->team;
+      team = c.team;
+      tc = &c;
+      break;
     }
   }
   Plan plan;
@@ -449,11 +479,11 @@ static int denoise_impl(evo_policy* p, int32_t batch, const float* obs_cond, con
   kp.batch = batch;
   kp.team = team;
   if (team > 1) {
-    if ((size_t)plan.n_tiles > (size_t)p->team_batch) return fail(EVO_E_STATE, "team plan exceeds the buffers");
+    if (plan.n_tiles > tc->max_batch) return fail(EVO_E_STATE, "team plan exceeds the buffers");
     kp.xchg = p->d_xchg;
     kp.tctr = p->d_tctr;
     kp.derr = p->d_derr;
-    kp.okv_member_stride = p->okv_stride;
+    kp.okv_member_stride = tc->okv_stride;
     kp.spin_limit = p->team_spin_limit;
     kp.withhold = p->team_withhold;
     HIP_TRY(launch_zero_u32(p->d_tctr, plan.n_tiles * 16, stream));

@@ -26,6 +26,7 @@
 //    tiles; the DDPM update is fused at the end of every step.
 #include "evo_kernels.hpp"
 
+#include <algorithm>
 #include <cmath>
 #include <type_traits>
 
@@ -1407,6 +1408,8 @@ hipError_t launch_ddpm_table(int T, float* table, hipStream_t stream) {
   X(__bf16, 768, 64, 32, 1, 3072, 8, 2, 256, 5, 1)        \
   X(float, 256, 64, 16, 1, 1024, 4, 1, 256, 8, 4)         \
   X(__bf16, 256, 64, 16, 1, 1024, 4, 1, 256, 8, 4)        \
+  X(float, 256, 64, 16, 1, 1024, 8, 2, 256, 8, 2)         \
+  X(__bf16, 256, 64, 16, 1, 1024, 8, 2, 256, 8, 2)        \
   X(__bf16, 768, 64, 32, 1, 3072, 8, 2, 256, 5, 2)
 
 template <class AT> constexpr int dtype_of() { return std::is_same<AT, float>::value ? 0 : 1; }
@@ -1436,15 +1439,16 @@ int kernel_max_obs_tokens_for(const KernelKey& key) {
 
 int kernel_max_action_dim() { return 16; }
 
-int kernel_team_size(const KernelKey& key) {
-  int best = 1;
+int kernel_team_sizes(const KernelKey& key, int out[4]) {
+  int n = 0;
 #define X(AT, D, DH, HZ, SPT, DFF, NW, HG, FC, SMAX, TEAM) \
-  if (TEAM > 1 && key.d == D && key.dh == DH && key.horizon == HZ && key.d_ff == DFF &&      \
-      key.dtype == dtype_of<AT>() && key.spt == SPT)                                         \
-    best = TEAM;
+  if (TEAM > 1 && n < 4 && key.d == D && key.dh == DH && key.horizon == HZ && key.d_ff == DFF &&      \
+      key.dtype == dtype_of<AT>() && key.spt == SPT)                                                   \
+    out[n++] = TEAM;
   EVO_SHAPES(X)
 #undef X
-  return best;
+  std::sort(out, out + n, [](int a, int b) { return a > b; });
+  return n;
 }
 
 int kernel_max_steps_x_spt() { return kMaskEntries; }

@@ -91,7 +91,8 @@ hipError_t launch_ddpm_table(int T, float* table, hipStream_t stream);
 hipError_t launch_zero_u32(unsigned* dst, int n, hipStream_t stream);
 
 // team size of the small-batch variant for a shape (1: none compiled)
-int kernel_team_size(const KernelKey& key);
+// team sizes (> 1) compiled for a shape, largest first; returns their number
+int kernel_team_sizes(const KernelKey& key, int out[4]);
 
 // Eq. 6 dissimilarity scores from recorded activations acts [R][U][T][V]:
 // part [R][U][T] receives each query's term, d [U][T] their mean over R

@@ -39,11 +39,11 @@ def _policy(shape, weights, dtype, max_batch, max_sched, cold=O.COLD_COMPUTE, cl
 
 
 def _case(name, shape, weights, obs, noise, lattices, ids, dtype, gran=O.GRAN_LAYER,
-          cold=O.COLD_COMPUTE, samples=None, max_batch=None, clip=True, team=True):
+          cold=O.COLD_COMPUTE, samples=None, max_batch=None, clip=True, team=True, env=None):
     say(f"[gpu] {name}: dtype={dtype} batch={obs.shape[0]} schedules={len(lattices)} gran={gran} cold={cold} "
-        f"team={team}")
+        f"team={team} env={env}")
     B = obs.shape[0]
-    pol = _policy(shape, weights, dtype, max_batch or B, len(lattices), cold, clip, team)
+    pol = _policy(shape, weights, dtype, max_batch or B, len(lattices), cold, clip, team, env)
     for j, lt in enumerate(lattices):
         pol.set_schedule(j, lt, gran)
     got, gst = run_gpu(pol, obs, noise, ids)
@@ -107,12 +107,15 @@ def test_pusht_b1_single_workgroup(name):
     pol.close()
 
 
+@pytest.mark.parametrize("size", [4, 2])
 @pytest.mark.parametrize("dtype", ["fp32", "bf16"])
-def test_team_variant_matches_single_workgroup(dtype):
-    """Batches of at most n_cu/4 samples run four workgroups per one-sample
-    tile (heads and d_ff chunks split among them, partial residuals summed
-    through memory).  Both variants match the oracle on a ragged batch with
-    mixed unit-granular schedules, and each other to summation order."""
+def test_team_variant_matches_single_workgroup(dtype, size):
+    """Small batches run `size` workgroups per one-sample tile (heads and
+    d_ff chunks split among them, partial residuals summed through memory;
+    teams of 4 up to n_cu/16 samples, teams of 2 up to n_cu/2, each forced
+    here with EVO_TEAM=<size>).  Both variants match the oracle on a ragged
+    batch with mixed unit-granular schedules, and each other to summation
+    order."""
     s = I.PUSHT
     wts = I.make_weights(s, 6, "perturbed")
     B = 7
@@ -120,15 +123,15 @@ def test_team_variant_matches_single_workgroup(dtype):
     rng = np.random.default_rng([6, 3])
     lats = [I.lattice_bernoulli(3 * s.n_layers, s.n_steps, p, rng) for p in (0.1, 0.3, 0.6)]
     ids = np.array([0, 1, 2, 2, 1, 0, 1], np.int32)
-    pol_t, got_t, st_t, _ = _case(f"team_{dtype}", s, wts, obs, noise, lats, ids, dtype, gran=O.GRAN_UNIT,
-                                  samples=[0, 3, 6])
+    pol_t, got_t, st_t, _ = _case(f"team{size}_{dtype}", s, wts, obs, noise, lats, ids, dtype, gran=O.GRAN_UNIT,
+                                  samples=[0, 3, 6], env={"EVO_TEAM": str(size)})
     pol_1, got_1, st_1, _ = _case(f"noteam_{dtype}", s, wts, obs, noise, lats, ids, dtype, gran=O.GRAN_UNIT,
                                   samples=[0, 3, 6], team=False)
     assert st_t["n_tiles"] == st_1["n_tiles"] == B
     assert st_1["n_workgroups"] == B
-    assert st_t["n_workgroups"] in (B, 4 * B)
-    if st_t["n_workgroups"] == 4 * B:
-        assert st_t["cache_bytes_written"] == 4 * st_1["cache_bytes_written"]
+    assert st_t["n_workgroups"] in (B, size * B)
+    if st_t["n_workgroups"] == size * B:
+        assert st_t["cache_bytes_written"] == size * st_1["cache_bytes_written"]
     d = float(np.max(np.abs(got_t - got_1)))
     say(f"  team vs single workgroup: max-abs diff {d:.3e}")
     if dtype == "fp32":
@@ -140,7 +143,8 @@ def test_team_variant_matches_single_workgroup(dtype):
     pol_1.close()
 
 
-def test_team_wait_timeout_is_reported():
+@pytest.mark.parametrize("size", [4, 2])
+def test_team_wait_timeout_is_reported(size):
     """Error path of the team variant, forced from the host: team member 0
     withholds its partial residuals (test hook) and the other members' waits
     give up after 64 polls.  The kernel still finishes; evo_synchronize
@@ -151,8 +155,9 @@ def test_team_wait_timeout_is_reported():
     wts = I.make_weights(s, 7, "perturbed")
     obs, noise = I.make_obs(s, 1, 7), I.make_noise(s, 1, 7)
     lat = I.lattice_bernoulli(3 * s.n_layers, s.n_steps, 0.2, np.random.default_rng(7))
-    say("[gpu] team wait timeout, forced from the host")
-    pol = _policy(s, wts, "bf16", 1, 1, env={"EVO_TEAM_TEST_WITHHOLD": "1", "EVO_TEAM_SPIN_LIMIT": "64"})
+    say(f"[gpu] team of {size}: wait timeout, forced from the host")
+    pol = _policy(s, wts, "bf16", 1, 1, env={"EVO_TEAM_TEST_WITHHOLD": "1", "EVO_TEAM_SPIN_LIMIT": "64",
+                                             "EVO_TEAM": str(size)})
     pol.set_schedule(0, lat, O.GRAN_UNIT)
     dev = device()
     pol.denoise(torch.from_numpy(obs).to(dev), torch.from_numpy(noise).to(dev), None)
@@ -161,6 +166,7 @@ def test_team_wait_timeout_is_reported():
         pol.synchronize()
         pol.close()
         pytest.skip("the team variant is not used on this device")
+    assert st["n_workgroups"] == size * st["n_tiles"]
     with pytest.raises(evo.EvoError) as e:
         pol.synchronize()
     assert e.value.code == -4 and "team barrier" in str(e.value)
@@ -219,17 +225,21 @@ def test_population_b512_sampled():
 def test_determinism_reset_and_independence():
     """Same inputs -> bitwise-same chunk; a call in between does not leak
     (caches are reset per query); a sample's chunk does not depend on the
-    other samples of the batch or on its tile position."""
+    other samples of the batch or on its tile position.  The kernel variant
+    is chosen by batch size (teams of 4 below 17 samples, of 2 above), and
+    variants sum partial residuals in different orders, so the variant is
+    fixed here (EVO_TEAM=2 serves both batch sizes)."""
     w = I.WORKLOADS["pusht_bf16_b64_d25"]
     s = w.shape
     inp = I.make_inputs(w)
     lats = I.population_lattices(s.n_layers, s.n_steps, 4, 0)
     ids = np.arange(64, dtype=np.int32) % 4
     say("[gpu] determinism/reset/independence pusht bf16 b64")
-    pol = _policy(s, inp.weights, "bf16", 64, 4)
+    pol = _policy(s, inp.weights, "bf16", 64, 4, env={"EVO_TEAM": "2"})
     for j, lt in enumerate(lats):
         pol.set_schedule(j, lt, O.GRAN_LAYER)
-    a1, _ = run_gpu(pol, inp.obs, inp.noise, ids)
+    a1, st = run_gpu(pol, inp.obs, inp.noise, ids)
+    assert st["n_workgroups"] in (64, 128)
     obs2, noise2 = I.make_obs(s, 64, 9), I.make_noise(s, 64, 9)
     run_gpu(pol, obs2, noise2, ids[::-1].copy())
     a2, _ = run_gpu(pol, inp.obs, inp.noise, ids)
