@@ -809,7 +809,6 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
           for (int m = 0; m < MPWQ; ++m)
 #pragma unroll
             for (int rb = 0; rb < RB; ++rb) y[m][rb] = f32x4{0.f, 0.f, 0.f, 0.f};
-          if (g != member) gemm_pref<NPQ, MPWQ>(b1q, pk + po.qkv, D / O::KF, 0, gcb_sa(g), lane);
           float bq[MPWQ];  // stage-1 biases, requested before the GEMM so their latency is hidden
 #pragma unroll
           for (int m = 0; m < MPWQ; ++m) bq[m] = raw[lo.b_qkv + gcb_sa(g)(m) * 16 + lc];
@@ -889,6 +888,8 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
             }
             wave_lds_sync();
           }
+          // the next head group's first stage-1 k-steps stream in during this output product
+          if (g + TEAM < NH / HG) gemm_pref<NPQ, MPWQ>(b1q, pk + po.qkv, D / O::KF, 0, gcb_sa(g + TEAM), lane);
           __syncthreads();
           gemm_run<AT, RB, CBW, GW / O::KF, INFL, NP2A>(r, zbuf, LDZ, pk + po.o, D / O::KF, g * (GW / O::KF), own, lane,
                                                        b2);
@@ -924,7 +925,6 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
           for (int m = 0; m < MPWC; ++m)
 #pragma unroll
             for (int rb = 0; rb < RB; ++rb) y[m][rb] = f32x4{0.f, 0.f, 0.f, 0.f};
-          if (g != member) gemm_pref<NPC, MPWC>(b1c, pk + po.q, D / O::KF, 0, gcb_ca(g), lane);
           float bq[MPWC];
 #pragma unroll
           for (int m = 0; m < MPWC; ++m) bq[m] = raw[lo.b_q + gcb_ca(g)(m) * 16 + lc];
@@ -990,6 +990,7 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
 #pragma unroll
             for (int d = 0; d < OD; ++d) O::store(zbuf, LDZ, row, c0 + d, o[d] * inv);
           }
+          if (g + TEAM < NH / HG) gemm_pref<NPC, MPWC>(b1c, pk + po.q, D / O::KF, 0, gcb_ca(g + TEAM), lane);
           __syncthreads();
           gemm_run<AT, RB, CBW, GW / O::KF, INFL, NP2A>(r, zbuf, LDZ, pk + po.o2, D / O::KF, g * (GW / O::KF), own,
                                                        lane, b2);
@@ -1006,7 +1007,6 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
           for (int m = 0; m < MPWF; ++m)
 #pragma unroll
             for (int rb = 0; rb < RB; ++rb) y[m][rb] = f32x4{0.f, 0.f, 0.f, 0.f};
-          if (ch != member) gemm_pref<NPF, MPWF>(b1f, pk + po.w1, D / O::KF, 0, gcb_ff(ch), lane);
           float b1v[MPWF];
 #pragma unroll
           for (int m = 0; m < MPWF; ++m) b1v[m] = raw[lo.b_1 + ch * FC + (w + NW * m) * 16 + lc];
@@ -1022,6 +1022,8 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
               for (int i = 0; i < 4; ++i)
                 O::store(zbuf, LDZ, rb * 16 + lq * 4 + i, loc, gelu_erf(y[m][rb][i] + b1v[m]));
           }
+          // the next chunk's first stage-1 k-steps stream in during this chunk's second product
+          if (ch + TEAM < DFF / FC) gemm_pref<NPF, MPWF>(b1f, pk + po.w1, D / O::KF, 0, gcb_ff(ch + TEAM), lane);
           __syncthreads();
           gemm_run<AT, RB, CBW, FC / O::KF, INFL, NP2F>(r, zbuf, LDZ, pk + po.w2, DFF / O::KF, ch * (FC / O::KF), own,
                                                         lane, b2);
