@@ -232,28 +232,33 @@ int evo_guided_sample(const double* probs, int32_t rows, int32_t n_steps, int32_
  * array is its signature.  Randomness: Philox4x64-10 (Salmon et al., SC
  * 2011), key (seed, 0), counter (generation, purpose << 32 | slot, index, 0),
  * first output word w; uniform (0, 1) = ((w >> 12) + 1/2) 2^-52, integer
- * [0, n) = ((w >> 32) n) >> 32, coin = top bit.  Purposes: 1 initial
- * individual, 2 tournament, 3 crossover, 4 mutation test, 5 mutation target,
- * 6 repair drop, 7 repair fill; slot = individual or child index, index =
- * lattice position or entrant number.
+ * [0, n) = ((w >> 32) n) >> 32.  Purposes: 1 initial individual, 2
+ * tournament, 3 crossover, 4 mutation test, 5 mutation target, 6 repair
+ * drop, 7 repair fill; slot = individual or child index; index = a lattice
+ * position (guided draws), a rank, an entrant or a draw number.
  *
  * Operators (the paper names them without parameters; these are the
  * readings):
  *  - initial population: individuals 0 .. n_guided-1 take K positions from
- *    Eq. 7's probabilities (evo_guided_sample with uniforms of purpose 1),
- *    the others the K positions with the largest purpose-1 words (a uniform
- *    K-subset);
+ *    Eq. 7's probabilities (evo_guided_sample with the purpose-1 uniforms of
+ *    every position), the others are uniform K-subsets built by `fill`
+ *    (below) from the empty set;
+ *  - fill: draw j = 0, 1, ... adds position [0, N) of word j unless present,
+ *    until K (after 64 N draws the missing positions are added in ascending
+ *    order; never reached in practice);
  *  - ranking: fitness descending, ties to the lower population index; the
  *    next population is the n_elite best in that order, then the children;
  *  - tournament: `tournament` entrants drawn with replacement, highest
  *    fitness wins, ties to the lower index; two tournaments per child;
- *  - set-level crossover: positions of both parents kept, each position of
- *    one parent kept on a coin;
- *  - mutation: each position replaced, with probability mutation_rate, by a
- *    position drawn uniformly from the whole lattice;
- *  - repair: duplicates merge; above K keep the K positions with the largest
- *    purpose-6 words; below K add the missing positions (not yet in the
- *    child) with the largest purpose-7 words. */
+ *  - set-level crossover: positions of both parents kept; the r-th position
+ *    (ascending) of those in one parent only is kept on bit r % 64 of word
+ *    r / 64;
+ *  - mutation: the r-th position (ascending) is replaced by a uniform
+ *    lattice position (purpose 5, index r) when the 32-bit half r % 2 of
+ *    word r / 2 is below floor(mutation_rate 2^32);
+ *  - repair: duplicates merge; a surplus loses, one at a time, the element at
+ *    index [0, size) of draw j = 0, 1, ... of the ascending list; a shortfall
+ *    is completed by `fill` (purpose 7). */
 typedef struct {
   int32_t K;                /* refreshes per schedule, 1 <= K <= rows*T (Eq. 5) */
   int32_t pop_size;         /* population size (Sec. 4.1: 30) */

@@ -31,22 +31,23 @@ Readings where the paper is silent (listed in the design notes):
 * Randomness comes from the counter-based generator Philox4x64-10 (Salmon,
   Moraes, Dror, Shaw, "Parallel random numbers: as easy as 1, 2, 3", SC 2011),
   keyed by (seed, 0) with counter (generation, purpose << 32 | slot, index, 0);
-  the first output word is used.  Every draw is addressed by what it decides,
-  so the result does not depend on the order in which draws are taken.
+  the first output word is used.  Every draw is addressed by the decision it
+  makes (an individual or child, and a rank or draw number within it).
 * Uniform in (0, 1): ((w >> 12) + 1/2) * 2^-52 (exact in fp64).  Uniform integer in [0, n):
   ((w >> 32) * n) >> 32.  Bernoulli(1/2): the top bit of w.
-* Random individuals: the K positions with the largest words (ties to the
-  lower index), i.e. a uniform K-subset.
+* Random individuals: uniform K-subsets, by `fill` from the empty set:
+  draw j adds position below(word(j), N) unless present.
 * Tournament: `tournament` entrants drawn with replacement from the
   population; the highest fitness wins, ties to the lower population index.
 * Crossover (always applied): positions in both parents are kept; each
-  position in exactly one parent is kept with probability 1/2.
-* Mutation: each position of the child is, with probability mutation_rate,
-  replaced by a position drawn uniformly from the whole lattice.
-* Repair: duplicates merge (sets); a child with more than K positions keeps
-  the K with the largest words of its DROP draws, one with fewer gains the
-  missing positions with the largest words of its FILL draws among those not
-  yet in it.
+  position in exactly one parent is kept with probability 1/2 (one bit of a
+  word per position, by rank).
+* Mutation: each position of the child is, with probability mutation_rate
+  (a 32-bit half-word against floor(rate * 2^32)), replaced by a position
+  drawn uniformly from the whole lattice.
+* Repair: duplicates merge (sets); a surplus is removed one uniformly chosen
+  element at a time; a shortfall is completed by uniform draws of positions
+  not yet present.
 * Ranking: fitness descending, ties to the lower population index.  The next
   population is the n_elite best in that order followed by the children.
 * max_generations counts evaluated populations, the initial one included.
@@ -114,14 +115,24 @@ class GAConfig:
     seed: int = 0
 
 
-def top_by_word(cands: Sequence[int], n: int, seed: int, gen: int, purpose: int, slot: int) -> List[int]:
-    """The n candidates with the largest words (ties to the lower index)."""
-    keyed = sorted(cands, key=lambda p: (-word(seed, gen, purpose, slot, p), p))
-    return sorted(keyed[:n])
+def fill(seed: int, gen: int, purpose: int, slot: int, s: set, K: int, N: int) -> set:
+    """Uniform completion to K distinct positions: draw j = 0, 1, ... adds
+    below(word(j), N) unless present.  After 64 N draws (never reached in
+    practice) the missing positions are added in ascending order."""
+    out = set(s)
+    j = 0
+    while len(out) < K and j < 64 * N:
+        out.add(below(word(seed, gen, purpose, slot, j), N))
+        j += 1
+    p = 0
+    while len(out) < K:
+        out.add(p)
+        p += 1
+    return out
 
 
 def random_individual(cfg: GAConfig, N: int, i: int) -> Tuple[int, ...]:
-    return tuple(top_by_word(range(N), cfg.K, cfg.seed, 0, INIT, i))
+    return tuple(sorted(fill(cfg.seed, 0, INIT, i, set(), cfg.K, N)))
 
 
 def guided_individual(cfg: GAConfig, probs: np.ndarray, i: int) -> Tuple[int, ...]:
@@ -154,32 +165,41 @@ def tournament(cfg: GAConfig, gen: int, child: int, parent: int, fit: Sequence[f
 
 
 def crossover(cfg: GAConfig, gen: int, child: int, a: Sequence[int], b: Sequence[int]) -> set:
+    """Positions in both parents are kept; the r-th position (ascending) of
+    those in exactly one parent is kept on bit r mod 64 of word(r div 64)."""
     A, B = set(a), set(b)
     out = A & B
-    for p in A ^ B:
-        if word(cfg.seed, gen, CROSS, child, p) >> 63:
+    for r, p in enumerate(sorted(A ^ B)):
+        if (word(cfg.seed, gen, CROSS, child, r // 64) >> (r % 64)) & 1:
             out.add(p)
     return out
 
 
 def mutate(cfg: GAConfig, gen: int, child: int, s: set, N: int) -> set:
+    """The r-th position (ascending) is replaced, when the 32-bit half
+    r mod 2 of word(r div 2) is below floor(mutation_rate * 2^32), by
+    below(word'(r), N) (purpose MUTPOS)."""
+    thr = int(cfg.mutation_rate * 2.0 ** 32)
     out = set()
-    for q in s:
-        if unit_interval(word(cfg.seed, gen, MUT, child, q)) < cfg.mutation_rate:
-            out.add(below(word(cfg.seed, gen, MUTPOS, child, q), N))
-        else:
-            out.add(q)
+    for r, q in enumerate(sorted(s)):
+        h = (word(cfg.seed, gen, MUT, child, r // 2) >> (32 * (r % 2))) & 0xFFFFFFFF
+        out.add(below(word(cfg.seed, gen, MUTPOS, child, r), N) if h < thr else q)
     return out
 
 
 def repair(cfg: GAConfig, gen: int, child: int, s: set, N: int) -> Tuple[int, ...]:
+    """Back to exactly K: a surplus loses, one at a time, the element at
+    index below(word(j), size) of the ascending list (purpose DROP, draw
+    j = 0, 1, ...); a shortfall is completed by `fill` (purpose FILL)."""
     K = cfg.K
-    if len(s) > K:
-        return tuple(top_by_word(sorted(s), K, cfg.seed, gen, DROP, child))
-    if len(s) < K:
-        missing = [p for p in range(N) if p not in s]
-        return tuple(sorted(s | set(top_by_word(missing, K - len(s), cfg.seed, gen, FILL, child))))
-    return tuple(sorted(s))
+    ss = sorted(s)
+    j = 0
+    while len(ss) > K:
+        del ss[below(word(cfg.seed, gen, DROP, child, j), len(ss))]
+        j += 1
+    if len(ss) < K:
+        ss = sorted(fill(cfg.seed, gen, FILL, child, set(ss), K, N))
+    return tuple(ss)
 
 
 def make_child(cfg: GAConfig, gen: int, child: int, pop: Sequence[Sequence[int]], fit: Sequence[float],

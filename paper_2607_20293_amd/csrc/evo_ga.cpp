@@ -54,18 +54,28 @@ inline double unit_interval(uint64_t w) { return ((double)(w >> 12) + 0.5) * 0x1
 // [0, n): high 32 bits scaled by n
 inline int32_t below(uint64_t w, uint32_t n) { return (int32_t)(((w >> 32) * (uint64_t)n) >> 32); }
 
-// the n candidates with the largest words (ties to the lower position), sorted
-std::vector<int32_t> top_by_word(const std::vector<int32_t>& cands, int n, const Draw& d, uint64_t purpose,
-                                 uint64_t slot) {
-  std::vector<std::pair<uint64_t, int32_t>> key(cands.size());
-  for (size_t i = 0; i < cands.size(); ++i) key[i] = {d.word(purpose, slot, (uint64_t)cands[i]), cands[i]};
-  std::partial_sort(key.begin(), key.begin() + n, key.end(), [](const auto& a, const auto& b) {
-    return a.first != b.first ? a.first > b.first : a.second < b.second;
-  });
-  std::vector<int32_t> out(n);
-  for (int i = 0; i < n; ++i) out[i] = key[i].second;
-  std::sort(out.begin(), out.end());
-  return out;
+// Completes the sorted set s to K distinct positions of [0, N): draw j adds
+// below(word(purpose, slot, j), N) unless present; after 64 N draws (never
+// reached in practice) the missing positions are added in ascending order.
+// mark: N zero bytes, returned zeroed.
+void fill(std::vector<int32_t>& s, int K, int N, const Draw& d, uint64_t purpose, uint64_t slot,
+          std::vector<uint8_t>& mark) {
+  for (int32_t q : s) mark[q] = 1;
+  const size_t start = s.size();
+  for (uint64_t j = 0; (int)s.size() < K && j < 64ull * (uint64_t)N; ++j) {
+    const int32_t p = below(d.word(purpose, slot, j), (uint32_t)N);
+    if (!mark[p]) {
+      mark[p] = 1;
+      s.push_back(p);
+    }
+  }
+  for (int32_t p = 0; (int)s.size() < K; ++p)
+    if (!mark[p]) {
+      mark[p] = 1;
+      s.push_back(p);
+    }
+  for (int32_t q : s) mark[q] = 0;
+  if (s.size() != start) std::sort(s.begin(), s.end());
 }
 
 std::vector<int32_t> ranking(const double* fit, int P) {
@@ -88,16 +98,24 @@ int32_t tournament(const evo_ga_config& c, const Draw& d, int child, int parent,
 void make_child(const evo_ga_config& c, const Draw& d, int child, const int32_t* A, const int32_t* B, int N,
                 std::vector<uint8_t>& mark, int32_t* out) {
   const int K = c.K;
-  // set-level crossover: A & B kept, each of A ^ B kept with probability 1/2
+  const uint64_t ch = (uint64_t)child;
+  // set-level crossover: A & B kept; the r-th position of A ^ B (ascending)
+  // kept on bit r % 64 of word(r / 64)
   std::vector<int32_t> s;
   s.reserve(2 * K);
+  uint64_t coins = 0;
+  int r = 0;
+  const auto coin = [&]() {
+    if (r % 64 == 0) coins = d.word(kCross, ch, (uint64_t)(r / 64));
+    return (coins >> (r++ % 64)) & 1ull;
+  };
   int i = 0, j = 0;
   while (i < K || j < K) {
     if (j >= K || (i < K && A[i] < B[j])) {
-      if (d.word(kCross, (uint64_t)child, (uint64_t)A[i]) >> 63) s.push_back(A[i]);
+      if (coin()) s.push_back(A[i]);
       ++i;
     } else if (i >= K || B[j] < A[i]) {
-      if (d.word(kCross, (uint64_t)child, (uint64_t)B[j]) >> 63) s.push_back(B[j]);
+      if (coin()) s.push_back(B[j]);
       ++j;
     } else {
       s.push_back(A[i]);
@@ -105,26 +123,27 @@ void make_child(const evo_ga_config& c, const Draw& d, int child, const int32_t*
       ++j;
     }
   }
-  // mutation: each position resampled from the whole lattice with probability mutation_rate
-  for (int32_t& q : s)
-    if (unit_interval(d.word(kMut, (uint64_t)child, (uint64_t)q)) < c.mutation_rate)
-      q = below(d.word(kMutPos, (uint64_t)child, (uint64_t)q), (uint32_t)N);
-  std::sort(s.begin(), s.end());
-  s.erase(std::unique(s.begin(), s.end()), s.end());
-  // repair to exactly K
-  if ((int)s.size() > K) {
-    s = top_by_word(s, K, d, kDrop, (uint64_t)child);
-  } else if ((int)s.size() < K) {
-    for (int32_t q : s) mark[q] = 1;
-    std::vector<int32_t> missing;
-    missing.reserve(N - s.size());
-    for (int p = 0; p < N; ++p)
-      if (!mark[p]) missing.push_back(p);
-    for (int32_t q : s) mark[q] = 0;
-    const std::vector<int32_t> add = top_by_word(missing, K - (int)s.size(), d, kFill, (uint64_t)child);
-    s.insert(s.end(), add.begin(), add.end());
-    std::sort(s.begin(), s.end());
+  // mutation: the r-th position replaced when the 32-bit half r % 2 of
+  // word(r / 2) is below floor(rate 2^32)
+  const uint64_t thr = (uint64_t)(c.mutation_rate * 4294967296.0);
+  uint64_t mw = 0;
+  bool moved = false;
+  for (size_t q = 0; q < s.size(); ++q) {
+    if (q % 2 == 0) mw = d.word(kMut, ch, (uint64_t)(q / 2));
+    if (((mw >> (32 * (q % 2))) & 0xFFFFFFFFull) < thr) {
+      s[q] = below(d.word(kMutPos, ch, (uint64_t)q), (uint32_t)N);
+      moved = true;
+    }
   }
+  if (moved) {
+    std::sort(s.begin(), s.end());
+    s.erase(std::unique(s.begin(), s.end()), s.end());
+  }
+  // repair to exactly K: remove uniformly chosen elements one at a time, or
+  // complete with uniform new positions
+  for (uint64_t k = 0; (int)s.size() > K; ++k)
+    s.erase(s.begin() + below(d.word(kDrop, ch, k), (uint32_t)s.size()));
+  if ((int)s.size() < K) fill(s, K, N, d, kFill, ch, mark);
   std::memcpy(out, s.data(), sizeof(int32_t) * K);
 }
 
@@ -160,8 +179,8 @@ int ga_check(const evo_ga_config* c, int rows, int T, const double* probs, bool 
 int ga_initial(const evo_ga_config& c, int rows, int T, const double* probs, int32_t* pop) {
   const int N = rows * T, K = c.K;
   const Draw d{c.seed, 0};
-  std::vector<int32_t> all(N);
-  for (int p = 0; p < N; ++p) all[p] = p;
+  std::vector<uint8_t> mark(N, 0);
+  std::vector<int32_t> sub;
   std::vector<double> u;
   std::vector<int32_t> pairs;
   for (int i = 0; i < c.pop_size; ++i) {
@@ -174,8 +193,9 @@ int ga_initial(const evo_ga_config& c, int rows, int T, const double* probs, int
       if (rc) return rc;
       for (int k = 0; k < K; ++k) ind[k] = pairs[2 * k] * T + pairs[2 * k + 1];
     } else {
-      const std::vector<int32_t> s = top_by_word(all, K, d, kInit, (uint64_t)i);
-      std::memcpy(ind, s.data(), sizeof(int32_t) * K);
+      sub.clear();
+      fill(sub, K, N, d, kInit, (uint64_t)i, mark);
+      std::memcpy(ind, sub.data(), sizeof(int32_t) * K);
     }
   }
   return EVO_OK;

@@ -59,7 +59,7 @@ def _tiny_case():
     return s, w, (obs_q, noise_q, obs_f, noise_f), probs
 
 
-TINY_TAU = 0.09
+TINY_TAU = 0.11
 
 
 def _gpu_deviations(pol, evals, episodes, rows, T, per_call):
