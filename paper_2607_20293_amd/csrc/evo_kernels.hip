@@ -351,7 +351,7 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
   // layer-merged residual sum accumulated in registers, else in its cache slot
   constexpr bool MAC_REG = CBW * RB <= 4;
   // weight fragments in flight per wave in the unit products
-  constexpr int INFL = (TEAM > 1 && RB == 1) ? 16 : (RB == 1 && CBW <= 2 ? 12 : 6);
+  constexpr int INFL = (TEAM > 1 && RB == 1) ? 16 : (RB == 1 && CBW <= 2 ? 10 : 6);
   constexpr float kScale = (DH == 64) ? 0.125f : (DH == 32 ? 0.17677669529663688f : 0.0f);
   static_assert(DH == 64 || DH == 32, "head dim");
 
