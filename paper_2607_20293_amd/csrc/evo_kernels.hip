@@ -351,7 +351,7 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
   // layer-merged residual sum accumulated in registers, else in its cache slot
   constexpr bool MAC_REG = CBW * RB <= 4;
   // weight fragments in flight per wave in the unit products
-  constexpr int INFL = (TEAM > 1 && RB == 1) ? 16 : (RB == 1 && CBW <= 2 ? 10 : 6);
+  constexpr int INFL = (TEAM > 1 && RB == 1) ? 16 : (RB == 1 && CBW <= 2 ? 12 : 6);
   constexpr float kScale = (DH == 64) ? 0.125f : (DH == 32 ? 0.17677669529663688f : 0.0f);
   static_assert(DH == 64 || DH == 32, "head dim");
 
@@ -1405,7 +1405,7 @@ hipError_t launch_ddpm_table(int T, float* table, hipStream_t stream) {
   X(__bf16, 64, 32, 8, 2, 256, 4, 2, 256, 8, 1)           \
   X(float, 256, 64, 16, 1, 1024, 8, 4, 256, 8, 1)         \
   X(float, 256, 64, 16, 2, 1024, 8, 2, 128, 8, 1)         \
-  X(__bf16, 256, 64, 16, 1, 1024, 8, 4, 512, 8, 1)        \
+  X(__bf16, 256, 64, 16, 1, 1024, 8, 4, 256, 8, 1)        \
   X(__bf16, 256, 64, 16, 2, 1024, 8, 2, 256, 8, 1)        \
   X(__bf16, 768, 64, 32, 1, 3072, 8, 2, 256, 5, 1)        \
   X(float, 256, 64, 16, 1, 1024, 4, 1, 256, 8, 4)         \
