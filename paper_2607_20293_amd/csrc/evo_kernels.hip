@@ -268,10 +268,13 @@ struct Cfg {
 
 // LayerNorm statistics of the tile rows from the register-resident stream:
 // per-lane (mean, M2) over its columns, merged across the 16 lanes of a row
-// group with shuffles and across waves through LDS (one barrier).
+// group with shuffles; the waves' partials of row r are merged by thread r
+// alone (one dependent chain per row instead of every lane merging all of
+// its rows) and broadcast through LDS (two barriers).
 template <class C>
 __device__ __forceinline__ void ln_stats(const f32x4 (&h)[C::CBW][C::RB], float (*red)[C::R][2],
-                                         float (&mu)[C::RB][4], float (&rs)[C::RB][4], int w, int lc, int lq) {
+                                         float (*fin)[2], float (&mu)[C::RB][4], float (&rs)[C::RB][4], int w,
+                                         int lc, int lq, int tid) {
   constexpr int D = C::CB * 16;
   constexpr float nw = 16.0f * C::CBW;
 #pragma unroll
@@ -307,22 +310,28 @@ __device__ __forceinline__ void ln_stats(const f32x4 (&h)[C::CBW][C::RB], float 
       }
     }
   __syncthreads();
+  if (tid < C::R) {
+    const int row = tid;
+    float M = red[0][row][0], Q = red[0][row][1], n = nw;
+#pragma unroll
+    for (int ww = 1; ww < C::NWV; ++ww) {
+      const float mb = red[ww][row][0], qb = red[ww][row][1];
+      const float d = mb - M, tot = n + nw;
+      M += d * (nw / tot);
+      Q += qb + d * d * (n * nw / tot);
+      n = tot;
+    }
+    fin[row][0] = M;
+    fin[row][1] = fast_rsqrt(Q * (1.0f / D) + 1e-5f);
+  }
+  __syncthreads();
 #pragma unroll
   for (int rb = 0; rb < C::RB; ++rb)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int row = rb * 16 + lq * 4 + i;
-      float M = red[0][row][0], Q = red[0][row][1], n = nw;
-#pragma unroll
-      for (int ww = 1; ww < C::NWV; ++ww) {
-        const float mb = red[ww][row][0], qb = red[ww][row][1];
-        const float d = mb - M, tot = n + nw;
-        M += d * (nw / tot);
-        Q += qb + d * d * (n * nw / tot);
-        n = tot;
-      }
-      mu[rb][i] = M;
-      rs[rb][i] = fast_rsqrt(Q * (1.0f / D) + 1e-5f);
+      mu[rb][i] = fin[row][0];
+      rs[rb][i] = fin[row][1];
     }
 }
 
@@ -361,6 +370,7 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
   __shared__ __attribute__((aligned(16))) float pw[NW * PWN];
   __shared__ __attribute__((aligned(16))) float kvbuf[SPT * SMAX * 2 * GW];
   __shared__ float red[NW][R][2];
+  __shared__ float fin[R][2];
   __shared__ __attribute__((aligned(16))) float xs[R * 16];
   __shared__ uint64_t msk[kMaskEntries * 3];
   __shared__ LayerOff s_loff[kMaxLayers];
@@ -784,7 +794,7 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
       // LayerNorm of the unit's input into the stage-1 operand buffer
       const auto layer_norm_to_xa = [&]() {
         float mu[RB][4], rs[RB][4];
-        ln_stats<C>(h, red, mu, rs, w, lc, lq);
+        ln_stats<C>(h, red, fin, mu, rs, w, lc, lq, tid);
 #pragma unroll
         for (int c = 0; c < CBW; ++c) {
           const int col = (w * CBW + c) * 16 + lc;
@@ -1196,7 +1206,7 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
     // ---- head (final LayerNorm + linear on fp32 MFMA) and DDPM update
     {
       float mu[RB][4], rs[RB][4];
-      ln_stats<C>(h, red, mu, rs, w, lc, lq);
+      ln_stats<C>(h, red, fin, mu, rs, w, lc, lq, tid);
       f32x4 eacc[RB];
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb) eacc[rb] = f32x4{0.f, 0.f, 0.f, 0.f};
