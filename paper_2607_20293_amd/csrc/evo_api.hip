@@ -33,6 +33,9 @@ int spt_options(int horizon, int out[2]) {
 }
 
 int check_supported(const Shape& s) {
+  // the kernels index one workgroup's observation keys/values with 32-bit offsets
+  if ((long long)s.max_batch * s.L * s.n_obs * 2 * s.d >= (1ll << 31))
+    return fail(EVO_E_UNSUPPORTED, "max_batch x n_layers x n_obs_tokens x 2 d_model must stay below 2^31");
   int opts[2];
   const int n = spt_options(s.H, opts);
   bool any = false;

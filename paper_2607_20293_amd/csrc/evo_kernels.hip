@@ -911,18 +911,23 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
         // memory keys/values of a head group: time token + observation tokens
         constexpr int KVN = SPT * SMAX * 2 * GW, KVQ = (KVN + NT - 1) / NT;
         float kvv[KVQ];
+        // branch-free: every lane loads (entries outside the memory tokens
+        // read the time-token row and are zeroed), so the loads issue back
+        // to back instead of one guarded branch each
         const auto load_kv = [&](int g) {
+          const float* trow = p.tkv + ((size_t)k * L + l) * (2 * D);
 #pragma unroll
           for (int q = 0; q < KVQ; ++q) {
             const int it = tid + q * NT;
-            kvv[q] = 0.f;
-            if (it < KVN) {
-              const int col = it % (2 * GW), sm_ = (it / (2 * GW)) % SMAX, j = it / (2 * GW * SMAX);
-              const int gcol = col < GW ? g * GW + col : D + g * GW + (col - GW);
-              if (sm_ < S && smp[j] >= 0)
-                kvv[q] = sm_ == 0 ? p.tkv[((size_t)k * L + l) * (2 * D) + gcol]
-                                  : okv[(((size_t)smp[j] * L + l) * nobs + (sm_ - 1)) * (2 * D) + gcol];
-            }
+            const int col = it % (2 * GW), sm_ = (it / (2 * GW)) % SMAX, j = it / (2 * GW * SMAX);
+            const int gcol = col < GW ? g * GW + col : D + g * GW + (col - GW);
+            const int s_ = smp[j < SPT ? j : 0];
+            const bool ok = it < KVN && sm_ < S && s_ >= 0;
+            const bool obs_tok = ok && sm_ > 0;
+            // 32-bit offsets: the observation K/V of a member is below 2^31 floats
+            const int off = obs_tok ? ((s_ * L + l) * nobs + (sm_ - 1)) * (2 * D) + gcol : gcol;
+            const float v = (obs_tok ? okv : trow)[off];
+            kvv[q] = ok ? v : 0.f;
           }
         };
         load_kv(member);
