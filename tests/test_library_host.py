@@ -56,6 +56,10 @@ def test_descriptor_validation():
     # the 768-wide shape is compiled for bf16 only
     assert evo.check_desc(evo.make_desc(I.BIMANUAL, "bf16", 4, 2)) == 0
     assert evo.check_desc(evo.make_desc(I.BIMANUAL, "fp32", 4, 2)) == -5
+    # observation keys/values of one workgroup are indexed with 32-bit offsets
+    big = evo.make_desc(I.BIMANUAL, "bf16", 200000, 2)      # 200000 x 12 x 4 x 1536 >= 2^31
+    assert evo.check_desc(big) == -5 and "2^31" in evo.lib().evo_last_error().decode()
+    assert evo.check_desc(evo.make_desc(I.BIMANUAL, "bf16", 10000, 2)) == 0
 
 
 @pytest.mark.parametrize("gran", [O.GRAN_LAYER, O.GRAN_UNIT])
