@@ -62,7 +62,7 @@ def _tiny_case():
 TINY_TAU = 0.11
 
 
-def _gpu_deviations(pol, evals, episodes, rows, T, per_call):
+def _gpu_deviations(pol, evals, episodes, rows, T, per_call, gran=evo.GRAN_UNIT):
     """Deviations of every schedule the oracle evaluated, recomputed from
     evo_denoise chunks (fp32 differences, as the search's device reduction)."""
     out = []
@@ -72,12 +72,12 @@ def _gpu_deviations(pol, evals, episodes, rows, T, per_call):
             continue
         obs, noise = episodes[kind]
         n = obs.shape[0]
-        pol.set_schedule(0, np.ones((rows, T), np.uint8), evo.GRAN_UNIT)
+        pol.set_schedule(0, np.ones((rows, T), np.uint8), gran)
         full = pol.denoise(obs, noise, np.zeros(n, np.int32)).cpu().numpy()
         for c0 in range(0, len(items), per_call):
             chunk = items[c0:c0 + per_call]
             for j, (sch, _, _) in enumerate(chunk):
-                pol.set_schedule_pairs(j, np.stack([np.array(sch) // T, np.array(sch) % T], 1), evo.GRAN_UNIT)
+                pol.set_schedule_pairs(j, np.stack([np.array(sch) // T, np.array(sch) % T], 1), gran)
             ob = obs.repeat(len(chunk), 1, 1)
             nz = noise.repeat(1, len(chunk), 1, 1).contiguous()
             ids = np.repeat(np.arange(len(chunk), dtype=np.int32), n)
@@ -130,6 +130,33 @@ def test_tiny_search_matches_oracle(early):
     finally:
         pol.close()
     _check(got, want, evals, pairs, TINY_TAU)
+
+
+def test_tiny_search_layer_granular_matches_oracle():
+    """The search over the layer lattice (2 x 10 positions, K = 8), with
+    formal evaluations that never pass Eq. 9 (so every generation runs)."""
+    import torch
+    s, w, (obs_q, noise_q, obs_f, noise_f), _ = _tiny_case()
+    rows, T = s.n_layers, s.n_steps
+    probs = R.guided_probabilities(np.random.default_rng(84).random((rows, T)), 0.05, 2.0)
+    kw = dict(pop_size=20, n_elite=6, max_generations=5, n_guided=8, mutation_rate=0.1, seed=6)
+    tau, delta = 0.07, 0.125
+    say(f"[gpu] tiny search fp32, layer granularity, tau={tau}")
+    want, evals = oracle_search(s, w, S.GAConfig(K=8, **kw), probs, tau, obs_q, noise_q, obs_f, noise_f,
+                                delta_acc=delta, gran=O.GRAN_LAYER)
+    assert want.formal_evaluations > 0 and not want.accepted
+    dev = device()
+    pol = evo.Policy(s, w, dtype="fp32", max_batch=20 * 8, max_schedules=20)
+    try:
+        t = lambda a: torch.from_numpy(np.ascontiguousarray(a, np.float32)).to(dev)
+        got = pol.search(evo.GAConfig.make(8, **kw), t(obs_q), t(noise_q), t(obs_f), t(noise_f), probs=probs,
+                         granularity=evo.GRAN_LAYER, tau=tau, q_base=1.0, delta_acc=delta)
+        say(f"  gpu: {({k: v for k, v in got.items() if k not in ('populations', 'fitness', 'best')})}")
+        pairs = _gpu_deviations(pol, evals, {"quick": (t(obs_q), t(noise_q)), "formal": (t(obs_f), t(noise_f))},
+                                rows, T, 10, evo.GRAN_LAYER)
+    finally:
+        pol.close()
+    _check(got, want, evals, pairs, tau)
 
 
 def test_pusht_bf16_search_properties_and_sampled_parity():
