@@ -182,327 +182,346 @@ int evo_create_policy(const evo_policy_desc* desc, const float* host_weights, si
   hipDeviceProp_t prop;
   if (hipGetDeviceProperties(&prop, p->device) == hipSuccess) p->n_cu = prop.multiProcessorCount;
 
+  // the rest releases the policy itself on a failed HIP call; an exception
+  // (a host allocation) is caught below and releases it too
+  const auto body = [&]() -> int {
 #define CREATE_TRY(expr)                                                                        \
-  do {                                                                                          \
-    hipError_t e_ = (expr);                                                                     \
-    if (e_ != hipSuccess) {                                                                     \
-      int code_ = (e_ == hipErrorOutOfMemory) ? EVO_E_NOMEM : EVO_E_HIP;                        \
-      fail(code_, "%s failed: %s", #expr, hipGetErrorString(e_));                               \
-      release(p);                                                                               \
-      return code_;                                                                             \
-    }                                                                                           \
-  } while (0)
+    do {                                                                                        \
+      hipError_t e_ = (expr);                                                                   \
+      if (e_ != hipSuccess) {                                                                   \
+        int code_ = (e_ == hipErrorOutOfMemory) ? EVO_E_NOMEM : EVO_E_HIP;                      \
+        fail(code_, "%s failed: %s", #expr, hipGetErrorString(e_));                             \
+        release(p);                                                                             \
+        return code_;                                                                           \
+      }                                                                                         \
+    } while (0)
 
-  const int L = s.L, d = s.d, T = s.T, U = s.U();
-  const int KF = s.dtype == EVO_BF16 ? 32 : 16;
-  // fp32 parameter copy (biases, norms, embeddings, head, and the source of the packed matrices)
-  CREATE_TRY(hipMalloc(&p->d_raw, wo.total * sizeof(float)));
-  CREATE_TRY(hipMemcpy(p->d_raw, host_weights, wo.total * sizeof(float), hipMemcpyHostToDevice));
+    const int L = s.L, d = s.d, T = s.T, U = s.U();
+    const int KF = s.dtype == EVO_BF16 ? 32 : 16;
+    // fp32 parameter copy (biases, norms, embeddings, head, and the source of the packed matrices)
+    CREATE_TRY(hipMalloc(&p->d_raw, wo.total * sizeof(float)));
+    CREATE_TRY(hipMemcpy(p->d_raw, host_weights, wo.total * sizeof(float), hipMemcpyHostToDevice));
 
-  // packed projection matrices
-  auto frag16 = [&](int N, int Kpad) { return (uint64_t)(N / 16) * (Kpad / KF) * 64; };
-  p->obs_pad = (s.obs_dim + 63) / 64 * 64;
-  uint64_t off = 0;
-  p->pk_obs = off;
-  off += frag16(d, p->obs_pad);
-  // embedding and head matrices stay fp32 (16 k per fragment)
-  p->pk_win = off;
-  off += (uint64_t)(d / 16) * 1 * 64;
-  p->pk_wout = off;
-  off += (uint64_t)1 * (d / 16) * 64;
-  p->poff_h.resize(L);
-  for (int l = 0; l < L; ++l) {
-    PackOff& po = p->poff_h[l];
-    po.qkv = off; off += frag16(3 * d, d);
-    po.o = off; off += frag16(d, d);
-    po.q = off; off += frag16(d, d);
-    po.kv = off; off += frag16(2 * d, d);
-    po.o2 = off; off += frag16(d, d);
-    po.w1 = off; off += frag16(s.dff, d);
-    po.w2 = off; off += frag16(d, s.dff);
-    po.pad_ = 0;
-  }
-  CREATE_TRY(hipMalloc(&p->d_pk, off * sizeof(uint4)));
-  CREATE_TRY(launch_pack(p->d_raw, wo.W_obs, d, d, s.obs_dim, p->obs_pad, s.dtype, p->d_pk + p->pk_obs, 0));
-  CREATE_TRY(launch_pack(p->d_raw, wo.W_in, d, d, s.A, 16, EVO_FP32, p->d_pk + p->pk_win, 0));
-  CREATE_TRY(launch_pack(p->d_raw, wo.W_out, 16, s.A, d, d, EVO_FP32, p->d_pk + p->pk_wout, 0));
-  for (int l = 0; l < L; ++l) {
-    const auto& y = wo.layer[l];
-    const PackOff& po = p->poff_h[l];
-    CREATE_TRY(launch_pack(p->d_raw, y.W_qkv, 3 * d, 3 * d, d, d, s.dtype, p->d_pk + po.qkv, 0));
-    CREATE_TRY(launch_pack(p->d_raw, y.W_o, d, d, d, d, s.dtype, p->d_pk + po.o, 0));
-    CREATE_TRY(launch_pack(p->d_raw, y.W_q, d, d, d, d, s.dtype, p->d_pk + po.q, 0));
-    CREATE_TRY(launch_pack(p->d_raw, y.W_kv, 2 * d, 2 * d, d, d, s.dtype, p->d_pk + po.kv, 0));
-    CREATE_TRY(launch_pack(p->d_raw, y.W_o2, d, d, d, d, s.dtype, p->d_pk + po.o2, 0));
-    CREATE_TRY(launch_pack(p->d_raw, y.W_1, s.dff, s.dff, d, d, s.dtype, p->d_pk + po.w1, 0));
-    CREATE_TRY(launch_pack(p->d_raw, y.W_2, d, d, s.dff, s.dff, s.dtype, p->d_pk + po.w2, 0));
-  }
-  // per-layer offsets of the small tensors
-  p->loff_h.resize(L);
-  std::vector<uint32_t> wkv(L), bkv(L);
-  for (int l = 0; l < L; ++l) {
-    const auto& y = wo.layer[l];
-    LayerOff& lo = p->loff_h[l];
-    lo.ln1_g = (uint32_t)y.ln1_g; lo.ln1_b = (uint32_t)y.ln1_b; lo.b_qkv = (uint32_t)y.b_qkv;
-    lo.b_o = (uint32_t)y.b_o; lo.ln2_g = (uint32_t)y.ln2_g; lo.ln2_b = (uint32_t)y.ln2_b;
-    lo.b_q = (uint32_t)y.b_q; lo.b_kv = (uint32_t)y.b_kv; lo.b_o2 = (uint32_t)y.b_o2;
-    lo.ln3_g = (uint32_t)y.ln3_g; lo.ln3_b = (uint32_t)y.ln3_b; lo.b_1 = (uint32_t)y.b_1;
-    lo.b_2 = (uint32_t)y.b_2;
-    lo.pad_[0] = lo.pad_[1] = lo.pad_[2] = 0;
-    wkv[l] = (uint32_t)y.W_kv;
-    bkv[l] = (uint32_t)y.b_kv;
-  }
-  CREATE_TRY(hipMalloc(&p->d_loff, L * sizeof(LayerOff)));
-  CREATE_TRY(hipMemcpy(p->d_loff, p->loff_h.data(), L * sizeof(LayerOff), hipMemcpyHostToDevice));
-  CREATE_TRY(hipMalloc(&p->d_poff, L * sizeof(PackOff)));
-  CREATE_TRY(hipMemcpy(p->d_poff, p->poff_h.data(), L * sizeof(PackOff), hipMemcpyHostToDevice));
-
-  // time-token keys/values for every timestep and layer; sampler constants
-  {
-    uint32_t *d_wkv = nullptr, *d_bkv = nullptr;
-    float* rows = nullptr;
-    CREATE_TRY(hipMalloc(&p->d_tkv, (size_t)T * L * 2 * d * sizeof(float)));
-    CREATE_TRY(hipMalloc(&d_wkv, L * sizeof(uint32_t)));
-    hipError_t e = hipMalloc(&d_bkv, L * sizeof(uint32_t));
-    if (e == hipSuccess) e = hipMalloc(&rows, (size_t)T * d * sizeof(float));
-    if (e == hipSuccess) e = hipMemcpy(d_wkv, wkv.data(), L * sizeof(uint32_t), hipMemcpyHostToDevice);
-    if (e == hipSuccess) e = hipMemcpy(d_bkv, bkv.data(), L * sizeof(uint32_t), hipMemcpyHostToDevice);
-    if (e == hipSuccess)
-      e = launch_time_kv(p->d_raw, (uint32_t)wo.P_mem, d_wkv, d_bkv, T, L, d, s.dtype, rows, p->d_tkv, 0);
-    if (e == hipSuccess) e = hipDeviceSynchronize();
-    (void)hipFree(d_wkv);
-    (void)hipFree(d_bkv);
-    (void)hipFree(rows);
-    CREATE_TRY(e);
-  }
-  CREATE_TRY(hipMalloc(&p->d_ddpm, (size_t)T * 8 * sizeof(float)));
-  CREATE_TRY(launch_ddpm_table(T, p->d_ddpm, 0));
-
-  // caches, observation keys/values, per-call plan buffers
-  {
-    int opts[2];
-    const int n = spt_options(s.H, opts);
-    size_t rows = 0, tiles = 0;
-    int spt_max = 1;
-    for (int i = 0; i < n; ++i) {
-      const size_t t = (size_t)(s.max_batch + opts[i] - 1) / opts[i];
-      rows = std::max(rows, t * opts[i] * s.H);
-      tiles = std::max(tiles, t);
-      spt_max = std::max(spt_max, opts[i]);
+    // packed projection matrices
+    auto frag16 = [&](int N, int Kpad) { return (uint64_t)(N / 16) * (Kpad / KF) * 64; };
+    p->obs_pad = (s.obs_dim + 63) / 64 * 64;
+    uint64_t off = 0;
+    p->pk_obs = off;
+    off += frag16(d, p->obs_pad);
+    // embedding and head matrices stay fp32 (16 k per fragment)
+    p->pk_win = off;
+    off += (uint64_t)(d / 16) * 1 * 64;
+    p->pk_wout = off;
+    off += (uint64_t)1 * (d / 16) * 64;
+    p->poff_h.resize(L);
+    for (int l = 0; l < L; ++l) {
+      PackOff& po = p->poff_h[l];
+      po.qkv = off; off += frag16(3 * d, d);
+      po.o = off; off += frag16(d, d);
+      po.q = off; off += frag16(d, d);
+      po.kv = off; off += frag16(2 * d, d);
+      po.o2 = off; off += frag16(d, d);
+      po.w1 = off; off += frag16(s.dff, d);
+      po.w2 = off; off += frag16(d, s.dff);
+      po.pad_ = 0;
     }
-    // team variants (one sample per tile, `team` workgroups per tile) for
-    // batches that fill at most n_cu workgroups; they need cooperative
-    // launch.  With teams of 4 and 2 compiled, teams of 4 serve batches up to
-    // n_cu / 16 (latency-bound, the most parallel split wins) and teams of 2
-    // up to n_cu / 2; a single compiled size serves up to n_cu / team.
-    // EVO_TEAM=0 switches teams off, EVO_TEAM=<size> keeps only that size.
-    const char* env = std::getenv("EVO_TEAM");
-    const int team_only = env ? std::atoi(env) : -1;
-    if (const char* e = std::getenv("EVO_TEAM_SPIN_LIMIT"))
-      p->team_spin_limit = (unsigned)std::min(std::strtoul(e, nullptr, 10), 1ul << 28);
-    if (const char* e = std::getenv("EVO_TEAM_TEST_WITHHOLD")) p->team_withhold = e[0] == '1';
-    int sizes[4];
-    int nsz = kernel_team_sizes(KernelKey{s.d, s.dh(), s.H, s.dff, s.dtype, 1, 0}, sizes);
-    if (team_only >= 0) {
-      int k = 0;
-      for (int i = 0; i < nsz; ++i)
-        if (sizes[i] == team_only) sizes[k++] = sizes[i];
-      nsz = k;
+    CREATE_TRY(hipMalloc(&p->d_pk, off * sizeof(uint4)));
+    CREATE_TRY(launch_pack(p->d_raw, wo.W_obs, d, d, s.obs_dim, p->obs_pad, s.dtype, p->d_pk + p->pk_obs, 0));
+    CREATE_TRY(launch_pack(p->d_raw, wo.W_in, d, d, s.A, 16, EVO_FP32, p->d_pk + p->pk_win, 0));
+    CREATE_TRY(launch_pack(p->d_raw, wo.W_out, 16, s.A, d, d, EVO_FP32, p->d_pk + p->pk_wout, 0));
+    for (int l = 0; l < L; ++l) {
+      const auto& y = wo.layer[l];
+      const PackOff& po = p->poff_h[l];
+      CREATE_TRY(launch_pack(p->d_raw, y.W_qkv, 3 * d, 3 * d, d, d, s.dtype, p->d_pk + po.qkv, 0));
+      CREATE_TRY(launch_pack(p->d_raw, y.W_o, d, d, d, d, s.dtype, p->d_pk + po.o, 0));
+      CREATE_TRY(launch_pack(p->d_raw, y.W_q, d, d, d, d, s.dtype, p->d_pk + po.q, 0));
+      CREATE_TRY(launch_pack(p->d_raw, y.W_kv, 2 * d, 2 * d, d, d, s.dtype, p->d_pk + po.kv, 0));
+      CREATE_TRY(launch_pack(p->d_raw, y.W_o2, d, d, d, d, s.dtype, p->d_pk + po.o2, 0));
+      CREATE_TRY(launch_pack(p->d_raw, y.W_1, s.dff, s.dff, d, d, s.dtype, p->d_pk + po.w1, 0));
+      CREATE_TRY(launch_pack(p->d_raw, y.W_2, d, d, s.dff, s.dff, s.dtype, p->d_pk + po.w2, 0));
     }
-    int coop = 0;
-    (void)hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, p->device);
-    const size_t okv_per = (size_t)L * s.n_obs * 2 * d;
-    size_t okv_floats = (size_t)s.max_batch * okv_per, xchg_rows = 0, ctr_tiles = 0;
-    if (coop) {
-      for (int i = nsz - 1; i >= 0; --i) {  // smallest team (largest batches) last in `teams`
-        const int t = sizes[i];
-        if (p->n_cu < t) continue;
-        const int cap = (nsz > 1 && t == sizes[0]) ? p->n_cu / (t * t) : p->n_cu / t;
-        evo_policy::TeamCfg tc;
-        tc.team = t;
-        tc.max_batch = std::min(s.max_batch, std::max(cap, 1));
-        tc.okv_stride = (size_t)tc.max_batch * okv_per;
-        p->teams.insert(p->teams.begin(), tc);
-        rows = std::max(rows, (size_t)tc.max_batch * t * s.H);
-        okv_floats = std::max(okv_floats, tc.okv_stride * t);
-        xchg_rows = std::max(xchg_rows, (size_t)tc.max_batch * t * s.H);
-        ctr_tiles = std::max(ctr_tiles, (size_t)tc.max_batch);
+    // per-layer offsets of the small tensors
+    p->loff_h.resize(L);
+    std::vector<uint32_t> wkv(L), bkv(L);
+    for (int l = 0; l < L; ++l) {
+      const auto& y = wo.layer[l];
+      LayerOff& lo = p->loff_h[l];
+      lo.ln1_g = (uint32_t)y.ln1_g; lo.ln1_b = (uint32_t)y.ln1_b; lo.b_qkv = (uint32_t)y.b_qkv;
+      lo.b_o = (uint32_t)y.b_o; lo.ln2_g = (uint32_t)y.ln2_g; lo.ln2_b = (uint32_t)y.ln2_b;
+      lo.b_q = (uint32_t)y.b_q; lo.b_kv = (uint32_t)y.b_kv; lo.b_o2 = (uint32_t)y.b_o2;
+      lo.ln3_g = (uint32_t)y.ln3_g; lo.ln3_b = (uint32_t)y.ln3_b; lo.b_1 = (uint32_t)y.b_1;
+      lo.b_2 = (uint32_t)y.b_2;
+      lo.pad_[0] = lo.pad_[1] = lo.pad_[2] = 0;
+      wkv[l] = (uint32_t)y.W_kv;
+      bkv[l] = (uint32_t)y.b_kv;
+    }
+    CREATE_TRY(hipMalloc(&p->d_loff, L * sizeof(LayerOff)));
+    CREATE_TRY(hipMemcpy(p->d_loff, p->loff_h.data(), L * sizeof(LayerOff), hipMemcpyHostToDevice));
+    CREATE_TRY(hipMalloc(&p->d_poff, L * sizeof(PackOff)));
+    CREATE_TRY(hipMemcpy(p->d_poff, p->poff_h.data(), L * sizeof(PackOff), hipMemcpyHostToDevice));
+
+    // time-token keys/values for every timestep and layer; sampler constants
+    {
+      uint32_t *d_wkv = nullptr, *d_bkv = nullptr;
+      float* rows = nullptr;
+      CREATE_TRY(hipMalloc(&p->d_tkv, (size_t)T * L * 2 * d * sizeof(float)));
+      CREATE_TRY(hipMalloc(&d_wkv, L * sizeof(uint32_t)));
+      hipError_t e = hipMalloc(&d_bkv, L * sizeof(uint32_t));
+      if (e == hipSuccess) e = hipMalloc(&rows, (size_t)T * d * sizeof(float));
+      if (e == hipSuccess) e = hipMemcpy(d_wkv, wkv.data(), L * sizeof(uint32_t), hipMemcpyHostToDevice);
+      if (e == hipSuccess) e = hipMemcpy(d_bkv, bkv.data(), L * sizeof(uint32_t), hipMemcpyHostToDevice);
+      if (e == hipSuccess)
+        e = launch_time_kv(p->d_raw, (uint32_t)wo.P_mem, d_wkv, d_bkv, T, L, d, s.dtype, rows, p->d_tkv, 0);
+      if (e == hipSuccess) e = hipDeviceSynchronize();
+      (void)hipFree(d_wkv);
+      (void)hipFree(d_bkv);
+      (void)hipFree(rows);
+      CREATE_TRY(e);
+    }
+    CREATE_TRY(hipMalloc(&p->d_ddpm, (size_t)T * 8 * sizeof(float)));
+    CREATE_TRY(launch_ddpm_table(T, p->d_ddpm, 0));
+
+    // caches, observation keys/values, per-call plan buffers
+    {
+      int opts[2];
+      const int n = spt_options(s.H, opts);
+      size_t rows = 0, tiles = 0;
+      int spt_max = 1;
+      for (int i = 0; i < n; ++i) {
+        const size_t t = (size_t)(s.max_batch + opts[i] - 1) / opts[i];
+        rows = std::max(rows, t * opts[i] * s.H);
+        tiles = std::max(tiles, t);
+        spt_max = std::max(spt_max, opts[i]);
       }
+      // team variants (one sample per tile, `team` workgroups per tile) for
+      // batches that fill at most n_cu workgroups; they need cooperative
+      // launch.  With teams of 4 and 2 compiled, teams of 4 serve batches up to
+      // n_cu / 16 (latency-bound, the most parallel split wins) and teams of 2
+      // up to n_cu / 2; a single compiled size serves up to n_cu / team.
+      // EVO_TEAM=0 switches teams off, EVO_TEAM=<size> keeps only that size.
+      const char* env = std::getenv("EVO_TEAM");
+      const int team_only = env ? std::atoi(env) : -1;
+      if (const char* e = std::getenv("EVO_TEAM_SPIN_LIMIT"))
+        p->team_spin_limit = (unsigned)std::min(std::strtoul(e, nullptr, 10), 1ul << 28);
+      if (const char* e = std::getenv("EVO_TEAM_TEST_WITHHOLD")) p->team_withhold = e[0] == '1';
+      int sizes[4];
+      int nsz = kernel_team_sizes(KernelKey{s.d, s.dh(), s.H, s.dff, s.dtype, 1, 0}, sizes);
+      if (team_only >= 0) {
+        int k = 0;
+        for (int i = 0; i < nsz; ++i)
+          if (sizes[i] == team_only) sizes[k++] = sizes[i];
+        nsz = k;
+      }
+      int coop = 0;
+      (void)hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, p->device);
+      const size_t okv_per = (size_t)L * s.n_obs * 2 * d;
+      size_t okv_floats = (size_t)s.max_batch * okv_per, xchg_rows = 0, ctr_tiles = 0;
+      if (coop) {
+        for (int i = nsz - 1; i >= 0; --i) {  // smallest team (largest batches) last in `teams`
+          const int t = sizes[i];
+          if (p->n_cu < t) continue;
+          const int cap = (nsz > 1 && t == sizes[0]) ? p->n_cu / (t * t) : p->n_cu / t;
+          evo_policy::TeamCfg tc;
+          tc.team = t;
+          tc.max_batch = std::min(s.max_batch, std::max(cap, 1));
+          tc.okv_stride = (size_t)tc.max_batch * okv_per;
+          p->teams.insert(p->teams.begin(), tc);
+          rows = std::max(rows, (size_t)tc.max_batch * t * s.H);
+          okv_floats = std::max(okv_floats, tc.okv_stride * t);
+          xchg_rows = std::max(xchg_rows, (size_t)tc.max_batch * t * s.H);
+          ctr_tiles = std::max(ctr_tiles, (size_t)tc.max_batch);
+        }
+      }
+      p->cache_floats = (size_t)U * rows * d;
+      CREATE_TRY(hipMalloc(&p->d_cache, p->cache_floats * sizeof(float)));
+      CREATE_TRY(hipMalloc(&p->d_okv, okv_floats * sizeof(float)));
+      CREATE_TRY(hipMalloc(&p->d_rpart, (size_t)s.max_batch * U * T * sizeof(float)));
+      if (!p->teams.empty()) {
+        CREATE_TRY(hipMalloc(&p->d_xchg, xchg_rows * 3 * d * sizeof(float)));
+        CREATE_TRY(hipMalloc(&p->d_tctr, ctr_tiles * 16 * sizeof(unsigned)));
+        CREATE_TRY(hipMalloc(&p->d_derr, sizeof(unsigned)));
+        CREATE_TRY(hipMemset(p->d_derr, 0, sizeof(unsigned)));
+      }
+      p->tiles_cap = tiles * spt_max;
+      p->codes_cap = (size_t)std::min(s.max_sched, s.max_batch) * T * 3 * sizeof(uint64_t);
+      p->plan_bytes = (2 * p->tiles_cap * sizeof(int32_t) + 255) / 256 * 256 + p->codes_cap;
+      CREATE_TRY(hipMalloc(&p->d_plan, p->plan_bytes));
+      for (int i = 0; i < 2; ++i) {
+        CREATE_TRY(hipHostMalloc((void**)&p->h_stage[i], p->plan_bytes, hipHostMallocDefault));
+        CREATE_TRY(hipEventCreateWithFlags(&p->ev[i], hipEventDisableTiming));
+      }
+      CREATE_TRY(hipEventCreateWithFlags(&p->ev_done, hipEventDisableTiming));
     }
-    p->cache_floats = (size_t)U * rows * d;
-    CREATE_TRY(hipMalloc(&p->d_cache, p->cache_floats * sizeof(float)));
-    CREATE_TRY(hipMalloc(&p->d_okv, okv_floats * sizeof(float)));
-    CREATE_TRY(hipMalloc(&p->d_rpart, (size_t)s.max_batch * U * T * sizeof(float)));
-    if (!p->teams.empty()) {
-      CREATE_TRY(hipMalloc(&p->d_xchg, xchg_rows * 3 * d * sizeof(float)));
-      CREATE_TRY(hipMalloc(&p->d_tctr, ctr_tiles * 16 * sizeof(unsigned)));
-      CREATE_TRY(hipMalloc(&p->d_derr, sizeof(unsigned)));
-      CREATE_TRY(hipMemset(p->d_derr, 0, sizeof(unsigned)));
-    }
-    p->tiles_cap = tiles * spt_max;
-    p->codes_cap = (size_t)std::min(s.max_sched, s.max_batch) * T * 3 * sizeof(uint64_t);
-    p->plan_bytes = (2 * p->tiles_cap * sizeof(int32_t) + 255) / 256 * 256 + p->codes_cap;
-    CREATE_TRY(hipMalloc(&p->d_plan, p->plan_bytes));
-    for (int i = 0; i < 2; ++i) {
-      CREATE_TRY(hipHostMalloc((void**)&p->h_stage[i], p->plan_bytes, hipHostMallocDefault));
-      CREATE_TRY(hipEventCreateWithFlags(&p->ev[i], hipEventDisableTiming));
-    }
-    CREATE_TRY(hipEventCreateWithFlags(&p->ev_done, hipEventDisableTiming));
-  }
-  CREATE_TRY(hipDeviceSynchronize());
+    CREATE_TRY(hipDeviceSynchronize());
 #undef CREATE_TRY
-  p->reg.assign(s.max_sched, Schedule());
-  *out = p;
-  return EVO_OK;
+    p->reg.assign(s.max_sched, Schedule());
+    *out = p;
+    return EVO_OK;
+  };
+  try {
+    return body();
+  } catch (const std::bad_alloc&) {
+    release(p);
+    return fail(EVO_E_NOMEM, "host allocation failed");
+  } catch (...) {
+    release(p);
+    return fail(EVO_E_STATE, "internal error");
+  }
 }
 
 int evo_set_schedule(evo_policy* p, int32_t schedule_id, const uint8_t* lattice, int32_t rows, int32_t n_steps,
                      int32_t granularity) {
-  clear_error();
-  if (!p) return fail(EVO_E_INVALID, "policy is NULL");
-  if (schedule_id < 0 || schedule_id >= p->s.max_sched)
-    return fail(EVO_E_INVALID, "schedule_id %d outside [0, %d)", schedule_id, p->s.max_sched);
-  if (n_steps != p->s.T) return fail(EVO_E_INVALID, "n_steps is %d, the policy has %d", n_steps, p->s.T);
-  Schedule sc;
-  const int rc = build_schedule(p->s, lattice, rows, granularity, &sc);
-  if (rc) return rc;
-  p->reg[schedule_id] = std::move(sc);
-  return EVO_OK;
+  return guarded([&]() -> int {
+    clear_error();
+    if (!p) return fail(EVO_E_INVALID, "policy is NULL");
+    if (schedule_id < 0 || schedule_id >= p->s.max_sched)
+      return fail(EVO_E_INVALID, "schedule_id %d outside [0, %d)", schedule_id, p->s.max_sched);
+    if (n_steps != p->s.T) return fail(EVO_E_INVALID, "n_steps is %d, the policy has %d", n_steps, p->s.T);
+    Schedule sc;
+    const int rc = build_schedule(p->s, lattice, rows, granularity, &sc);
+    if (rc) return rc;
+    p->reg[schedule_id] = std::move(sc);
+    return EVO_OK;
+  });
 }
 
 int evo_set_schedule_pairs(evo_policy* p, int32_t schedule_id, const int32_t* pairs, int32_t K,
                            int32_t granularity) {
-  clear_error();
-  if (!p) return fail(EVO_E_INVALID, "policy is NULL");
-  if (K < 0 || (K > 0 && !pairs)) return fail(EVO_E_INVALID, "bad pairs / K");
-  if (granularity != EVO_GRAN_LAYER && granularity != EVO_GRAN_UNIT)
-    return fail(EVO_E_INVALID, "bad granularity");
-  const int rows = granularity == EVO_GRAN_LAYER ? p->s.L : p->s.U();
-  const int T = p->s.T;
-  std::vector<uint8_t> lat((size_t)rows * T, 0);
-  for (int i = 0; i < K; ++i) {
-    const int b = pairs[2 * i], t = pairs[2 * i + 1];
-    if (b < 0 || b >= rows || t < 0 || t >= T) return fail(EVO_E_INVALID, "pair %d = (%d, %d) out of range", i, b, t);
-    if (lat[(size_t)b * T + t]) return fail(EVO_E_INVALID, "pair %d = (%d, %d) is a duplicate", i, b, t);
-    lat[(size_t)b * T + t] = 1;
-  }
-  return evo_set_schedule(p, schedule_id, lat.data(), rows, T, granularity);
+  return guarded([&]() -> int {
+    clear_error();
+    if (!p) return fail(EVO_E_INVALID, "policy is NULL");
+    if (K < 0 || (K > 0 && !pairs)) return fail(EVO_E_INVALID, "bad pairs / K");
+    if (granularity != EVO_GRAN_LAYER && granularity != EVO_GRAN_UNIT)
+      return fail(EVO_E_INVALID, "bad granularity");
+    const int rows = granularity == EVO_GRAN_LAYER ? p->s.L : p->s.U();
+    const int T = p->s.T;
+    std::vector<uint8_t> lat((size_t)rows * T, 0);
+    for (int i = 0; i < K; ++i) {
+      const int b = pairs[2 * i], t = pairs[2 * i + 1];
+      if (b < 0 || b >= rows || t < 0 || t >= T) return fail(EVO_E_INVALID, "pair %d = (%d, %d) out of range", i, b, t);
+      if (lat[(size_t)b * T + t]) return fail(EVO_E_INVALID, "pair %d = (%d, %d) is a duplicate", i, b, t);
+      lat[(size_t)b * T + t] = 1;
+    }
+    return evo_set_schedule(p, schedule_id, lat.data(), rows, T, granularity);
+  });
 }
 
 static int denoise_impl(evo_policy* p, int32_t batch, const float* obs_cond, const float* noise,
                         const int32_t* schedule_ids, float* actions_out, float* acts_out, void* hip_stream) {
-  clear_error();
-  if (!p) return fail(EVO_E_INVALID, "policy is NULL");
-  const Shape& s = p->s;
-  if (batch < 1 || batch > s.max_batch) return fail(EVO_E_INVALID, "batch %d outside [1, %d]", batch, s.max_batch);
-  if (!obs_cond || !noise || !actions_out) return fail(EVO_E_INVALID, "NULL device pointer");
-  for (int n = 0; n < batch; ++n) {
-    const int id = schedule_ids ? schedule_ids[n] : 0;
-    if (id < 0 || id >= s.max_sched) return fail(EVO_E_INVALID, "schedule id %d of sample %d out of range", id, n);
-    if (!p->reg[id].valid) return fail(EVO_E_STATE, "schedule id %d of sample %d is not registered", id, n);
-  }
-  DeviceGuard guard(p->device);
-  hipStream_t stream = (hipStream_t)hip_stream;
-  // samples per tile: two when a single-sample tiling would oversubscribe the CUs
-  int opts[2];
-  const int nopt = spt_options(s.H, opts);
-  int spt = 0, threads = 0, team = 1;
-  for (int i = 0; i < nopt; ++i) {
-    KernelKey k{s.d, s.dh(), s.H, s.dff, s.dtype, opts[i], 1};
-    int th;
-    if (!kernel_available(k, &th)) continue;
-    if (spt == 0 || (opts[i] > spt && batch > p->n_cu)) {
-      spt = opts[i];
-      threads = th;
+  return guarded([&]() -> int {
+    clear_error();
+    if (!p) return fail(EVO_E_INVALID, "policy is NULL");
+    const Shape& s = p->s;
+    if (batch < 1 || batch > s.max_batch) return fail(EVO_E_INVALID, "batch %d outside [1, %d]", batch, s.max_batch);
+    if (!obs_cond || !noise || !actions_out) return fail(EVO_E_INVALID, "NULL device pointer");
+    for (int n = 0; n < batch; ++n) {
+      const int id = schedule_ids ? schedule_ids[n] : 0;
+      if (id < 0 || id >= s.max_sched) return fail(EVO_E_INVALID, "schedule id %d of sample %d out of range", id, n);
+      if (!p->reg[id].valid) return fail(EVO_E_STATE, "schedule id %d of sample %d is not registered", id, n);
     }
-  }
-  if (!spt) return fail(EVO_E_UNSUPPORTED, "no kernel for this shape");
-  // small batches: several workgroups per one-sample tile
-  const evo_policy::TeamCfg* tc = nullptr;
-  for (const auto& c : p->teams) {
-    if (batch > c.max_batch) continue;
-    KernelKey k{s.d, s.dh(), s.H, s.dff, s.dtype, 1, c.team};
-    int th;
-    if (kernel_available(k, &th)) {
-      spt = 1;
-      threads = th;
-      team = c.team;
-      tc = &c;
-      break;
+    DeviceGuard guard(p->device);
+    hipStream_t stream = (hipStream_t)hip_stream;
+    // samples per tile: two when a single-sample tiling would oversubscribe the CUs
+    int opts[2];
+    const int nopt = spt_options(s.H, opts);
+    int spt = 0, threads = 0, team = 1;
+    for (int i = 0; i < nopt; ++i) {
+      KernelKey k{s.d, s.dh(), s.H, s.dff, s.dtype, opts[i], 1};
+      int th;
+      if (!kernel_available(k, &th)) continue;
+      if (spt == 0 || (opts[i] > spt && batch > p->n_cu)) {
+        spt = opts[i];
+        threads = th;
+      }
     }
-  }
-  Plan plan;
-  int rc = build_plan(s, p->reg, schedule_ids, batch, spt, 8, &plan);
-  if (rc) return rc;
-  const size_t ntile_ent = (size_t)plan.n_tiles * spt;
-  const size_t codes_off = (2 * p->tiles_cap * sizeof(int32_t) + 255) / 256 * 256;
-  const size_t ucodes = (size_t)s.T * 3 * sizeof(uint64_t);
-  if (ntile_ent > p->tiles_cap || plan.used.size() * ucodes > p->codes_cap)
-    return fail(EVO_E_STATE, "plan exceeds the policy's buffers");
-  // Calls on a different stream than the previous one wait for it: the
-  // plan, caches and observation keys/values are per-policy buffers.
-  if (p->launched && stream != p->last_stream) HIP_TRY(hipStreamWaitEvent(stream, p->ev_done, 0));
-  // Stage the plan in pinned memory and upload it, unless the device copy
-  // already holds exactly these bytes (repeated calls with the same ids).
-  const size_t nbytes = codes_off + plan.used.size() * ucodes;
-  {
-    std::vector<uint8_t> bytes(nbytes, 0);
-    std::memcpy(bytes.data(), plan.tile_sample.data(), ntile_ent * sizeof(int32_t));
-    std::memcpy(bytes.data() + p->tiles_cap * sizeof(int32_t), plan.tile_slot.data(), ntile_ent * sizeof(int32_t));
-    for (size_t i = 0; i < plan.used.size(); ++i)
-      std::memcpy(bytes.data() + codes_off + i * ucodes, p->reg[plan.used[i]].masks.data(), ucodes);
-    if (bytes != p->uploaded) {
-      const int st = p->stage;
-      if (hipEventSynchronize(p->ev[st]) != hipSuccess) return fail(EVO_E_HIP, "event synchronize failed");
-      std::memcpy(p->h_stage[st], bytes.data(), nbytes);
-      HIP_TRY(hipMemcpyAsync(p->d_plan, p->h_stage[st], nbytes, hipMemcpyHostToDevice, stream));
-      HIP_TRY(hipEventRecord(p->ev[st], stream));
-      p->stage ^= 1;
-      p->uploaded.swap(bytes);
+    if (!spt) return fail(EVO_E_UNSUPPORTED, "no kernel for this shape");
+    // small batches: several workgroups per one-sample tile
+    const evo_policy::TeamCfg* tc = nullptr;
+    for (const auto& c : p->teams) {
+      if (batch > c.max_batch) continue;
+      KernelKey k{s.d, s.dh(), s.H, s.dff, s.dtype, 1, c.team};
+      int th;
+      if (kernel_available(k, &th)) {
+        spt = 1;
+        threads = th;
+        team = c.team;
+        tc = &c;
+        break;
+      }
     }
-  }
+    Plan plan;
+    int rc = build_plan(s, p->reg, schedule_ids, batch, spt, 8, &plan);
+    if (rc) return rc;
+    const size_t ntile_ent = (size_t)plan.n_tiles * spt;
+    const size_t codes_off = (2 * p->tiles_cap * sizeof(int32_t) + 255) / 256 * 256;
+    const size_t ucodes = (size_t)s.T * 3 * sizeof(uint64_t);
+    if (ntile_ent > p->tiles_cap || plan.used.size() * ucodes > p->codes_cap)
+      return fail(EVO_E_STATE, "plan exceeds the policy's buffers");
+    // Calls on a different stream than the previous one wait for it: the
+    // plan, caches and observation keys/values are per-policy buffers.
+    if (p->launched && stream != p->last_stream) HIP_TRY(hipStreamWaitEvent(stream, p->ev_done, 0));
+    // Stage the plan in pinned memory and upload it, unless the device copy
+    // already holds exactly these bytes (repeated calls with the same ids).
+    const size_t nbytes = codes_off + plan.used.size() * ucodes;
+    {
+      std::vector<uint8_t> bytes(nbytes, 0);
+      std::memcpy(bytes.data(), plan.tile_sample.data(), ntile_ent * sizeof(int32_t));
+      std::memcpy(bytes.data() + p->tiles_cap * sizeof(int32_t), plan.tile_slot.data(), ntile_ent * sizeof(int32_t));
+      for (size_t i = 0; i < plan.used.size(); ++i)
+        std::memcpy(bytes.data() + codes_off + i * ucodes, p->reg[plan.used[i]].masks.data(), ucodes);
+      if (bytes != p->uploaded) {
+        const int st = p->stage;
+        if (hipEventSynchronize(p->ev[st]) != hipSuccess) return fail(EVO_E_HIP, "event synchronize failed");
+        std::memcpy(p->h_stage[st], bytes.data(), nbytes);
+        HIP_TRY(hipMemcpyAsync(p->d_plan, p->h_stage[st], nbytes, hipMemcpyHostToDevice, stream));
+        HIP_TRY(hipEventRecord(p->ev[st], stream));
+        p->stage ^= 1;
+        p->uploaded.swap(bytes);
+      }
+    }
 
-  KParams kp;
-  std::memset(&kp, 0, sizeof(kp));
-  kp.L = s.L; kp.A = s.A; kp.n_obs = s.n_obs; kp.obs_dim = s.obs_dim; kp.obs_pad = p->obs_pad;
-  kp.T = s.T; kp.clip = s.clip; kp.n_tiles = plan.n_tiles;
-  kp.raw = p->d_raw; kp.pk = p->d_pk; kp.loff = p->d_loff; kp.poff = p->d_poff; kp.pk_obs = p->pk_obs;
-  const WeightOffsets& wo = p->wo;
-  kp.W_in = (uint32_t)wo.W_in; kp.b_in = (uint32_t)wo.b_in; kp.P_act = (uint32_t)wo.P_act;
-  kp.b_obs = (uint32_t)wo.b_obs; kp.P_mem = (uint32_t)wo.P_mem; kp.lnf_g = (uint32_t)wo.lnf_g;
-  kp.lnf_b = (uint32_t)wo.lnf_b; kp.W_out = (uint32_t)wo.W_out; kp.b_out = (uint32_t)wo.b_out;
-  kp.tkv = p->d_tkv; kp.ddpm = p->d_ddpm;
-  kp.tile_sample = reinterpret_cast<const int32_t*>(p->d_plan);
-  kp.tile_slot = reinterpret_cast<const int32_t*>(p->d_plan) + p->tiles_cap;
-  kp.masks = reinterpret_cast<const uint64_t*>(p->d_plan + codes_off);
-  kp.pk_win = p->pk_win;
-  kp.pk_wout = p->pk_wout;
-  kp.obs = obs_cond; kp.noise = noise; kp.out = actions_out; kp.okv = p->d_okv; kp.cache = p->d_cache;
-  kp.acts = acts_out;
-  kp.batch = batch;
-  kp.team = team;
-  if (team > 1) {
-    if (plan.n_tiles > tc->max_batch) return fail(EVO_E_STATE, "team plan exceeds the buffers");
-    kp.xchg = p->d_xchg;
-    kp.tctr = p->d_tctr;
-    kp.derr = p->d_derr;
-    kp.okv_member_stride = tc->okv_stride;
-    kp.spin_limit = p->team_spin_limit;
-    kp.withhold = p->team_withhold;
-    HIP_TRY(launch_zero_u32(p->d_tctr, plan.n_tiles * 16, stream));
-  }
-  KernelKey key{s.d, s.dh(), s.H, s.dff, s.dtype, spt, team};
-  HIP_TRY(launch_denoise(key, kp, stream));
-  HIP_TRY(hipEventRecord(p->ev_done, stream));
-  p->last_stream = stream;
-  p->launched = true;
+    KParams kp;
+    std::memset(&kp, 0, sizeof(kp));
+    kp.L = s.L; kp.A = s.A; kp.n_obs = s.n_obs; kp.obs_dim = s.obs_dim; kp.obs_pad = p->obs_pad;
+    kp.T = s.T; kp.clip = s.clip; kp.n_tiles = plan.n_tiles;
+    kp.raw = p->d_raw; kp.pk = p->d_pk; kp.loff = p->d_loff; kp.poff = p->d_poff; kp.pk_obs = p->pk_obs;
+    const WeightOffsets& wo = p->wo;
+    kp.W_in = (uint32_t)wo.W_in; kp.b_in = (uint32_t)wo.b_in; kp.P_act = (uint32_t)wo.P_act;
+    kp.b_obs = (uint32_t)wo.b_obs; kp.P_mem = (uint32_t)wo.P_mem; kp.lnf_g = (uint32_t)wo.lnf_g;
+    kp.lnf_b = (uint32_t)wo.lnf_b; kp.W_out = (uint32_t)wo.W_out; kp.b_out = (uint32_t)wo.b_out;
+    kp.tkv = p->d_tkv; kp.ddpm = p->d_ddpm;
+    kp.tile_sample = reinterpret_cast<const int32_t*>(p->d_plan);
+    kp.tile_slot = reinterpret_cast<const int32_t*>(p->d_plan) + p->tiles_cap;
+    kp.masks = reinterpret_cast<const uint64_t*>(p->d_plan + codes_off);
+    kp.pk_win = p->pk_win;
+    kp.pk_wout = p->pk_wout;
+    kp.obs = obs_cond; kp.noise = noise; kp.out = actions_out; kp.okv = p->d_okv; kp.cache = p->d_cache;
+    kp.acts = acts_out;
+    kp.batch = batch;
+    kp.team = team;
+    if (team > 1) {
+      if (plan.n_tiles > tc->max_batch) return fail(EVO_E_STATE, "team plan exceeds the buffers");
+      kp.xchg = p->d_xchg;
+      kp.tctr = p->d_tctr;
+      kp.derr = p->d_derr;
+      kp.okv_member_stride = tc->okv_stride;
+      kp.spin_limit = p->team_spin_limit;
+      kp.withhold = p->team_withhold;
+      HIP_TRY(launch_zero_u32(p->d_tctr, plan.n_tiles * 16, stream));
+    }
+    KernelKey key{s.d, s.dh(), s.H, s.dff, s.dtype, spt, team};
+    HIP_TRY(launch_denoise(key, kp, stream));
+    HIP_TRY(hipEventRecord(p->ev_done, stream));
+    p->last_stream = stream;
+    p->launched = true;
 
-  call_stats(s, p->reg, schedule_ids, batch, &plan, team, &p->last);
-  p->has_last = true;
-  p->last_plan = std::move(plan);
-  p->last_threads = threads;
-  p->last_team = team;
-  return EVO_OK;
+    call_stats(s, p->reg, schedule_ids, batch, &plan, team, &p->last);
+    p->has_last = true;
+    p->last_plan = std::move(plan);
+    p->last_threads = threads;
+    p->last_team = team;
+    return EVO_OK;
+  });
 }
 
 int evo_synchronize(evo_policy* p) {
@@ -534,37 +553,43 @@ int evo_collect_activations(evo_policy* p, int32_t batch, const float* obs_cond,
 }
 
 int evo_redundancy_scores(evo_policy* p, int32_t rollouts, const float* acts, float* scores_out, void* hip_stream) {
-  clear_error();
-  if (!p) return fail(EVO_E_INVALID, "policy is NULL");
-  const Shape& s = p->s;
-  if (!acts || !scores_out) return fail(EVO_E_INVALID, "NULL device pointer");
-  if (rollouts < 1 || rollouts > s.max_batch)
-    return fail(EVO_E_INVALID, "rollouts %d outside [1, %d]", rollouts, s.max_batch);
-  if (s.T < 2 || s.T > kGramMaxSteps)
-    return fail(EVO_E_UNSUPPORTED, "redundancy scores need 2 <= n_steps <= %d", kGramMaxSteps);
-  DeviceGuard guard(p->device);
-  hipStream_t stream = (hipStream_t)hip_stream;
-  if (p->launched && stream != p->last_stream) HIP_TRY(hipStreamWaitEvent(stream, p->ev_done, 0));
-  HIP_TRY(launch_redundancy(acts, rollouts, s.U(), s.T, (long long)s.H * s.d, p->d_rpart, scores_out, stream));
-  HIP_TRY(hipEventRecord(p->ev_done, stream));
-  p->last_stream = stream;
-  p->launched = true;
-  return EVO_OK;
+  return guarded([&]() -> int {
+    clear_error();
+    if (!p) return fail(EVO_E_INVALID, "policy is NULL");
+    const Shape& s = p->s;
+    if (!acts || !scores_out) return fail(EVO_E_INVALID, "NULL device pointer");
+    if (rollouts < 1 || rollouts > s.max_batch)
+      return fail(EVO_E_INVALID, "rollouts %d outside [1, %d]", rollouts, s.max_batch);
+    if (s.T < 2 || s.T > kGramMaxSteps)
+      return fail(EVO_E_UNSUPPORTED, "redundancy scores need 2 <= n_steps <= %d", kGramMaxSteps);
+    DeviceGuard guard(p->device);
+    hipStream_t stream = (hipStream_t)hip_stream;
+    if (p->launched && stream != p->last_stream) HIP_TRY(hipStreamWaitEvent(stream, p->ev_done, 0));
+    HIP_TRY(launch_redundancy(acts, rollouts, s.U(), s.T, (long long)s.H * s.d, p->d_rpart, scores_out, stream));
+    HIP_TRY(hipEventRecord(p->ev_done, stream));
+    p->last_stream = stream;
+    p->launched = true;
+    return EVO_OK;
+  });
 }
 
 int evo_guided_probabilities(const float* scores, int32_t rows, int32_t n_steps, double eps, double gamma,
                              double* probs_out) {
-  clear_error();
-  if (!scores || !probs_out || rows < 1 || n_steps < 1) return fail(EVO_E_INVALID, "bad arguments");
-  if (!(eps >= 0.0) || !(gamma >= 0.0)) return fail(EVO_E_INVALID, "eps and gamma must be >= 0");
-  return guided_probabilities(scores, (size_t)rows * n_steps, eps, gamma, probs_out);
+  return guarded([&]() -> int {
+    clear_error();
+    if (!scores || !probs_out || rows < 1 || n_steps < 1) return fail(EVO_E_INVALID, "bad arguments");
+    if (!(eps >= 0.0) || !(gamma >= 0.0)) return fail(EVO_E_INVALID, "eps and gamma must be >= 0");
+    return guided_probabilities(scores, (size_t)rows * n_steps, eps, gamma, probs_out);
+  });
 }
 
 int evo_guided_sample(const double* probs, int32_t rows, int32_t n_steps, int32_t K, const double* uniforms,
                       int32_t* pairs_out) {
-  clear_error();
-  if (!probs || !uniforms || !pairs_out || rows < 1 || n_steps < 1) return fail(EVO_E_INVALID, "bad arguments");
-  return guided_sample(probs, rows, n_steps, K, uniforms, pairs_out);
+  return guarded([&]() -> int {
+    clear_error();
+    if (!probs || !uniforms || !pairs_out || rows < 1 || n_steps < 1) return fail(EVO_E_INVALID, "bad arguments");
+    return guided_sample(probs, rows, n_steps, K, uniforms, pairs_out);
+  });
 }
 
 int evo_get_stats(const evo_policy* p, evo_stats* out) {
@@ -577,66 +602,72 @@ int evo_get_stats(const evo_policy* p, evo_stats* out) {
 
 int evo_schedule_stats(const evo_policy_desc* desc, const uint8_t* lattices, int32_t n_lat, int32_t rows,
                        int32_t granularity, const int32_t* ids, int32_t batch, evo_stats* out) {
-  clear_error();
-  Shape s;
-  int rc = shape_from_desc(desc, &s);
-  if (rc) return rc;
-  if (!lattices || !out || n_lat < 1 || batch < 1) return fail(EVO_E_INVALID, "bad arguments");
-  std::vector<Schedule> reg(n_lat);
-  for (int i = 0; i < n_lat; ++i) {
-    rc = build_schedule(s, lattices + (size_t)i * rows * s.T, rows, granularity, &reg[i]);
+  return guarded([&]() -> int {
+    clear_error();
+    Shape s;
+    int rc = shape_from_desc(desc, &s);
     if (rc) return rc;
-  }
-  for (int n = 0; n < batch; ++n) {
-    const int id = ids ? ids[n] : 0;
-    if (id < 0 || id >= n_lat) return fail(EVO_E_INVALID, "id %d of sample %d out of range", id, n);
-  }
-  call_stats(s, reg, ids, batch, nullptr, 1, out);
-  return EVO_OK;
+    if (!lattices || !out || n_lat < 1 || batch < 1) return fail(EVO_E_INVALID, "bad arguments");
+    std::vector<Schedule> reg(n_lat);
+    for (int i = 0; i < n_lat; ++i) {
+      rc = build_schedule(s, lattices + (size_t)i * rows * s.T, rows, granularity, &reg[i]);
+      if (rc) return rc;
+    }
+    for (int n = 0; n < batch; ++n) {
+      const int id = ids ? ids[n] : 0;
+      if (id < 0 || id >= n_lat) return fail(EVO_E_INVALID, "id %d of sample %d out of range", id, n);
+    }
+    call_stats(s, reg, ids, batch, nullptr, 1, out);
+    return EVO_OK;
+  });
 }
 
 int evo_schedule_codes(const evo_policy_desc* desc, const uint8_t* lattice, int32_t rows, int32_t granularity,
                        uint8_t* out) {
-  clear_error();
-  Shape s;
-  int rc = shape_from_desc(desc, &s);
-  if (rc) return rc;
-  if (!out) return fail(EVO_E_INVALID, "out is NULL");
-  Schedule sc;
-  rc = build_schedule(s, lattice, rows, granularity, &sc);
-  if (rc) return rc;
-  std::memcpy(out, sc.codes.data(), sc.codes.size());
-  return EVO_OK;
+  return guarded([&]() -> int {
+    clear_error();
+    Shape s;
+    int rc = shape_from_desc(desc, &s);
+    if (rc) return rc;
+    if (!out) return fail(EVO_E_INVALID, "out is NULL");
+    Schedule sc;
+    rc = build_schedule(s, lattice, rows, granularity, &sc);
+    if (rc) return rc;
+    std::memcpy(out, sc.codes.data(), sc.codes.size());
+    return EVO_OK;
+  });
 }
 
 int evo_debug_read_cache(evo_policy* p, int32_t unit, int32_t sample, float* host_dst) {
-  clear_error();
-  if (!p || !host_dst) return fail(EVO_E_INVALID, "NULL argument");
-  if (!p->has_last) return fail(EVO_E_STATE, "no evo_denoise call yet");
-  const Shape& s = p->s;
-  if (unit < 0 || unit >= s.U()) return fail(EVO_E_INVALID, "unit out of range");
-  const Plan& pl = p->last_plan;
-  int tile = -1, slot = -1;
-  for (int q = 0; q < pl.n_tiles && tile < 0; ++q)
-    for (int j = 0; j < pl.spt; ++j)
-      if (pl.tile_sample[(size_t)q * pl.spt + j] == sample) { tile = q; slot = j; }
-  if (tile < 0) return fail(EVO_E_INVALID, "sample %d not in the last call", sample);
-  DeviceGuard guard(p->device);
-  HIP_TRY(hipDeviceSynchronize());
-  const int R = pl.spt * s.H, d = s.d, NW = p->last_threads / 64, RB = R / 16, CBW = d / 16 / NW;
-  std::vector<float> buf((size_t)R * d);
-  HIP_TRY(hipMemcpy(buf.data(), p->d_cache + ((size_t)tile * p->last_team * s.U() + unit) * R * d,
-                    buf.size() * sizeof(float),
-                    hipMemcpyDeviceToHost));
-  for (int i = 0; i < s.H; ++i) {
-    const int row = slot * s.H + i, rb = row / 16, rr = row % 16;
-    for (int col = 0; col < d; ++col) {
-      const int cbk = col / 16, w = cbk / CBW, c = cbk % CBW;
-      const int lane = (col % 16) + 16 * (rr / 4);
-      host_dst[(size_t)i * d + col] = buf[((size_t)((w * RB + rb) * CBW + c) * 64 + lane) * 4 + rr % 4];
+  return guarded([&]() -> int {
+    clear_error();
+    if (!p || !host_dst) return fail(EVO_E_INVALID, "NULL argument");
+    if (!p->has_last) return fail(EVO_E_STATE, "no evo_denoise call yet");
+    const Shape& s = p->s;
+    if (unit < 0 || unit >= s.U()) return fail(EVO_E_INVALID, "unit out of range");
+    const Plan& pl = p->last_plan;
+    int tile = -1, slot = -1;
+    for (int q = 0; q < pl.n_tiles && tile < 0; ++q)
+      for (int j = 0; j < pl.spt; ++j)
+        if (pl.tile_sample[(size_t)q * pl.spt + j] == sample) { tile = q; slot = j; }
+    if (tile < 0) return fail(EVO_E_INVALID, "sample %d not in the last call", sample);
+    DeviceGuard guard(p->device);
+    HIP_TRY(hipDeviceSynchronize());
+    const int R = pl.spt * s.H, d = s.d, NW = p->last_threads / 64, RB = R / 16, CBW = d / 16 / NW;
+    std::vector<float> buf((size_t)R * d);
+    HIP_TRY(hipMemcpy(buf.data(), p->d_cache + ((size_t)tile * p->last_team * s.U() + unit) * R * d,
+                      buf.size() * sizeof(float),
+                      hipMemcpyDeviceToHost));
+    for (int i = 0; i < s.H; ++i) {
+      const int row = slot * s.H + i, rb = row / 16, rr = row % 16;
+      for (int col = 0; col < d; ++col) {
+        const int cbk = col / 16, w = cbk / CBW, c = cbk % CBW;
+        const int lane = (col % 16) + 16 * (rr / 4);
+        host_dst[(size_t)i * d + col] = buf[((size_t)((w * RB + rb) * CBW + c) * 64 + lane) * 4 + rr % 4];
+      }
     }
-  }
-  return EVO_OK;
+    return EVO_OK;
+  });
 }
 
 void evo_destroy_policy(evo_policy* p) {

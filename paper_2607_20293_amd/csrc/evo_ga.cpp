@@ -156,6 +156,8 @@ int ga_check(const evo_ga_config* c, int rows, int T, const double* probs, bool 
   if (N > (1ll << 30)) return fail(EVO_E_INVALID, "lattice too large");
   if (c->K < 1 || c->K > N) return fail(EVO_E_INVALID, "K = %d outside [1, %lld]", c->K, N);
   if (c->pop_size < 1 || c->pop_size > (1 << 20)) return fail(EVO_E_INVALID, "pop_size %d", c->pop_size);
+  if ((long long)c->pop_size * c->K > (1ll << 28))
+    return fail(EVO_E_INVALID, "pop_size x K = %lld exceeds 2^28", (long long)c->pop_size * c->K);
   if (c->n_elite < 0 || c->n_elite > c->pop_size)
     return fail(EVO_E_INVALID, "n_elite %d outside [0, pop_size]", c->n_elite);
   if (c->max_generations < 1) return fail(EVO_E_INVALID, "max_generations %d < 1", c->max_generations);
@@ -306,51 +308,57 @@ extern "C" {
 
 int evo_ga_initial_population(const evo_ga_config* cfg, int32_t rows, int32_t n_steps, const double* probs,
                               int32_t* pop_out) {
-  evo::clear_error();
-  int rc = evo::ga_check(cfg, rows, n_steps, probs, true);
-  if (rc) return rc;
-  if (!pop_out) return evo::fail(EVO_E_INVALID, "pop_out is NULL");
-  return evo::ga_initial(*cfg, rows, n_steps, probs, pop_out);
+  return evo::guarded([&]() -> int {
+    evo::clear_error();
+    int rc = evo::ga_check(cfg, rows, n_steps, probs, true);
+    if (rc) return rc;
+    if (!pop_out) return evo::fail(EVO_E_INVALID, "pop_out is NULL");
+    return evo::ga_initial(*cfg, rows, n_steps, probs, pop_out);
+  });
 }
 
 int evo_ga_next_generation(const evo_ga_config* cfg, int32_t rows, int32_t n_steps, int32_t generation,
                            const int32_t* pop, const double* fitness, int32_t* next_out) {
-  evo::clear_error();
-  int rc = evo::ga_check(cfg, rows, n_steps, nullptr, false);
-  if (rc) return rc;
-  if (!pop || !fitness || !next_out) return evo::fail(EVO_E_INVALID, "NULL pointer");
-  if (generation < 1) return evo::fail(EVO_E_INVALID, "generation %d < 1", generation);
-  for (int i = 0; i < cfg->pop_size; ++i)
-    if (std::isnan(fitness[i])) return evo::fail(EVO_E_INVALID, "fitness %d is NaN", i);
-  rc = evo::ga_check_population(pop, cfg->pop_size, cfg->K, rows * n_steps);
-  if (rc) return rc;
-  return evo::ga_next(*cfg, rows, n_steps, generation, pop, fitness, next_out);
+  return evo::guarded([&]() -> int {
+    evo::clear_error();
+    int rc = evo::ga_check(cfg, rows, n_steps, nullptr, false);
+    if (rc) return rc;
+    if (!pop || !fitness || !next_out) return evo::fail(EVO_E_INVALID, "NULL pointer");
+    if (generation < 1) return evo::fail(EVO_E_INVALID, "generation %d < 1", generation);
+    for (int i = 0; i < cfg->pop_size; ++i)
+      if (std::isnan(fitness[i])) return evo::fail(EVO_E_INVALID, "fitness %d is NaN", i);
+    rc = evo::ga_check_population(pop, cfg->pop_size, cfg->K, rows * n_steps);
+    if (rc) return rc;
+    return evo::ga_next(*cfg, rows, n_steps, generation, pop, fitness, next_out);
+  });
 }
 
 int evo_ga_search(const evo_ga_config* cfg, int32_t rows, int32_t n_steps, const double* probs,
                   evo_quick_fn quick, evo_formal_fn formal, void* user, double q_base, double delta_acc,
                   evo_search_result* result, int32_t* best_out, int32_t* pop_history, double* fit_history) {
-  evo::clear_error();
-  int rc = evo::ga_check(cfg, rows, n_steps, probs, true);
-  if (rc) return rc;
-  if (!quick || !result || !best_out) return evo::fail(EVO_E_INVALID, "NULL pointer");
-  if (std::isnan(q_base) || std::isnan(delta_acc)) return evo::fail(EVO_E_INVALID, "q_base / delta_acc NaN");
-  evo::SearchEval ev;
-  ev.quick = [&](int n, const int32_t* sch, double* out) {
-    const int r = quick(user, n, sch, out);
-    if (r) return evo::fail(EVO_E_STATE, "quick evaluation callback returned %d", r);
-    for (int i = 0; i < n; ++i)
-      if (std::isnan(out[i])) return evo::fail(EVO_E_INVALID, "quick evaluation returned NaN");
-    return (int)EVO_OK;
-  };
-  if (formal)
-    ev.formal = [&](const int32_t* sch, double* out) {
-      const int r = formal(user, sch, out);
-      if (r) return evo::fail(EVO_E_STATE, "formal evaluation callback returned %d", r);
+  return evo::guarded([&]() -> int {
+    evo::clear_error();
+    int rc = evo::ga_check(cfg, rows, n_steps, probs, true);
+    if (rc) return rc;
+    if (!quick || !result || !best_out) return evo::fail(EVO_E_INVALID, "NULL pointer");
+    if (std::isnan(q_base) || std::isnan(delta_acc)) return evo::fail(EVO_E_INVALID, "q_base / delta_acc NaN");
+    evo::SearchEval ev;
+    ev.quick = [&](int n, const int32_t* sch, double* out) {
+      const int r = quick(user, n, sch, out);
+      if (r) return evo::fail(EVO_E_STATE, "quick evaluation callback returned %d", r);
+      for (int i = 0; i < n; ++i)
+        if (std::isnan(out[i])) return evo::fail(EVO_E_INVALID, "quick evaluation returned NaN");
       return (int)EVO_OK;
     };
-  return evo::ga_search(*cfg, rows, n_steps, probs, ev, q_base, delta_acc, result, best_out, pop_history,
-                        fit_history);
+    if (formal)
+      ev.formal = [&](const int32_t* sch, double* out) {
+        const int r = formal(user, sch, out);
+        if (r) return evo::fail(EVO_E_STATE, "formal evaluation callback returned %d", r);
+        return (int)EVO_OK;
+      };
+    return evo::ga_search(*cfg, rows, n_steps, probs, ev, q_base, delta_acc, result, best_out, pop_history,
+                          fit_history);
+  });
 }
 
 }  // extern "C"

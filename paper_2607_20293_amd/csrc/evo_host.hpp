@@ -6,7 +6,9 @@
 
 #include <cstdint>
 #include <string>
+#include <exception>
 #include <functional>
+#include <new>
 #include <vector>
 
 #include "evo.h"
@@ -117,6 +119,22 @@ int guided_sample(const double* p, int rows, int T, int K, const double* u, int3
 // shape and device of a policy (evo_api.hip)
 const Shape& policy_shape(const evo_policy* p);
 int policy_device(const evo_policy* p);
+
+// Runs an ABI call's body and turns C++ exceptions (host allocation
+// failures of vectors sized by the caller's arguments) into error codes, so
+// none crosses the C boundary.
+template <class F>
+int guarded(F&& f) {
+  try {
+    return f();
+  } catch (const std::bad_alloc&) {
+    return fail(EVO_E_NOMEM, "host allocation failed");
+  } catch (const std::exception& e) {
+    return fail(EVO_E_STATE, "internal error: %s", e.what());
+  } catch (...) {
+    return fail(EVO_E_STATE, "internal error");
+  }
+}
 
 // schedule search (evo_ga.cpp)
 struct SearchEval {

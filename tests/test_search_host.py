@@ -94,6 +94,8 @@ def test_callback_error_and_invalid_configs():
         kw.update(bad)
         with pytest.raises(evo.EvoError):
             evo.ga_initial_population(evo.GAConfig.make(**kw), 2, 5)
+    with pytest.raises(evo.EvoError, match="2\\^28"):
+        evo.ga_initial_population(evo.GAConfig.make(1 << 24, pop_size=30, n_guided=0), 1 << 12, 1 << 12)
     with pytest.raises(evo.EvoError, match="probabilities"):
         evo.ga_initial_population(evo.GAConfig.make(4, pop_size=6, n_elite=2, n_guided=2), 2, 5)
     p = np.zeros((2, 5))
