@@ -16,6 +16,8 @@ Seed streams (numpy ``default_rng`` with a sequence seed):
   [seed, 2]     sampler noise, N(0, 1)
   [seed, 3, j]  refresh lattice j
   [seed, 4]     sample -> schedule assignment
+  [seed, 5]     observation-encoder weights
+  [seed, 6]     images
 """
 from __future__ import annotations
 
@@ -356,3 +358,96 @@ def make_inputs(w: Workload, seed: int = 0, batch: int | None = None,
 
 def with_batch(w: Workload, batch: int) -> Workload:
     return replace(w, batch=batch)
+
+
+# --------------------------------------------------------------------------
+# observation encoder (images -> the visual part of an observation token)
+# --------------------------------------------------------------------------
+@dataclass(frozen=True)
+class EncoderShape:
+    """A ResNet-18-topology image encoder with GroupNorm and global average
+    pooling: a 7x7 stride-2 stem convolution, 3x3 stride-2 max pooling, then
+    stages of basic blocks (two 3x3 convolutions and a shortcut; the first
+    block of stages 2.. halves the resolution and projects the shortcut with
+    a 1x1 stride-2 convolution).  GroupNorm uses groups of `gn_group`
+    channels.  Images are NHWC [N][height][width][in_ch]."""
+    height: int
+    width: int
+    in_ch: int = 3
+    stem_ch: int = 64
+    widths: Tuple[int, ...] = (64, 128, 256, 512)
+    blocks: Tuple[int, ...] = (2, 2, 2, 2)
+    gn_group: int = 16
+
+    @property
+    def out_dim(self) -> int:
+        return self.widths[-1]
+
+
+ENC_PUSHT = EncoderShape(96, 96)                # Push-T camera images
+ENC_ROBOMIMIC = EncoderShape(84, 84)            # RoboMimic camera images
+ENC_TINY = EncoderShape(20, 20, stem_ch=16, widths=(16, 32, 32, 64), blocks=(1, 1, 1, 1), gn_group=8)
+
+
+def encoder_layout(e: EncoderShape) -> List[Tuple[str, Tuple[int, ...], str]]:
+    """Flat parameter order: (name, shape, kind), kind 'conv' ([out][kh][kw][in])
+    or 'gn_g' / 'gn_b'.  Blocks are named s<stage>b<block>: conv a, conv b and,
+    where the shortcut changes shape, conv d."""
+    out: List[Tuple[str, Tuple[int, ...], str]] = [
+        ("stem", (e.stem_ch, 7, 7, e.in_ch), "conv"),
+        ("stem_g", (e.stem_ch,), "gn_g"), ("stem_b", (e.stem_ch,), "gn_b")]
+    cin = e.stem_ch
+    for si, (c, nb) in enumerate(zip(e.widths, e.blocks)):
+        for bi in range(nb):
+            p = f"s{si}b{bi}."
+            stride = 2 if (si > 0 and bi == 0) else 1
+            out += [(p + "a", (c, 3, 3, cin), "conv"), (p + "a_g", (c,), "gn_g"), (p + "a_b", (c,), "gn_b"),
+                    (p + "b", (c, 3, 3, c), "conv"), (p + "b_g", (c,), "gn_g"), (p + "b_b", (c,), "gn_b")]
+            if stride != 1 or cin != c:
+                out += [(p + "d", (c, 1, 1, cin), "conv"), (p + "d_g", (c,), "gn_g"), (p + "d_b", (c,), "gn_b")]
+            cin = c
+    return out
+
+
+def n_encoder_floats(e: EncoderShape) -> int:
+    return int(sum(int(np.prod(shp)) for _, shp, _ in encoder_layout(e)))
+
+
+def make_encoder_weights(e: EncoderShape, seed: int = 0, variant: str = "default") -> np.ndarray:
+    """Flat float32 encoder parameters (seed stream [seed, 5]): convolution
+    weights N(0, 2 / fan_in); GroupNorm gain 1 and shift 0, or with
+    'perturbed' gain 1 + N(0, 0.1^2) and shift N(0, 0.1^2)."""
+    rng = np.random.default_rng([seed, 5])
+    out = np.empty(n_encoder_floats(e), np.float32)
+    off = 0
+    for _, shp, kind in encoder_layout(e):
+        n = int(np.prod(shp))
+        v = out[off:off + n]
+        off += n
+        if kind == "conv":
+            rng.standard_normal(out=v, dtype=np.float32)
+            v *= np.float32(np.sqrt(2.0 / (shp[1] * shp[2] * shp[3])))
+        elif variant == "default":
+            v[:] = 1.0 if kind == "gn_g" else 0.0
+        else:
+            rng.standard_normal(out=v, dtype=np.float32)
+            v *= np.float32(0.1)
+            if kind == "gn_g":
+                v += np.float32(1.0)
+    return out
+
+
+def split_encoder_weights(e: EncoderShape, flat: np.ndarray) -> Dict[str, np.ndarray]:
+    out, off = {}, 0
+    for name, shp, _ in encoder_layout(e):
+        n = int(np.prod(shp))
+        out[name] = flat[off:off + n].reshape(shp)
+        off += n
+    assert off == flat.size
+    return out
+
+
+def make_images(e: EncoderShape, batch: int, seed: int = 0) -> np.ndarray:
+    """[batch][height][width][in_ch] float32 in [0, 1) (seed stream [seed, 6])."""
+    rng = np.random.default_rng([seed, 6])
+    return rng.random((batch, e.height, e.width, e.in_ch), dtype=np.float32)
