@@ -372,6 +372,68 @@ int evo_debug_read_cache(evo_policy* p, int32_t unit, int32_t sample, float* hos
  * the policy's device first. */
 void evo_destroy_policy(evo_policy* p);
 
+/* ---- Observation encoder --------------------------------------------
+ * The image policies turn camera frames into observation features with a
+ * pretrained encoder that the method leaves unchanged (Sec. 3.1, Sec. 3.4;
+ * the appendix's wall-clock table times action generation with visual
+ * encoding included).  The paper prints no architecture; this library
+ * builds a ResNet-18-topology network with GroupNorm in place of
+ * BatchNorm and global average pooling, no final linear layer:
+ *   stem: conv 7x7 stride 2 (pad 3), GroupNorm, ReLU, max pool 3x3 stride 2
+ *   (pad 1); stage s (0-based), block b: y = ReLU(GN(conv3x3(ReLU(GN(
+ *   conv3x3_stride(x))))) + sc(x)), stride 2 for b == 0 and s > 0,
+ *   sc = GN(conv1x1_stride(x)) where the stride or width changes, else x;
+ *   features = mean over the final map's pixels.
+ * Convolutions have no bias; GroupNorm: groups of gn_group consecutive
+ * channels, population variance over the group's channels and pixels,
+ * eps 1e-5, per-channel gain and shift. */
+typedef struct {
+  int32_t height, width; /* image size, 8 .. 4096 */
+  int32_t in_ch;         /* image channels, 1 .. 64 */
+  int32_t stem_ch;       /* stem width, a multiple of 8 and of gn_group */
+  int32_t n_stages;      /* 1 .. 4 */
+  int32_t widths[4];     /* stage widths, multiples of 8 and of gn_group, <= 4096 */
+  int32_t blocks[4];     /* basic blocks per stage, 1 .. 16 */
+  int32_t gn_group;      /* channels per GroupNorm group */
+  int32_t dtype;         /* EVO_BF16: convolution operands rounded to bf16
+                            (fp32 accumulation); EVO_FP32: fp32 operands */
+  int32_t max_batch;     /* largest batch of evo_encode, 1 .. 65536 */
+} evo_encoder_desc;
+
+typedef struct evo_encoder evo_encoder;
+
+/* Number of floats of the encoder's flat parameter array, or a negative
+ * EVO_E_* code.  Order: "stem" conv [stem_ch][7][7][in_ch], its GroupNorm
+ * gain [stem_ch] and shift [stem_ch]; then per stage and block: conv a
+ * [c][3][3][cin], gain, shift; conv b [c][3][3][c], gain, shift; and where
+ * the shortcut is projected, conv d [c][1][1][cin], gain, shift.  Host-only. */
+int64_t evo_encoder_weight_count(const evo_encoder_desc* desc);
+
+/* Build an encoder on the current HIP device.  host_weights: host float
+ * [n_floats] in the order above (copied; the caller keeps ownership).
+ * Allocates the packed weights and activation buffers for max_batch images.
+ * Errors: EVO_E_INVALID (desc, n_floats, image too small for the network),
+ * EVO_E_UNSUPPORTED, EVO_E_NOMEM, EVO_E_HIP.  On error *out is untouched. */
+int evo_create_encoder(const evo_encoder_desc* desc, const float* host_weights, size_t n_floats,
+                       evo_encoder** out);
+
+/* Encode `batch` images.  images: device float [batch][height][width]
+ * [in_ch] (NHWC), read only.  features_out: device float, row n at
+ * features_out + n * out_stride holds widths[n_stages-1] features (so
+ * features can be written straight into a policy's observation rows);
+ * other elements are not touched.  Asynchronous on hip_stream (NULL = the
+ * null stream); uses the encoder's activation buffers, so calls on one
+ * encoder must not overlap. */
+int evo_encode(evo_encoder* e, int32_t batch, const float* images, float* features_out, int32_t out_stride,
+               void* hip_stream);
+
+/* Convolution FLOPs of one evo_encode of `batch` images (2 per
+ * multiply-add; normalisation and pooling not counted).  Host-only. */
+int evo_encoder_flops(const evo_encoder* e, int32_t batch, uint64_t* flops_out);
+
+/* Release the encoder (NULL is a no-op); synchronises its device first. */
+void evo_destroy_encoder(evo_encoder* e);
+
 /* Thread-local message of the last failed call on this thread. */
 const char* evo_last_error(void);
 

@@ -13,7 +13,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libevo.so")
-SOURCES = ["evo_host.cpp", "evo_ga.cpp", "evo_kernels.hip", "evo_redundancy.hip", "evo_search.hip", "evo_api.hip"]
+SOURCES = ["evo_host.cpp", "evo_ga.cpp", "evo_kernels.hip", "evo_redundancy.hip", "evo_search.hip", "evo_encoder.hip",
+           "evo_api.hip"]
 ARCH = os.environ.get("EVO_OFFLOAD_ARCH", "gfx950")
 
 

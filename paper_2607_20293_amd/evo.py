@@ -25,7 +25,8 @@ EXPORTED = ("evo_weight_count", "evo_check_desc", "evo_create_policy", "evo_set_
             "evo_schedule_codes", "evo_debug_read_cache", "evo_synchronize", "evo_destroy_policy",
             "evo_last_error", "evo_collect_activations", "evo_redundancy_scores", "evo_guided_probabilities",
             "evo_guided_sample", "evo_ga_initial_population", "evo_ga_next_generation", "evo_ga_search",
-            "evo_search")
+            "evo_search", "evo_encoder_weight_count", "evo_create_encoder", "evo_encode", "evo_encoder_flops",
+            "evo_destroy_encoder")
 
 
 def guided_probabilities(scores, eps: float, gamma: float) -> np.ndarray:
@@ -241,6 +242,16 @@ def lib() -> ctypes.CDLL:
         L.evo_synchronize.restype = ctypes.c_int
         L.evo_destroy_policy.argtypes = [P]
         L.evo_destroy_policy.restype = None
+        L.evo_encoder_weight_count.argtypes = [ctypes.POINTER(EncoderDesc)]
+        L.evo_encoder_weight_count.restype = ctypes.c_int64
+        L.evo_create_encoder.argtypes = [ctypes.POINTER(EncoderDesc), P, ctypes.c_size_t, ctypes.POINTER(P)]
+        L.evo_create_encoder.restype = ctypes.c_int
+        L.evo_encode.argtypes = [P, I32, P, P, I32, P]
+        L.evo_encode.restype = ctypes.c_int
+        L.evo_encoder_flops.argtypes = [P, I32, ctypes.POINTER(U64)]
+        L.evo_encoder_flops.restype = ctypes.c_int
+        L.evo_destroy_encoder.argtypes = [P]
+        L.evo_destroy_encoder.restype = None
         L.evo_last_error.argtypes = []
         L.evo_last_error.restype = ctypes.c_char_p
         _lib = L
@@ -435,3 +446,78 @@ class Policy:
         buf = np.zeros((self.shape.horizon, self.shape.d_model), np.float32)
         _check(lib().evo_debug_read_cache(self._h, unit, sample, buf.ctypes.data))
         return buf
+
+
+class EncoderDesc(ctypes.Structure):
+    _fields_ = [("height", ctypes.c_int32), ("width", ctypes.c_int32), ("in_ch", ctypes.c_int32),
+                ("stem_ch", ctypes.c_int32), ("n_stages", ctypes.c_int32), ("widths", ctypes.c_int32 * 4),
+                ("blocks", ctypes.c_int32 * 4), ("gn_group", ctypes.c_int32), ("dtype", ctypes.c_int32),
+                ("max_batch", ctypes.c_int32)]
+
+
+def make_encoder_desc(e, dtype: str = "bf16", max_batch: int = 1) -> EncoderDesc:
+    """e: an encoder shape with height, width, in_ch, stem_ch, widths, blocks,
+    gn_group (at most 4 stages)."""
+    n = len(e.widths)
+    if n != len(e.blocks) or not 1 <= n <= 4:
+        raise ValueError("widths and blocks must have the same length, 1 to 4")
+    w = (ctypes.c_int32 * 4)(*(list(e.widths) + [0] * (4 - n)))
+    b = (ctypes.c_int32 * 4)(*(list(e.blocks) + [0] * (4 - n)))
+    return EncoderDesc(e.height, e.width, e.in_ch, e.stem_ch, n, w, b, e.gn_group,
+                       EVO_BF16 if dtype == "bf16" else EVO_FP32, max_batch)
+
+
+def encoder_weight_count(desc: EncoderDesc) -> int:
+    n = lib().evo_encoder_weight_count(ctypes.byref(desc))
+    if n < 0:
+        _check(int(n))
+    return int(n)
+
+
+class Encoder:
+    """A created observation encoder on the current HIP device (see
+    include/evo.h)."""
+
+    def __init__(self, e, weights: np.ndarray, dtype: str = "bf16", max_batch: int = 1):
+        self.shape = e
+        self.out_dim = int(e.widths[-1])
+        self.desc = make_encoder_desc(e, dtype, max_batch)
+        w = np.ascontiguousarray(weights, dtype=np.float32)
+        h = ctypes.c_void_p()
+        _check(lib().evo_create_encoder(ctypes.byref(self.desc), w.ctypes.data, w.size, ctypes.byref(h)))
+        self._h = h
+
+    def close(self):
+        if getattr(self, "_h", None):
+            lib().evo_destroy_encoder(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def encode(self, images, out=None, stream=None):
+        """images: float32 HIP tensor [B][height][width][in_ch].  out: None, or
+        a float32 HIP tensor [B][out_dim] whose rows may be strided (e.g. a
+        column slice of the policy's observation rows).  Returns out."""
+        import torch
+        e = self.shape
+        B = int(images.shape[0])
+        pi = _dev_ptr(images, "float32", (B, e.height, e.width, e.in_ch))
+        if out is None:
+            out = torch.empty((B, self.out_dim), dtype=torch.float32, device=images.device)
+        if not isinstance(out, torch.Tensor) or not out.is_cuda or out.dtype != torch.float32:
+            raise TypeError("out must be a float32 HIP tensor")
+        if tuple(out.shape) != (B, self.out_dim) or out.stride(1) != 1 or (B > 1 and out.stride(0) < self.out_dim):
+            raise ValueError(f"out must be [{B}][{self.out_dim}] with unit column stride")
+        row = out.stride(0) if B > 1 else self.out_dim
+        st = torch.cuda.current_stream(images.device) if stream is None else stream
+        _check(lib().evo_encode(self._h, B, pi, out.data_ptr(), row, ctypes.c_void_p(st.cuda_stream)))
+        return out
+
+    def flops(self, batch: int) -> int:
+        v = ctypes.c_uint64()
+        _check(lib().evo_encoder_flops(self._h, batch, ctypes.byref(v)))
+        return int(v.value)

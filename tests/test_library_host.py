@@ -210,3 +210,29 @@ def test_fixed_interval_and_blockwise_families():
         st2 = evo.schedule_stats(desc, [blk], np.zeros(1, np.int32), evo.GRAN_UNIT)
         assert st2["flops_cacheable"] == st["flops_cacheable"]
     assert I.lattice_fixed_interval(2, 100, 8)[0].nonzero()[0].tolist() == [0, 12, 25, 37, 50, 62, 75, 87]
+
+
+@pytest.mark.parametrize("shape", [I.ENC_TINY, I.ENC_PUSHT, I.ENC_ROBOMIMIC])
+def test_encoder_weight_count_matches_layout(shape):
+    _lib_or_skip()
+    assert evo.encoder_weight_count(evo.make_encoder_desc(shape, "bf16", 4)) == I.n_encoder_floats(shape)
+
+
+def test_encoder_descriptor_validation():
+    _lib_or_skip()
+    L = evo.lib()
+    import ctypes
+
+    def count(**kw):
+        d = evo.make_encoder_desc(I.ENC_PUSHT, "bf16", 4)
+        for k, v in kw.items():
+            setattr(d, k, v)
+        return int(L.evo_encoder_weight_count(ctypes.byref(d)))
+
+    assert count() == I.n_encoder_floats(I.ENC_PUSHT)
+    assert count(gn_group=24) == -1          # widths not multiples of the group
+    assert count(n_stages=0) == -1
+    assert count(height=4) == -1
+    assert count(dtype=3) == -1
+    assert count(max_batch=0) == -1
+    assert count(max_batch=60000, height=4096, width=4096) == -5   # pixel indices beyond 32 bits
