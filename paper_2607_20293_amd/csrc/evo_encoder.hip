@@ -4,12 +4,19 @@
 //
 // Activations are NHWC fp32 in HBM.  Convolutions are implicit GEMMs on
 // MFMA: M = output pixels, N = output channels, K = kh * kw * Cin in
-// (kh, kw, Cin) order, which is the packed weight layout [Cout][K] (padded
-// to the K step).  The A tile is gathered from the input with the
-// convolution's padding on the fly (no im2col buffer) and converted to the
-// operand type in LDS.  GroupNorm is a statistics pass (per image and group,
-// fp32 partial sums reduced in fp64) and an elementwise pass that applies
-// the affine, the optional residual and ReLU.
+// (kh, kw, Cin) order, which is the packed weight layout [Cout][Kp] (K
+// padded to the K step).  The A tile is gathered from the input with the
+// convolution's padding on the fly (no im2col buffer), converted to the
+// operand type and double-buffered in LDS with the next step's global loads
+// in flight during the current step's MFMAs.  Layers with few output tiles
+// (small batches, late stages) split K over workgroups into partial
+// outputs that the GroupNorm statistics pass sums in a fixed order.
+//
+// GroupNorm is two passes per layer: partial statistics over pixel chunks
+// (shifted sums, fp64 across threads and chunks), then an apply pass that
+// adds the residual and ReLU and, where the network pools next, does the
+// pooling itself: 3x3/2 max pooling after the stem, global average pooling
+// after the last block (the last block's output is never stored).
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -27,246 +34,413 @@ namespace {
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 
-constexpr int kBM = 64, kBN = 64, kThreads = 256;
+constexpr int kThreads = 256;
+constexpr int kTargetWG = 512;      // split K below this many output tiles
+constexpr int kMaxSplit = 16;
+constexpr long long kWsFloats = 1024ll * 4096;  // split-K partials (>= splits * tiles * 64 * 64)
+constexpr int kGnTarget = 1024;     // GroupNorm workgroups aimed at when chunking pixels
+constexpr int kMaxPart = 16 * 1024; // partial statistics beyond one per (image, group)
 
-template <class AT> struct ConvOp;
-template <> struct ConvOp<__bf16> {
-  static constexpr int KS = 32;  // K per step: one 16x16x32 MFMA per tile
+template <class AT> struct ConvStep;
+template <> struct ConvStep<__bf16> {
+  static constexpr int KS = 64;  // K per stage: two 16x16x32 MFMAs per tile
 };
-template <> struct ConvOp<float> {
-  static constexpr int KS = 16;  // K per step: four 16x16x4 MFMAs per tile
+template <> struct ConvStep<float> {
+  static constexpr int KS = 32;  // K per stage: eight 16x16x4 MFMAs per tile
 };
-
-__device__ __forceinline__ void put(__bf16* p, float v) { *p = (__bf16)v; }
-__device__ __forceinline__ void put(float* p, float v) { *p = v; }
 
 struct ConvArgs {
-  const float* x;   // [N][H][W][Cin]
-  const void* w;    // [Cout][Kp] operand type
-  float* y;         // [N][Ho][Wo][Cout]
-  int N, H, W, Cin, Ho, Wo, Cout, kh, kw, stride, pad, K, Kp;
+  const float* x;    // [N][H][W][Cin]
+  const void* w;     // [Cout][Kp] operand type
+  float* y;          // [N][Ho][Wo][Cout], or split z at y + z * split_stride
+  int H, W, Cin, Ho, Wo, Cout, kw, stride, pad, K, Kp;
+  int M, mt, nt, splits, spp;  // pixels, tile counts, K splits, K steps per split
+  long long split_stride;
 };
 
-// One 64 x 64 output tile per workgroup; wave (wm, wn) owns a 32 x 32 quarter
-// as 2 x 2 MFMA tiles.  Thread t stages A row t / 4 (one output pixel) and B
-// row t / 4 (one output channel), 8 consecutive K elements each.
-template <class AT>
+// Maps a workgroup to a logical tile so that the workgroups of one XCD
+// (blockIdx % 8) take a contiguous range of logical ids: neighbouring tiles
+// that share input pixels or weights then meet in the same L2.
+__device__ __forceinline__ int xcd_linear(int b, int total) {
+  const int per = total >> 3, rem = total & 7, xcd = b & 7, slot = b >> 3;
+  return xcd < rem ? xcd * (per + 1) + slot : rem * (per + 1) + (xcd - rem) * per + slot;
+}
+
+// Block tile BM x BN, 4 waves as 2 x 2, wave tile (BM/2) x (BN/2) of 16x16
+// MFMA tiles.  Thread t stages chunk t % 4 (SEG = KS / 4 consecutive K) of
+// rows t / 4 + p * 64 of the A (pixels) and B (output channels) tiles.
+template <class AT, int BM, int BN>
 __global__ void __launch_bounds__(kThreads) conv_kernel(const ConvArgs a) {
-  constexpr int KS = ConvOp<AT>::KS, LDK = KS + 8;
-  __shared__ __attribute__((aligned(16))) AT As[kBM * LDK];
-  __shared__ __attribute__((aligned(16))) AT Bs[kBN * LDK];
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int wm = w >> 1, wn = w & 1;
-  const int M = a.N * a.Ho * a.Wo;
-  const int m0 = blockIdx.x * kBM, n0 = blockIdx.y * kBN;
-  // the staged A row: output pixel (n, oh, ow)
-  const int ar = tid >> 2, aseg = (tid & 3) * (KS / 4);
-  const int pm = m0 + ar;
-  const bool prow = pm < M;
-  int pn = 0, poh = 0, pow_ = 0;
-  if (prow) {
-    pn = pm / (a.Ho * a.Wo);
-    const int r = pm - pn * a.Ho * a.Wo;
-    poh = r / a.Wo;
-    pow_ = r - poh * a.Wo;
+  constexpr int KS = ConvStep<AT>::KS, LDK = KS + 8, SEG = KS / 4, CPR = 4, RPP = kThreads / CPR;
+  constexpr int PA = BM / RPP, PB = BN / RPP, MI = BM / 32, NJ = BN / 32;
+  constexpr int BV = SEG * (int)sizeof(AT) / 16;  // 16-byte loads per B chunk
+  static_assert(BM % RPP == 0 && BN % RPP == 0, "tile rows must be a multiple of the staging rows");
+  __shared__ __attribute__((aligned(16))) AT As[2][BM * LDK];
+  __shared__ __attribute__((aligned(16))) AT Bs[2][BN * LDK];
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, wm = wv >> 1, wn = wv & 1;
+  const int lr = lane & 15, lq = lane >> 4;
+
+  const int id = xcd_linear(blockIdx.x, a.mt * a.nt * a.splits);
+  const int nti = id % a.nt, rest = id / a.nt, mti = rest % a.mt, z = rest / a.mt;
+  const int m0 = mti * BM, n0 = nti * BN;
+  const int steps = a.Kp / KS;
+  const int s_begin = z * a.spp, s_end = min(steps, s_begin + a.spp);
+
+  const int chunk = tid % CPR, row0 = tid / CPR;
+  // the A rows this thread stages: output pixel -> image base and window origin
+  // (rlo, rhi: the part of a kernel row of kw * Cin contiguous K elements
+  // that falls inside the image horizontally)
+  const float* xb[PA];
+  int ih0[PA], iw0[PA], rlo[PA], rhi[PA];
+  bool pv[PA];
+#pragma unroll
+  for (int p = 0; p < PA; ++p) {
+    const int pm = m0 + row0 + p * RPP;
+    pv[p] = pm < a.M;
+    const int hw = a.Ho * a.Wo;
+    const int pn = pv[p] ? pm / hw : 0;
+    const int r = pv[p] ? pm - pn * hw : 0;
+    const int oh = r / a.Wo, ow = r - oh * a.Wo;
+    xb[p] = a.x + (size_t)pn * a.H * a.W * a.Cin;
+    ih0[p] = oh * a.stride - a.pad;
+    iw0[p] = ow * a.stride - a.pad;
+    rlo[p] = max(0, -iw0[p]) * a.Cin;
+    rhi[p] = min(a.kw, a.W - iw0[p]) * a.Cin;
   }
-  const int ih0 = poh * a.stride - a.pad, iw0 = pow_ * a.stride - a.pad;
-  const float* xn = a.x + (size_t)pn * a.H * a.W * a.Cin;
-  // the staged B row: output channel n0 + ar
-  const int bc = n0 + ar;
-  const AT* wrow = reinterpret_cast<const AT*>(a.w) + (size_t)(bc < a.Cout ? bc : 0) * a.Kp;
-  const bool vec = (a.Cin % (KS / 4)) == 0;  // the thread's K run stays inside one input pixel
+  const AT* wb[PB];
+  bool bv[PB];
+#pragma unroll
+  for (int p = 0; p < PB; ++p) {
+    const int c = n0 + row0 + p * RPP;
+    bv[p] = c < a.Cout;
+    wb[p] = reinterpret_cast<const AT*>(a.w) + (size_t)(bv[p] ? c : 0) * a.Kp + chunk * SEG;
+  }
+  const bool vec = (a.Cin % SEG) == 0;  // a chunk then lies inside one input pixel
 
-  f32x4 acc[2][2];
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int j = 0; j < 2; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  // one K step of staged operands
+  struct Regs {
+    float a[PA][SEG];
+    uint4 b[PB][BV];
+  };
 
-  for (int k0 = 0; k0 < a.Kp; k0 += KS) {
-    // ---- stage A: KS / 4 consecutive K of this pixel
-    {
-      AT* dst = As + ar * LDK + aseg;
-      const int kk = k0 + aseg;
-      if (vec) {
-        float v[KS / 4];
+  auto load = [&](Regs& rg, int s) {
+    const int kk = s * KS + chunk * SEG;
+    if (vec) {
+      const int c = kk % a.Cin, pix = kk / a.Cin, ka = pix / a.kw, kb = pix - ka * a.kw;
 #pragma unroll
-        for (int q = 0; q < KS / 4; ++q) v[q] = 0.f;
-        if (prow && kk < a.K) {
-          const int c = kk % a.Cin, ab = kk / a.Cin;
-          const int kb = ab % a.kw, ka = ab / a.kw;
-          const int ih = ih0 + ka, iw = iw0 + kb;
-          if (ih >= 0 && ih < a.H && iw >= 0 && iw < a.W) {
-            const f32x4* src = reinterpret_cast<const f32x4*>(xn + ((size_t)ih * a.W + iw) * a.Cin + c);
+      for (int p = 0; p < PA; ++p) {
+        const int ih = ih0[p] + ka, iw = iw0[p] + kb;
+        if (pv[p] && kk < a.K && ih >= 0 && ih < a.H && iw >= 0 && iw < a.W) {
+          const f32x4* src = reinterpret_cast<const f32x4*>(xb[p] + ((size_t)ih * a.W + iw) * a.Cin + c);
 #pragma unroll
-            for (int q = 0; q < KS / 16; ++q) {
-              const f32x4 t = src[q];
-              v[4 * q] = t[0];
-              v[4 * q + 1] = t[1];
-              v[4 * q + 2] = t[2];
-              v[4 * q + 3] = t[3];
-            }
+          for (int q = 0; q < SEG / 4; ++q) {
+            const f32x4 t = src[q];
+            rg.a[p][4 * q] = t[0];
+            rg.a[p][4 * q + 1] = t[1];
+            rg.a[p][4 * q + 2] = t[2];
+            rg.a[p][4 * q + 3] = t[3];
           }
-        }
+        } else {
 #pragma unroll
-        for (int q = 0; q < KS / 4; ++q) put(dst + q, v[q]);
-      } else {
-#pragma unroll
-        for (int q = 0; q < KS / 4; ++q) {
-          const int k = kk + q;
-          float v = 0.f;
-          if (prow && k < a.K) {
-            const int c = k % a.Cin, ab = k / a.Cin;
-            const int kb = ab % a.kw, ka = ab / a.kw;
-            const int ih = ih0 + ka, iw = iw0 + kb;
-            if (ih >= 0 && ih < a.H && iw >= 0 && iw < a.W) v = xn[((size_t)ih * a.W + iw) * a.Cin + c];
-          }
-          put(dst + q, v);
-        }
-      }
-    }
-    // ---- stage B: KS / 4 consecutive K of this output channel (zero padded in memory)
-    {
-      AT* dst = Bs + ar * LDK + aseg;
-      if (bc < a.Cout) {
-        const AT* src = wrow + k0 + aseg;
-#pragma unroll
-        for (int q = 0; q < KS / 4; ++q) dst[q] = src[q];
-      } else {
-#pragma unroll
-        for (int q = 0; q < KS / 4; ++q) put(dst + q, 0.f);
-      }
-    }
-    __syncthreads();
-    const int lr = lane & 15, lq = lane >> 4;
-    if constexpr (sizeof(AT) == 2) {
-#pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        const uint4 av = *reinterpret_cast<const uint4*>(As + (wm * 32 + i * 16 + lr) * LDK + lq * 8);
-#pragma unroll
-        for (int j = 0; j < 2; ++j) {
-          const uint4 bv = *reinterpret_cast<const uint4*>(Bs + (wn * 32 + j * 16 + lr) * LDK + lq * 8);
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, av),
-                                                              __builtin_bit_cast(bf16x8_t, bv), acc[i][j], 0, 0, 0);
+          for (int q = 0; q < SEG; ++q) rg.a[p][q] = 0.f;
         }
       }
     } else {
+      // walk the chunk along kernel rows: K element (ka, r) sits at input
+      // row ih0 + ka, offset iw0 * Cin + r of that row
+      const int rowlen = a.kw * a.Cin, ka0 = kk / rowlen, r0 = kk - ka0 * rowlen;
 #pragma unroll
-      for (int s4 = 0; s4 < 4; ++s4)
+      for (int p = 0; p < PA; ++p) {
+        int ka = ka0, r = r0;
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {
-          const float av = As[(wm * 32 + i * 16 + lr) * LDK + s4 * 4 + lq];
-#pragma unroll
-          for (int j = 0; j < 2; ++j) {
-            const float bv = Bs[(wn * 32 + j * 16 + lr) * LDK + s4 * 4 + lq];
-            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv, acc[i][j], 0, 0, 0);
+        for (int q = 0; q < SEG; ++q) {
+          const int ih = ih0[p] + ka;
+          float v = 0.f;
+          if (pv[p] && kk + q < a.K && ih >= 0 && ih < a.H && r >= rlo[p] && r < rhi[p])
+            v = xb[p][((long long)ih * a.W + iw0[p]) * a.Cin + r];
+          rg.a[p][q] = v;
+          if (++r == rowlen) {
+            r = 0;
+            ++ka;
           }
         }
+      }
     }
+#pragma unroll
+    for (int p = 0; p < PB; ++p) {
+      const uint4* src = reinterpret_cast<const uint4*>(wb[p] + (size_t)s * KS);
+#pragma unroll
+      for (int q = 0; q < BV; ++q) rg.b[p][q] = bv[p] ? src[q] : uint4{0u, 0u, 0u, 0u};
+    }
+  };
+  auto store = [&](const Regs& rg, int buf) {
+#pragma unroll
+    for (int p = 0; p < PA; ++p) {
+      AT* dst = As[buf] + (row0 + p * RPP) * LDK + chunk * SEG;
+      if constexpr (sizeof(AT) == 2) {
+#pragma unroll
+        for (int h = 0; h < SEG / 8; ++h) {
+          bf16x8_t t;
+#pragma unroll
+          for (int q = 0; q < 8; ++q) t[q] = (__bf16)rg.a[p][8 * h + q];
+          *reinterpret_cast<bf16x8_t*>(dst + 8 * h) = t;
+        }
+      } else {
+#pragma unroll
+        for (int h = 0; h < SEG / 4; ++h)
+          *reinterpret_cast<f32x4*>(dst + 4 * h) =
+              f32x4{rg.a[p][4 * h], rg.a[p][4 * h + 1], rg.a[p][4 * h + 2], rg.a[p][4 * h + 3]};
+      }
+    }
+#pragma unroll
+    for (int p = 0; p < PB; ++p) {
+      uint4* dst = reinterpret_cast<uint4*>(Bs[buf] + (row0 + p * RPP) * LDK + chunk * SEG);
+#pragma unroll
+      for (int q = 0; q < BV; ++q) dst[q] = rg.b[p][q];
+    }
+  };
+
+  f32x4 acc[MI][NJ];
+#pragma unroll
+  for (int i = 0; i < MI; ++i)
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  auto compute = [&](int buf) {
+    const AT* A = As[buf] + (wm * (BM / 2) + lr) * LDK;
+    const AT* B = Bs[buf] + (wn * (BN / 2) + lr) * LDK;
+    if constexpr (sizeof(AT) == 2) {
+#pragma unroll
+      for (int kk = 0; kk < KS / 32; ++kk) {
+        bf16x8_t af[MI], bf[NJ];
+#pragma unroll
+        for (int i = 0; i < MI; ++i) af[i] = *reinterpret_cast<const bf16x8_t*>(A + i * 16 * LDK + kk * 32 + lq * 8);
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) bf[j] = *reinterpret_cast<const bf16x8_t*>(B + j * 16 * LDK + kk * 32 + lq * 8);
+#pragma unroll
+        for (int i = 0; i < MI; ++i)
+#pragma unroll
+          for (int j = 0; j < NJ; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bf[j], acc[i][j], 0, 0, 0);
+      }
+    } else {
+#pragma unroll
+      for (int k4 = 0; k4 < KS / 4; ++k4) {
+        float af[MI], bf[NJ];
+#pragma unroll
+        for (int i = 0; i < MI; ++i) af[i] = A[i * 16 * LDK + k4 * 4 + lq];
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) bf[j] = B[j * 16 * LDK + k4 * 4 + lq];
+#pragma unroll
+        for (int i = 0; i < MI; ++i)
+#pragma unroll
+          for (int j = 0; j < NJ; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(af[i], bf[j], acc[i][j], 0, 0, 0);
+      }
+    }
+  };
+
+  // Step i computes from LDS buffer i % 2 while the loads of step i + 1 are
+  // in flight; they go to the other buffer, which step i - 1 read before the
+  // barrier that ended it.  (A second register set for two steps of slack
+  // costs occupancy and measured slower.)
+  const int n = s_end - s_begin;
+  Regs r;
+  if (n > 0) {
+    load(r, s_begin);
+    store(r, 0);
+  }
+  __syncthreads();
+  for (int i = 0; i < n; ++i) {
+    const bool more = i + 1 < n;
+    if (more) load(r, s_begin + i + 1);
+    compute(i & 1);
+    if (more) store(r, (i & 1) ^ 1);
     __syncthreads();
   }
-  // ---- D: lane holds rows 4 * (lane / 16) + r of column lane % 16 of each tile
-  const int lr = lane & 15, lq = lane >> 4;
+  // D: lane holds rows 4 * (lane / 16) + r of column lane % 16 of each tile
+  float* y = a.y + (long long)z * a.split_stride;
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < MI; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int col = n0 + wn * 32 + j * 16 + lr;
+    for (int j = 0; j < NJ; ++j) {
+      const int col = n0 + wn * (BN / 2) + j * 16 + lr;
       if (col >= a.Cout) continue;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int row = m0 + wm * 32 + i * 16 + lq * 4 + r;
-        if (row < M) a.y[(size_t)row * a.Cout + col] = acc[i][j][r];
+        const int row = m0 + wm * (BM / 2) + i * 16 + lq * 4 + r;
+        if (row < a.M) y[(size_t)row * a.Cout + col] = acc[i][j][r];
       }
     }
 }
 
-// GroupNorm statistics: one workgroup per (image, group); mean and 1/sqrt(var + eps)
-__global__ void __launch_bounds__(256) gn_stats_kernel(const float* __restrict__ x, int HW, int C, int G,
-                                                       float eps, float2* __restrict__ stats) {
-  const int ng = blockIdx.x, groups = C / G;
-  const int n = ng / groups, g = ng % groups;
-  const float* base = x + (size_t)n * HW * C + (size_t)g * G;
-  // sums of (x - x0) with x0 the group's first element, so that a mean far
-  // from zero does not cancel the variance
-  const float x0 = base[0];
-  float s = 0.f, q = 0.f;
-  for (int e = threadIdx.x; e < HW * G; e += 256) {
-    const int p = e / G, c = e - p * G;
-    const float v = base[(size_t)p * C + c] - x0;
-    s += v;
-    q += v * v;
+enum { GN_PLAIN = 0, GN_MAXPOOL = 1, GN_AVGPOOL = 2 };
+
+struct GnArgs {
+  const float* ws;   // split-K partials (splits > 1): x = sum over z of ws[z * split_stride + i]
+  int splits;
+  long long split_stride;
+  float* x;          // conv output [N][HW][C] (written by the statistics pass when splits > 1)
+  const float* gamma;
+  const float* beta;
+  const float* res;  // residual [N][HW][C] or NULL
+  float* y;          // PLAIN: [N][HW][C] (may be x); MAXPOOL: [N][Hp][Wp][C]; AVGPOOL: out + n * out_stride
+  double2* part;     // [N][groups][ps_stats] shifted (sum, sum of squares)
+  float* shift;      // [N][groups] the shift x0 (read before the apply pass may overwrite x in place)
+  int relu, mode, H, W, C, G, gpw, ps_stats, ps_apply, Hp, Wp, out_stride;
+  float eps;
+};
+
+// Statistics pass: workgroup (image n, channel chunk of gpw groups, pixel
+// chunk); thread t reads float4 column t % Q of pixel rows t / Q + i * RP.
+// Sums are of (x - x0), x0 the group's first element, so that a mean far
+// from zero does not cancel the variance.
+__global__ void __launch_bounds__(kThreads) gn_stats_kernel(const GnArgs a) {
+  const int HW = a.H * a.W, CW = a.G * a.gpw, Q = CW >> 2, RP = kThreads / Q;
+  const int chunks = a.C / CW, groups = a.C / a.G;
+  const int pi = blockIdx.x % a.ps_stats, rest = blockIdx.x / a.ps_stats;
+  const int ch = rest % chunks, n = rest / chunks;
+  const int tid = threadIdx.x, col = tid % Q, prow = tid / Q;
+  const int c = ch * CW + col * 4, j = (col * 4) / a.G;
+  const size_t base = (size_t)n * HW * a.C;
+  const int pc = (HW + a.ps_stats - 1) / a.ps_stats, p0 = pi * pc, p1 = min(HW, p0 + pc);
+  const bool split = a.splits > 1;
+
+  float x0;
+  {
+    const size_t i0 = base + ch * CW + j * a.G;
+    if (!split) {
+      x0 = a.x[i0];
+    } else {
+      x0 = a.ws[i0];
+      for (int z = 1; z < a.splits; ++z) x0 += a.ws[(long long)z * a.split_stride + i0];
+    }
   }
-  __shared__ double rs[256], rq[256];
-  rs[threadIdx.x] = s;
-  rq[threadIdx.x] = q;
+  float s = 0.f, q = 0.f;
+  for (int p = p0 + prow; p < p1; p += RP) {
+    const size_t i = base + (size_t)p * a.C + c;
+    f32x4 v;
+    if (!split) {
+      v = *reinterpret_cast<const f32x4*>(a.x + i);
+    } else {
+      v = *reinterpret_cast<const f32x4*>(a.ws + i);
+      for (int z = 1; z < a.splits; ++z) v += *reinterpret_cast<const f32x4*>(a.ws + (long long)z * a.split_stride + i);
+      *reinterpret_cast<f32x4*>(a.x + i) = v;
+    }
+    const f32x4 d = v - x0;
+    s += (d[0] + d[1]) + (d[2] + d[3]);
+    q += (d[0] * d[0] + d[1] * d[1]) + (d[2] * d[2] + d[3] * d[3]);
+  }
+  __shared__ double sd[kThreads], qd[kThreads];
+  sd[tid] = s;
+  qd[tid] = q;
   __syncthreads();
-  for (int h = 128; h > 0; h >>= 1) {
-    if (threadIdx.x < h) {
-      rs[threadIdx.x] += rs[threadIdx.x + h];
-      rq[threadIdx.x] += rq[threadIdx.x + h];
+  for (int h = RP >> 1; h > 0; h >>= 1) {
+    if (prow < h) {
+      sd[tid] += sd[tid + h * Q];
+      qd[tid] += qd[tid + h * Q];
     }
     __syncthreads();
   }
-  if (threadIdx.x == 0) {
-    const double cnt = (double)HW * G;
-    const double m = rs[0] / cnt;
-    const double var = std::max(rq[0] / cnt - m * m, 0.0);
-    stats[ng] = make_float2((float)((double)x0 + m), (float)(1.0 / std::sqrt(var + (double)eps)));
-  }
-}
-
-// y = [relu]((x - mean) rstd gamma + beta [+ res]); element i of [N][HW][C]
-// (x and y may be the same buffer: every element is read and written by one thread)
-__global__ void __launch_bounds__(256) gn_apply_kernel(const float* x, const float2* __restrict__ stats,
-                                                       const float* __restrict__ gamma, const float* __restrict__ beta,
-                                                       const float* res, int relu, long long total, int HW, int C,
-                                                       int G, float* y) {
-  const int groups = C / G;
-  for (long long i = (long long)blockIdx.x * 256 + threadIdx.x; i < total; i += (long long)gridDim.x * 256) {
-    const int c = (int)(i % C);
-    const long long n = i / ((long long)HW * C);
-    const float2 st = stats[n * groups + c / G];
-    float v = (x[i] - st.x) * st.y * gamma[c] + beta[c];
-    if (res) v += res[i];
-    y[i] = relu ? fmaxf(v, 0.f) : v;
-  }
-}
-
-// 3x3 stride-2 max pooling, padding 1 (padding excluded)
-__global__ void __launch_bounds__(256) max_pool_kernel(const float* __restrict__ x, int N, int H, int W, int C,
-                                                       int Ho, int Wo, float* __restrict__ y) {
-  const long long total = (long long)N * Ho * Wo * C;
-  for (long long i = (long long)blockIdx.x * 256 + threadIdx.x; i < total; i += (long long)gridDim.x * 256) {
-    const int c = (int)(i % C);
-    long long r = i / C;
-    const int ow = (int)(r % Wo);
-    r /= Wo;
-    const int oh = (int)(r % Ho);
-    const int n = (int)(r / Ho);
-    float m = -INFINITY;
-    for (int a = 0; a < 3; ++a) {
-      const int ih = oh * 2 - 1 + a;
-      if (ih < 0 || ih >= H) continue;
-      for (int b = 0; b < 3; ++b) {
-        const int iw = ow * 2 - 1 + b;
-        if (iw < 0 || iw >= W) continue;
-        m = fmaxf(m, x[(((size_t)n * H + ih) * W + iw) * C + c]);
-      }
+  if (tid < a.gpw) {
+    const int cols = a.G >> 2;
+    double S = 0.0, Qs = 0.0;
+    for (int k = 0; k < cols; ++k) {
+      S += sd[tid * cols + k];
+      Qs += qd[tid * cols + k];
     }
-    y[i] = m;
+    a.part[((size_t)n * groups + ch * a.gpw + tid) * a.ps_stats + pi] = make_double2(S, Qs);
   }
+  if (pi == 0 && col * 4 % a.G == 0 && prow == 0) a.shift[(size_t)n * groups + ch * a.gpw + j] = x0;
 }
 
-// global average pooling: out[n * stride + c] = mean over pixels
-__global__ void __launch_bounds__(256) avg_pool_kernel(const float* __restrict__ x, int N, int HW, int C,
-                                                       float* __restrict__ out, int stride) {
-  const int i = blockIdx.x * 256 + threadIdx.x;
-  if (i >= N * C) return;
-  const int n = i / C, c = i % C;
-  float s = 0.f;
-  for (int p = 0; p < HW; ++p) s += x[((size_t)n * HW + p) * C + c];
-  out[(size_t)n * stride + c] = s / (float)HW;
+// Apply pass: mean and 1/sqrt(var + eps) from the partials, then
+// f(v) = [relu]((v - mean) rstd gamma + beta [+ res]) per mode.
+__global__ void __launch_bounds__(kThreads) gn_apply_kernel(const GnArgs a) {
+  const int HW = a.H * a.W, CW = a.G * a.gpw, Q = CW >> 2, RP = kThreads / Q;
+  const int chunks = a.C / CW, groups = a.C / a.G;
+  const int pi = blockIdx.x % a.ps_apply, rest = blockIdx.x / a.ps_apply;
+  const int ch = rest % chunks, n = rest / chunks;
+  const int tid = threadIdx.x, col = tid % Q, prow = tid / Q;
+  const int c = ch * CW + col * 4, j = (col * 4) / a.G;
+  const size_t base = (size_t)n * HW * a.C;
+  __shared__ float2 st[16];
+  if (tid < a.gpw) {
+    const int g = ch * a.gpw + tid;
+    const double2* pp = a.part + ((size_t)n * groups + g) * a.ps_stats;
+    double S = 0.0, Qs = 0.0;
+    for (int k = 0; k < a.ps_stats; ++k) {
+      S += pp[k].x;
+      Qs += pp[k].y;
+    }
+    const double cnt = (double)HW * a.G, m = S / cnt;
+    const double var = std::max(Qs / cnt - m * m, 0.0);
+    const float x0 = a.shift[(size_t)n * groups + g];
+    st[tid] = make_float2((float)((double)x0 + m), (float)(1.0 / std::sqrt(var + (double)a.eps)));
+  }
+  __syncthreads();
+  const float2 ms = st[j];
+  const f32x4 gm = *reinterpret_cast<const f32x4*>(a.gamma + c);
+  const f32x4 bt = *reinterpret_cast<const f32x4*>(a.beta + c);
+  auto f = [&](f32x4 v, size_t i) -> f32x4 {
+    f32x4 r;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) r[k] = (v[k] - ms.x) * ms.y * gm[k] + bt[k];
+    if (a.res) r += *reinterpret_cast<const f32x4*>(a.res + i);
+    if (a.relu) {
+#pragma unroll
+      for (int k = 0; k < 4; ++k) r[k] = fmaxf(r[k], 0.f);
+    }
+    return r;
+  };
+  if (a.mode == GN_PLAIN) {
+    const int pc = (HW + a.ps_apply - 1) / a.ps_apply, p0 = pi * pc, p1 = min(HW, p0 + pc);
+    for (int p = p0 + prow; p < p1; p += RP) {
+      const size_t i = base + (size_t)p * a.C + c;
+      *reinterpret_cast<f32x4*>(a.y + i) = f(*reinterpret_cast<const f32x4*>(a.x + i), i);
+    }
+  } else if (a.mode == GN_MAXPOOL) {
+    const int HWp = a.Hp * a.Wp, pc = (HWp + a.ps_apply - 1) / a.ps_apply, p0 = pi * pc, p1 = min(HWp, p0 + pc);
+    for (int p = p0 + prow; p < p1; p += RP) {
+      const int oh = p / a.Wp, ow = p - oh * a.Wp;
+      f32x4 m = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+      for (int u = 0; u < 3; ++u) {
+        const int ih = oh * 2 - 1 + u;
+        if (ih < 0 || ih >= a.H) continue;
+        for (int v = 0; v < 3; ++v) {
+          const int iw = ow * 2 - 1 + v;
+          if (iw < 0 || iw >= a.W) continue;
+          const size_t i = base + ((size_t)ih * a.W + iw) * a.C + c;
+          const f32x4 r = f(*reinterpret_cast<const f32x4*>(a.x + i), i);
+#pragma unroll
+          for (int k = 0; k < 4; ++k) m[k] = fmaxf(m[k], r[k]);
+        }
+      }
+      *reinterpret_cast<f32x4*>(a.y + (size_t)n * HWp * a.C + (size_t)p * a.C + c) = m;
+    }
+  } else {
+    // global average pooling (one pixel chunk): column sums over the rows
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int p = prow; p < HW; p += RP) {
+      const size_t i = base + (size_t)p * a.C + c;
+      acc += f(*reinterpret_cast<const f32x4*>(a.x + i), i);
+    }
+    __shared__ f32x4 red[kThreads];
+    red[tid] = acc;
+    __syncthreads();
+    for (int h = RP >> 1; h > 0; h >>= 1) {
+      if (prow < h) red[tid] += red[tid + h * Q];
+      __syncthreads();
+    }
+    if (prow == 0) {
+      const f32x4 m = red[tid] / (float)HW;
+      float* o = a.y + (size_t)n * a.out_stride + c;
+      o[0] = m[0];
+      o[1] = m[1];
+      o[2] = m[2];
+      o[3] = m[3];
+    }
+  }
 }
 
 // weights [Cout][K] fp32 -> [Cout][Kp] operand type, zero padded
@@ -280,13 +454,11 @@ __global__ void pack_conv_kernel(const float* __restrict__ w, int Cout, int K, i
   }
 }
 
-unsigned grid_for(long long total) {
-  return (unsigned)std::min<long long>((total + 255) / 256, 16384);
-}
+unsigned grid_for(long long total) { return (unsigned)std::min<long long>((total + 255) / 256, 16384); }
 
 struct ConvLayer {
   int cin, cout, k, stride, pad, K, Kp;
-  void* w = nullptr;            // packed operand weights
+  void* w = nullptr;             // packed operand weights
   const float* gamma = nullptr;  // GroupNorm affine (device, inside the raw copy)
   const float* beta = nullptr;
 };
@@ -297,11 +469,14 @@ struct evo_encoder {
   evo_encoder_desc desc{};
   int device = 0;
   int bf = 1;
-  float* d_raw = nullptr;             // fp32 parameter copy (GroupNorm affine, packing source)
-  std::vector<ConvLayer> convs;       // stem, then per block a, b[, d]
+  float* d_raw = nullptr;        // fp32 parameter copy (GroupNorm affine, packing source)
+  std::vector<ConvLayer> convs;  // stem, then per block a, b[, d]
   float* buf[4] = {nullptr, nullptr, nullptr, nullptr};
   size_t buf_floats = 0;
-  float2* d_stats = nullptr;
+  float* ws = nullptr;           // split-K partials, kWsFloats
+  double2* part = nullptr;       // GroupNorm partial statistics
+  size_t part_cap = 0;
+  float* shift = nullptr;        // GroupNorm shifts, part_cap floats
   uint64_t flops_per_image = 0;
 };
 
@@ -322,6 +497,8 @@ int enc_check(const evo_encoder_desc* d) {
                   d->widths[s], s);
     if (d->blocks[s] < 1 || d->blocks[s] > 16) return fail(EVO_E_INVALID, "blocks[%d] = %d", s, d->blocks[s]);
   }
+  if (d->gn_group != 4 && d->gn_group != 8 && d->gn_group != 16 && d->gn_group != 32 && d->gn_group != 64)
+    return fail(EVO_E_UNSUPPORTED, "gn_group must be 4, 8, 16, 32 or 64");
   if (d->dtype != EVO_FP32 && d->dtype != EVO_BF16) return fail(EVO_E_INVALID, "bad dtype");
   if (d->max_batch < 1 || d->max_batch > (1 << 16)) return fail(EVO_E_INVALID, "max_batch %d", d->max_batch);
   // pixel indices of a batch (stem output and below) are 32-bit
@@ -347,40 +524,113 @@ std::vector<ConvLayer> enc_layers(const evo_encoder_desc* d) {
 }
 
 inline int out_size(int h, int k, int s, int p) { return (h + 2 * p - k) / s + 1; }
+inline int cdiv(long long a, long long b) { return (int)((a + b - 1) / b); }
 
+// Launch shape of one convolution: tile, K splits.
+struct ConvPlan {
+  int bm, bn, mt, nt, splits, spp;
+};
+
+ConvPlan plan_conv(int M, int Cout, int steps) {
+  static const int cand[3][2] = {{128, 128}, {128, 64}, {64, 64}};
+  ConvPlan pl{};
+  for (const auto& t : cand) {
+    if (t[1] > 64 && Cout < 128) continue;
+    pl.bm = t[0];
+    pl.bn = t[1];
+    pl.mt = cdiv(M, t[0]);
+    pl.nt = cdiv(Cout, t[1]);
+    if ((long long)pl.mt * pl.nt >= kTargetWG) break;
+  }
+  const int tiles = pl.mt * pl.nt;
+  int splits = 1;
+  if (tiles < kTargetWG) splits = std::min({cdiv(kTargetWG, tiles), std::max(1, steps / 2), kMaxSplit});
+  pl.spp = cdiv(steps, splits);
+  pl.splits = cdiv(steps, pl.spp);  // every split has at least one step
+  return pl;
+}
+
+template <class AT>
+void launch_conv_t(const ConvPlan& pl, const ConvArgs& a, unsigned grid, hipStream_t st) {
+  if (pl.bm == 128 && pl.bn == 128)
+    hipLaunchKernelGGL((conv_kernel<AT, 128, 128>), dim3(grid), dim3(kThreads), 0, st, a);
+  else if (pl.bm == 128)
+    hipLaunchKernelGGL((conv_kernel<AT, 128, 64>), dim3(grid), dim3(kThreads), 0, st, a);
+  else
+    hipLaunchKernelGGL((conv_kernel<AT, 64, 64>), dim3(grid), dim3(kThreads), 0, st, a);
+}
+
+// The conv result lands in `y` (one split) or as partials in the encoder's
+// workspace; `*gn` gets the source fields of the GroupNorm that follows.
 hipError_t launch_conv(const evo_encoder* e, const ConvLayer& L, const float* x, int N, int H, int W, float* y,
-                       int* Ho, int* Wo, hipStream_t st) {
+                       int* Ho, int* Wo, GnArgs* gn, hipStream_t st) {
   ConvArgs a;
   a.x = x;
   a.w = L.w;
-  a.y = y;
-  a.N = N;
   a.H = H;
   a.W = W;
   a.Cin = L.cin;
   a.Ho = *Ho = out_size(H, L.k, L.stride, L.pad);
   a.Wo = *Wo = out_size(W, L.k, L.stride, L.pad);
   a.Cout = L.cout;
-  a.kh = a.kw = L.k;
+  a.kw = L.k;
   a.stride = L.stride;
   a.pad = L.pad;
   a.K = L.K;
   a.Kp = L.Kp;
-  const long long M = (long long)N * a.Ho * a.Wo;
-  dim3 grid((unsigned)((M + kBM - 1) / kBM), (unsigned)((L.cout + kBN - 1) / kBN));
-  if (e->bf) hipLaunchKernelGGL(conv_kernel<__bf16>, grid, dim3(kThreads), 0, st, a);
-  else hipLaunchKernelGGL(conv_kernel<float>, grid, dim3(kThreads), 0, st, a);
+  a.M = N * a.Ho * a.Wo;
+  const int KS = e->bf ? ConvStep<__bf16>::KS : ConvStep<float>::KS;
+  const ConvPlan pl = plan_conv(a.M, L.cout, L.Kp / KS);
+  a.mt = pl.mt;
+  a.nt = pl.nt;
+  a.splits = pl.splits;
+  a.spp = pl.spp;
+  a.split_stride = (long long)a.M * L.cout;
+  // splits * tiles * 64 * 64 bounds the partials, below the workspace by construction
+  if (pl.splits > 1 && (long long)pl.splits * a.split_stride > kWsFloats) return hipErrorInvalidValue;
+  a.y = pl.splits > 1 ? e->ws : y;
+  gn->ws = e->ws;
+  gn->splits = pl.splits;
+  gn->split_stride = a.split_stride;
+  gn->x = y;
+  const unsigned grid = (unsigned)((long long)pl.mt * pl.nt * pl.splits);
+  if (e->bf) launch_conv_t<__bf16>(pl, a, grid, st);
+  else launch_conv_t<float>(pl, a, grid, st);
   return hipGetLastError();
 }
 
-hipError_t launch_gn(const evo_encoder* e, const ConvLayer& L, const float* x, int N, int HW, const float* res,
-                     int relu, float* y, hipStream_t st) {
-  const int C = L.cout, G = e->desc.gn_group;
-  hipLaunchKernelGGL(gn_stats_kernel, dim3((unsigned)(N * (C / G))), dim3(256), 0, st, x, HW, C, G, 1e-5f,
-                     e->d_stats);
-  const long long total = (long long)N * HW * C;
-  hipLaunchKernelGGL(gn_apply_kernel, dim3(grid_for(total)), dim3(256), 0, st, x, e->d_stats, L.gamma, L.beta, res,
-                     relu, total, HW, C, G, y);
+// GroupNorm of layer L's conv output (g.ws / splits / x set by launch_conv).
+hipError_t launch_gn(const evo_encoder* e, const ConvLayer& L, GnArgs g, int N, int H, int W, const float* res,
+                     int relu, int mode, float* y, int out_stride, hipStream_t st) {
+  const int C = L.cout, G = e->desc.gn_group, groups = C / G;
+  int gpw = 1;  // groups per workgroup: up to 64 channels, a power of two dividing the group count
+  while (gpw * 2 * G <= 64 && groups % (gpw * 2) == 0) gpw *= 2;
+  const int chunks = groups / gpw, HW = H * W;
+  const int base = N * chunks;
+  int ps = std::max(1, std::min(cdiv(kGnTarget, base), cdiv(HW, 16)));
+  if ((size_t)N * groups * ps > e->part_cap) ps = std::max(1, (int)(e->part_cap / ((size_t)N * groups)));
+  g.gamma = L.gamma;
+  g.beta = L.beta;
+  g.res = res;
+  g.y = y;
+  g.part = e->part;
+  g.shift = e->shift;
+  g.relu = relu;
+  g.mode = mode;
+  g.H = H;
+  g.W = W;
+  g.C = C;
+  g.G = G;
+  g.gpw = gpw;
+  g.ps_stats = ps;
+  g.Hp = mode == GN_MAXPOOL ? out_size(H, 3, 2, 1) : 0;
+  g.Wp = mode == GN_MAXPOOL ? out_size(W, 3, 2, 1) : 0;
+  g.out_stride = out_stride;
+  g.eps = 1e-5f;
+  const int out_px = mode == GN_MAXPOOL ? g.Hp * g.Wp : HW;
+  g.ps_apply = mode == GN_AVGPOOL ? 1 : std::max(1, std::min(cdiv(kGnTarget, base), cdiv(out_px, 16)));
+  hipLaunchKernelGGL(gn_stats_kernel, dim3((unsigned)(base * ps)), dim3(kThreads), 0, st, g);
+  hipLaunchKernelGGL(gn_apply_kernel, dim3((unsigned)(base * g.ps_apply)), dim3(kThreads), 0, st, g);
   return hipGetLastError();
 }
 
@@ -404,29 +654,57 @@ int evo_create_encoder(const evo_encoder_desc* desc, const float* host_weights, 
   if (rc) return rc;
   if (!host_weights || !out) return fail(EVO_E_INVALID, "NULL pointer");
   const int64_t need = evo_encoder_weight_count(desc);
-  if ((int64_t)n_floats != need) return fail(EVO_E_INVALID, "n_floats is %zu, this encoder needs %lld", n_floats,
-                                             (long long)need);
+  if ((int64_t)n_floats != need)
+    return fail(EVO_E_INVALID, "n_floats is %zu, this encoder needs %lld", n_floats, (long long)need);
   evo_encoder* e = new (std::nothrow) evo_encoder();
   if (!e) return fail(EVO_E_NOMEM, "host allocation failed");
   const auto body = [&]() -> int {
     e->desc = *desc;
     e->bf = desc->dtype == EVO_BF16;
     if (hipGetDevice(&e->device) != hipSuccess) return fail(EVO_E_HIP, "no current HIP device");
-#define ENC_TRY(expr)                                                                              \
-    do {                                                                                           \
-      hipError_t e_ = (expr);                                                                      \
-      if (e_ != hipSuccess)                                                                        \
-        return fail(e_ == hipErrorOutOfMemory ? EVO_E_NOMEM : EVO_E_HIP, "%s failed: %s", #expr,   \
-                    hipGetErrorString(e_));                                                        \
-    } while (0)
+#define ENC_TRY(expr)                                                                          \
+  do {                                                                                         \
+    hipError_t e_ = (expr);                                                                    \
+    if (e_ != hipSuccess)                                                                      \
+      return fail(e_ == hipErrorOutOfMemory ? EVO_E_NOMEM : EVO_E_HIP, "%s failed: %s", #expr, \
+                  hipGetErrorString(e_));                                                      \
+  } while (0)
+    // activation sizes and FLOPs: walk the network once
+    size_t maxact = 0;
+    int maxgroups = 0;
+    uint64_t flops = 0;
+    {
+      int h = out_size(desc->height, 7, 2, 3), w = out_size(desc->width, 7, 2, 3);
+      maxact = std::max(maxact, (size_t)h * w * desc->stem_ch);
+      maxgroups = desc->stem_ch / desc->gn_group;
+      flops += 2ull * h * w * desc->stem_ch * 49 * desc->in_ch;
+      h = out_size(h, 3, 2, 1);
+      w = out_size(w, 3, 2, 1);
+      int cin = desc->stem_ch;
+      for (int s = 0; s < desc->n_stages; ++s)
+        for (int b = 0; b < desc->blocks[s]; ++b) {
+          const int c = desc->widths[s], stride = (s > 0 && b == 0) ? 2 : 1;
+          const int ho = out_size(h, 3, stride, 1), wo = out_size(w, 3, stride, 1);
+          if (ho < 1 || wo < 1) return fail(EVO_E_INVALID, "the image is too small for the network");
+          maxact = std::max(maxact, (size_t)ho * wo * c);
+          maxgroups = std::max(maxgroups, c / desc->gn_group);
+          flops += 2ull * ho * wo * c * 9 * cin + 2ull * ho * wo * c * 9 * c;
+          if (stride != 1 || cin != c) flops += 2ull * ho * wo * c * cin;
+          h = ho;
+          w = wo;
+          cin = c;
+        }
+    }
+    if (maxact * desc->max_batch >= (size_t(1) << 31))
+      return fail(EVO_E_UNSUPPORTED, "activations of max_batch images exceed 2^31 floats");
+    e->flops_per_image = flops;
+    e->buf_floats = maxact * desc->max_batch;
+    e->part_cap = (size_t)desc->max_batch * maxgroups + kMaxPart;
     ENC_TRY(hipMalloc(&e->d_raw, n_floats * sizeof(float)));
     ENC_TRY(hipMemcpy(e->d_raw, host_weights, n_floats * sizeof(float), hipMemcpyHostToDevice));
     e->convs = enc_layers(desc);
-    const int KS = e->bf ? 32 : 16;
+    const int KS = e->bf ? ConvStep<__bf16>::KS : ConvStep<float>::KS;
     size_t off = 0;
-    int H = desc->height, W = desc->width, maxg = 0;
-    size_t maxact = 0;
-    uint64_t flops = 0;
     for (ConvLayer& L : e->convs) {
       L.K = L.k * L.k * L.cin;
       L.Kp = (L.K + KS - 1) / KS * KS;
@@ -438,33 +716,11 @@ int evo_create_encoder(const evo_encoder_desc* desc, const float* host_weights, 
       L.gamma = e->d_raw + off;
       L.beta = e->d_raw + off + L.cout;
       off += 2 * (size_t)L.cout;
-      maxg = std::max(maxg, L.cout / desc->gn_group);
     }
-    // activation sizes: walk the network once
-    {
-      int h = out_size(H, 7, 2, 3), w = out_size(W, 7, 2, 3);
-      maxact = std::max(maxact, (size_t)h * w * desc->stem_ch);
-      flops += 2ull * h * w * desc->stem_ch * 49 * desc->in_ch;
-      h = out_size(h, 3, 2, 1);
-      w = out_size(w, 3, 2, 1);
-      int cin = desc->stem_ch;
-      for (int s = 0; s < desc->n_stages; ++s)
-        for (int b = 0; b < desc->blocks[s]; ++b) {
-          const int c = desc->widths[s], stride = (s > 0 && b == 0) ? 2 : 1;
-          const int ho = out_size(h, 3, stride, 1), wo = out_size(w, 3, stride, 1);
-          if (ho < 1 || wo < 1) return fail(EVO_E_INVALID, "the image is too small for the network");
-          maxact = std::max(maxact, (size_t)ho * wo * c);
-          flops += 2ull * ho * wo * c * 9 * cin + 2ull * ho * wo * c * 9 * c;
-          if (stride != 1 || cin != c) flops += 2ull * ho * wo * c * cin;
-          h = ho;
-          w = wo;
-          cin = c;
-        }
-    }
-    e->flops_per_image = flops;
-    e->buf_floats = maxact * desc->max_batch;
     for (int i = 0; i < 4; ++i) ENC_TRY(hipMalloc(&e->buf[i], e->buf_floats * sizeof(float)));
-    ENC_TRY(hipMalloc(&e->d_stats, (size_t)desc->max_batch * maxg * sizeof(float2)));
+    ENC_TRY(hipMalloc(&e->ws, (size_t)kWsFloats * sizeof(float)));
+    ENC_TRY(hipMalloc(&e->part, e->part_cap * sizeof(double2)));
+    ENC_TRY(hipMalloc(&e->shift, e->part_cap * sizeof(float)));
     ENC_TRY(hipDeviceSynchronize());
 #undef ENC_TRY
     *out = e;
@@ -489,52 +745,48 @@ int evo_encode(evo_encoder* e, int32_t batch, const float* images, float* featur
   float *X = e->buf[0], *Y = e->buf[1], *Z = e->buf[2], *R = e->buf[3];
   int H = d.height, W = d.width, Ho, Wo;
   size_t li = 0;
-#define ENC_HIP(expr)                                                                               \
-  do {                                                                                              \
-    hipError_t e_ = (expr);                                                                         \
-    if (e_ != hipSuccess) return fail(EVO_E_HIP, "%s failed: %s", #expr, hipGetErrorString(e_));    \
+  GnArgs g{};
+#define ENC_HIP(expr)                                                                            \
+  do {                                                                                           \
+    hipError_t e_ = (expr);                                                                      \
+    if (e_ != hipSuccess) return fail(EVO_E_HIP, "%s failed: %s", #expr, hipGetErrorString(e_)); \
   } while (0)
-  // stem: conv 7x7/2, GN, ReLU, max pool 3x3/2
+  // stem: conv 7x7/2, then GroupNorm + ReLU + max pool 3x3/2 in one apply pass
   {
     const ConvLayer& L = e->convs[li++];
-    ENC_HIP(launch_conv(e, L, images, batch, H, W, Y, &Ho, &Wo, st));
-    ENC_HIP(launch_gn(e, L, Y, batch, Ho * Wo, nullptr, 1, Y, st));
-    const int Hp = out_size(Ho, 3, 2, 1), Wp = out_size(Wo, 3, 2, 1);
-    const long long total = (long long)batch * Hp * Wp * L.cout;
-    hipLaunchKernelGGL(max_pool_kernel, dim3(grid_for(total)), dim3(256), 0, st, Y, batch, Ho, Wo, L.cout, Hp, Wp, X);
-    ENC_HIP(hipGetLastError());
-    H = Hp;
-    W = Wp;
+    ENC_HIP(launch_conv(e, L, images, batch, H, W, Y, &Ho, &Wo, &g, st));
+    ENC_HIP(launch_gn(e, L, g, batch, Ho, Wo, nullptr, 1, GN_MAXPOOL, X, 0, st));
+    H = out_size(Ho, 3, 2, 1);
+    W = out_size(Wo, 3, 2, 1);
   }
   int cin = d.stem_ch;
   for (int s = 0; s < d.n_stages; ++s)
     for (int b = 0; b < d.blocks[s]; ++b) {
       const int c = d.widths[s];
+      const bool last = s == d.n_stages - 1 && b == d.blocks[s] - 1;
       const ConvLayer& La = e->convs[li++];
       const ConvLayer& Lb = e->convs[li++];
       const bool proj = La.stride != 1 || cin != c;
       int H2, W2, H3, W3;
-      ENC_HIP(launch_conv(e, La, X, batch, H, W, Y, &H2, &W2, st));
-      ENC_HIP(launch_gn(e, La, Y, batch, H2 * W2, nullptr, 1, Y, st));
-      ENC_HIP(launch_conv(e, Lb, Y, batch, H2, W2, Z, &H3, &W3, st));
+      ENC_HIP(launch_conv(e, La, X, batch, H, W, Y, &H2, &W2, &g, st));
+      ENC_HIP(launch_gn(e, La, g, batch, H2, W2, nullptr, 1, GN_PLAIN, Y, 0, st));
       const float* shortcut = X;
-      if (proj) {
+      if (proj) {  // before conv b: each conv's partials are consumed before the next conv runs
         const ConvLayer& Ld = e->convs[li++];
         int Hd, Wd;
-        ENC_HIP(launch_conv(e, Ld, X, batch, H, W, R, &Hd, &Wd, st));
-        ENC_HIP(launch_gn(e, Ld, R, batch, Hd * Wd, nullptr, 0, R, st));
+        ENC_HIP(launch_conv(e, Ld, X, batch, H, W, R, &Hd, &Wd, &g, st));
+        ENC_HIP(launch_gn(e, Ld, g, batch, Hd, Wd, nullptr, 0, GN_PLAIN, R, 0, st));
         shortcut = R;
       }
-      // block output = ReLU(GN(conv b) + shortcut), written over the block input
-      ENC_HIP(launch_gn(e, Lb, Z, batch, H3 * W3, shortcut, 1, Y, st));
+      ENC_HIP(launch_conv(e, Lb, Y, batch, H2, W2, Z, &H3, &W3, &g, st));
+      // block output = ReLU(GN(conv b) + shortcut): into Y, or averaged into the features
+      if (last) ENC_HIP(launch_gn(e, Lb, g, batch, H3, W3, shortcut, 1, GN_AVGPOOL, features_out, out_stride, st));
+      else ENC_HIP(launch_gn(e, Lb, g, batch, H3, W3, shortcut, 1, GN_PLAIN, Y, 0, st));
       std::swap(X, Y);
       H = H3;
       W = W3;
       cin = c;
     }
-  hipLaunchKernelGGL(avg_pool_kernel, dim3((unsigned)((batch * C_out + 255) / 256)), dim3(256), 0, st, X, batch,
-                     H * W, C_out, features_out, out_stride);
-  ENC_HIP(hipGetLastError());
 #undef ENC_HIP
   return EVO_OK;
 }
@@ -552,7 +804,9 @@ void evo_destroy_encoder(evo_encoder* e) {
   (void)hipDeviceSynchronize();
   for (ConvLayer& L : e->convs) (void)hipFree(L.w);
   for (int i = 0; i < 4; ++i) (void)hipFree(e->buf[i]);
-  (void)hipFree(e->d_stats);
+  (void)hipFree(e->ws);
+  (void)hipFree(e->part);
+  (void)hipFree(e->shift);
   (void)hipFree(e->d_raw);
   delete e;
 }
