@@ -125,6 +125,74 @@ def cpu_baseline(inp, budget_s=12.0):
                       f"{el:.1f} s)"}
 
 
+def bench_encoder(dev):
+    """Observation encoder of the image policy (84x84 frames, ResNet-18
+    topology with GroupNorm, bf16 operands) at 512 frames (256 chunks x 2
+    observation steps), and the whole action query at batch 1: encode the 2
+    observation frames into the observation rows, then the cached loop."""
+    import torch
+    from paper_2607_20293_amd import evo
+    from paper_2607_20293_amd import inputs as I
+    extras = {}
+    e, s = I.ENC_ROBOMIMIC, I.IMAGE
+    nf = 256 * s.n_obs
+    enc = evo.Encoder(e, I.make_encoder_weights(e, 0), "bf16", max_batch=nf)
+    imgs = torch.from_numpy(I.make_images(e, nf, 0)).to(dev)
+    obs_e = torch.from_numpy(I.make_obs(s, 256, 0)).to(dev)
+    feats = obs_e.view(nf, s.obs_dim)[:, :e.out_dim]
+    for _ in range(3):
+        enc.encode(imgs, out=feats)
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    reps = 20
+    ev[0].record()
+    for _ in range(reps):
+        enc.encode(imgs, out=feats)
+    ev[1].record()
+    torch.cuda.synchronize()
+    enc_ms = ev[0].elapsed_time(ev[1]) / reps
+    enc_tf = enc.flops(nf) / (enc_ms * 1e-3) / 1e12
+    flops_frame = enc.flops(1)
+    wts = I.make_weights(s, 0)
+    img1 = imgs[:s.n_obs].contiguous()
+    pa = {}
+    for dens in (0.25, 1.0):
+        lt = I.make_lattice("all" if dens == 1.0 else "dirichlet", s.n_layers, s.n_steps, dens, 0)
+        r = Runner(f"image_bf16_b1_{dens}", s, wts, "bf16", [lt], np.zeros(1, np.int32),
+                   I.make_obs(s, 1, 0), I.make_noise(s, 1, 0))
+        f1 = r.obs.view(s.n_obs, s.obs_dim)[:, :e.out_dim]
+
+        def query():
+            enc.encode(img1, out=f1)
+            r.call()
+
+        for _ in range(3):
+            query()
+        torch.cuda.synchronize()
+        ls, le = [], []
+        for _ in range(30):
+            t = time.perf_counter()
+            query()
+            torch.cuda.synchronize()
+            ls.append((time.perf_counter() - t) * 1e3)
+        for _ in range(30):
+            t = time.perf_counter()
+            enc.encode(img1, out=f1)
+            torch.cuda.synchronize()
+            le.append((time.perf_counter() - t) * 1e3)
+        r.pol.synchronize()
+        r.close()
+        pa[str(dens)] = {"p50_ms": round(statistics.median(ls), 4), "encode_p50_ms": round(statistics.median(le), 4)}
+    enc.close()
+    extras["encoder_robomimic_bf16_b512"] = {
+        "frames_per_s": round(nf / (enc_ms * 1e-3), 1), "ms": round(enc_ms, 4), "TFLOPs": round(enc_tf, 2),
+        "frac_peak": round(enc_tf / PEAK["bf16"], 4), "flops_per_frame": flops_frame}
+    extras["predict_action_image_bf16_b1"] = pa
+    log(f"[bench] encoder_robomimic_bf16_b512: {extras['encoder_robomimic_bf16_b512']}")
+    log(f"[bench] predict_action_image_bf16_b1: {pa}")
+    return extras
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -134,6 +202,8 @@ def main():
     ap.add_argument("--workload", default="image_bf16_b256_d12",
                     help="workload timed for the main line (profiling runs of other workloads)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--only-encoder", action="store_true",
+                    help="observation encoder and batch-1 action query only (profiling runs)")
     ap.add_argument("--calib-copy", action="store_true", help="also run one 256 MiB device copy (counter scale)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -146,6 +216,10 @@ def main():
     from paper_2607_20293_amd import inputs as I
     evo.lib()
     assert torch.cuda.is_available(), "bench.py needs a GPU"
+
+    if args.only_encoder:
+        print(json.dumps(bench_encoder(torch.device("cuda:0"))), flush=True)
+        return
 
     if args.calib_copy:
         x = torch.ones(64 << 20, dtype=torch.float32, device="cuda:0")
@@ -312,6 +386,8 @@ def main():
             "mean_quick_initial": round(float(np.mean(fits[0])), 4),
             "mean_quick_last": round(float(np.mean(fits[-1])), 4)}
         log(f"[bench] search_pusht_bf16_K240: {extras['search_pusht_bf16_K240']}")
+
+        extras.update(bench_encoder(dev))
 
     cpu = None
     if not args.no_cpu_baseline:

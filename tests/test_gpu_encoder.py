@@ -5,11 +5,15 @@ normwise relative <= 3e-2 (the oracle rounds the same weights to bf16; the
 kernel also rounds the activations it multiplies).  Sizes: a tiny network
 with ragged tiles (channels and pixel counts not multiples of 64) and the
 96x96 network at a small batch; strided output rows."""
+from dataclasses import replace
+
 import numpy as np
 import pytest
 
 from oracle import evo_encoder as E
+from oracle import evo_oracle as O
 from paper_2607_20293_amd import inputs as I
+from tests.gpu_util import compare
 
 pytestmark = pytest.mark.gpu
 
@@ -102,3 +106,39 @@ def test_encoder_rejects_bad_arguments():
         enc.encode(x)                       # batch above max_batch
     with pytest.raises(evo.EvoError):
         evo.Encoder(e, I.make_encoder_weights(e, 3)[:-1], "fp32")
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_encode_then_denoise_matches_oracle_chain(dtype):
+    """The whole action query: camera frames -> encoder features written into
+    the observation rows beside the proprioceptive columns -> cached
+    denoising, against the oracle's encoder followed by the oracle's loop."""
+    torch = _torch()
+    from paper_2607_20293_amd import evo
+    e = I.ENC_TINY
+    s = replace(I.TINY, obs_dim=e.out_dim + 4)
+    B = 3
+    ew = I.make_encoder_weights(e, 21, "perturbed")
+    pw = I.make_weights(s, 21, "perturbed")
+    imgs = I.make_images(e, B * s.n_obs, 21)   # frame t of sample b is image b * n_obs + t
+    obs = I.make_obs(s, B, 21)                 # the last 4 columns stay (proprioception)
+    noise = I.make_noise(s, B, 21)
+    lats = [I.lattice_bernoulli(s.n_layers, s.n_steps, 0.4, np.random.default_rng(21))]
+    ids = np.zeros(B, np.int32)
+
+    enc = evo.Encoder(e, ew, dtype, max_batch=B * s.n_obs)
+    pol = evo.Policy(s, pw, dtype=dtype, max_batch=B, max_schedules=1)
+    pol.set_schedule(0, lats[0], evo.GRAN_LAYER)
+    obs_d = torch.from_numpy(obs).cuda()
+    enc.encode(torch.from_numpy(imgs).cuda(), out=obs_d.view(B * s.n_obs, s.obs_dim)[:, :e.out_dim])
+    got = pol.denoise(obs_d, torch.from_numpy(noise).cuda(), ids).cpu().numpy()
+    assert np.array_equal(obs_d[:, :, e.out_dim:].cpu().numpy(), obs[:, :, e.out_dim:])
+    pol.close()
+    enc.close()
+
+    f = E.encode(e, I.split_encoder_weights(e, ew), imgs, dtype)
+    obs_ref = obs.astype(np.float64)
+    obs_ref[:, :, :e.out_dim] = f.reshape(B, s.n_obs, e.out_dim)
+    ref, _ = O.denoise(s, I.split_weights(s, pw), obs_ref, noise, lats, ids, granularity=O.GRAN_LAYER,
+                       cold_policy=O.COLD_COMPUTE, clip=True, dtype=dtype)
+    compare(got, ref, dtype, f"encode+denoise {dtype}")
