@@ -142,3 +142,41 @@ def test_encode_then_denoise_matches_oracle_chain(dtype):
     ref, _ = O.denoise(s, I.split_weights(s, pw), obs_ref, noise, lats, ids, granularity=O.GRAN_LAYER,
                        cold_policy=O.COLD_COMPUTE, clip=True, dtype=dtype)
     compare(got, ref, dtype, f"encode+denoise {dtype}")
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_encoder_large_tiles_sampled_frames(dtype):
+    """A batch large enough for the 128x128 and 128x64 convolution tiles
+    (no K split), checked on sampled frames: frames are independent, so the
+    oracle runs on those frames alone."""
+    torch = _torch()
+    from paper_2607_20293_amd import evo
+    e = I.EncoderShape(64, 64, stem_ch=64, widths=(128, 256), blocks=(1, 1), gn_group=16)
+    B, pick = 256, [0, 77, 255]
+    w = I.make_encoder_weights(e, 31, "perturbed")
+    imgs = I.make_images(e, B, 31)
+    enc = evo.Encoder(e, w, dtype, max_batch=B)
+    got = enc.encode(torch.from_numpy(imgs).cuda()).cpu().numpy().astype(np.float64)[pick]
+    enc.close()
+    want = E.encode(e, I.split_encoder_weights(e, w), imgs[pick], dtype)
+    if dtype == "fp32":
+        print("large tiles fp32 max-abs", np.max(np.abs(got - want)))
+        assert np.max(np.abs(got - want)) <= 1e-4
+    else:
+        print("large tiles bf16 rel", _rel(got, want))
+        assert _rel(got, want) <= 3e-2
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_encoder_odd_shape(dtype):
+    """Odd image sizes (ragged maps at every stage), one input channel (the
+    element-wise gather), GroupNorm groups of 4 channels, two blocks in the
+    first stage (identity shortcuts)."""
+    e = I.EncoderShape(37, 29, in_ch=1, stem_ch=8, widths=(8, 16), blocks=(2, 1), gn_group=4)
+    got, want = _run(e, dtype, 2, 32)
+    if dtype == "fp32":
+        print("odd fp32 max-abs", np.max(np.abs(got - want)))
+        assert np.max(np.abs(got - want)) <= 1e-4
+    else:
+        print("odd bf16 rel", _rel(got, want))
+        assert _rel(got, want) <= 3e-2
