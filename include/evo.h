@@ -390,14 +390,19 @@ void evo_destroy_policy(evo_policy* p);
 typedef struct {
   int32_t height, width; /* image size, 8 .. 4096 */
   int32_t in_ch;         /* image channels, 1 .. 64 */
-  int32_t stem_ch;       /* stem width, a multiple of 8 and of gn_group */
+  int32_t stem_ch;       /* stem width, a multiple of 8 and of gn_group
+                            (not a multiple of 8: EVO_E_UNSUPPORTED) */
   int32_t n_stages;      /* 1 .. 4 */
   int32_t widths[4];     /* stage widths, multiples of 8 and of gn_group, <= 4096 */
   int32_t blocks[4];     /* basic blocks per stage, 1 .. 16 */
-  int32_t gn_group;      /* channels per GroupNorm group */
+  int32_t gn_group;      /* channels per GroupNorm group: 4, 8, 16, 32 or 64
+                            (others: EVO_E_UNSUPPORTED) */
   int32_t dtype;         /* EVO_BF16: convolution operands rounded to bf16
                             (fp32 accumulation); EVO_FP32: fp32 operands */
-  int32_t max_batch;     /* largest batch of evo_encode, 1 .. 65536 */
+  int32_t max_batch;     /* largest batch of evo_encode, 1 .. 65536; also
+                            max_batch * height * width < 2^31 and the largest
+                            activation map of max_batch images < 2^31 floats
+                            (EVO_E_UNSUPPORTED otherwise) */
 } evo_encoder_desc;
 
 typedef struct evo_encoder evo_encoder;
