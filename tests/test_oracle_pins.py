@@ -112,25 +112,88 @@ def test_units_equal_torch_decoder_layer(shape):
     h2 = h1 + r2
     ours = h2 + O.unit_residual(3 * l + 2, h2, mem, P, nh)
 
+    layer = _torch_layer(shape, P, l)
+    with torch.no_grad():
+        mask = torch.nn.Transformer.generate_square_subsequent_mask(shape.horizon, dtype=torch.float64)
+        ref = layer(_t(h), _t(mem), tgt_mask=mask).numpy()
+    np.testing.assert_allclose(ours, ref, rtol=0, atol=1e-12)
+
+
+def _t(a):
+    return torch.tensor(np.asarray(a, np.float64))
+
+
+def _torch_layer(shape, P, l):
+    """torch's pre-norm decoder layer (exact-erf GELU) holding layer l's weights."""
+    d, nh = shape.d_model, shape.n_heads
     layer = torch.nn.TransformerDecoderLayer(d, nh, shape.d_ff, dropout=0.0, activation="gelu",
                                              batch_first=True, norm_first=True, layer_norm_eps=1e-5)
     layer = layer.double().eval()
     p = f"l{l}."
     with torch.no_grad():
-        t = lambda a: torch.tensor(np.asarray(a, np.float64))
-        layer.norm1.weight.copy_(t(P[p + "ln1_g"])); layer.norm1.bias.copy_(t(P[p + "ln1_b"]))
-        layer.self_attn.in_proj_weight.copy_(t(P[p + "W_qkv"])); layer.self_attn.in_proj_bias.copy_(t(P[p + "b_qkv"]))
-        layer.self_attn.out_proj.weight.copy_(t(P[p + "W_o"])); layer.self_attn.out_proj.bias.copy_(t(P[p + "b_o"]))
-        layer.norm2.weight.copy_(t(P[p + "ln2_g"])); layer.norm2.bias.copy_(t(P[p + "ln2_b"]))
-        layer.multihead_attn.in_proj_weight.copy_(t(np.concatenate([P[p + "W_q"], P[p + "W_kv"]])))
-        layer.multihead_attn.in_proj_bias.copy_(t(np.concatenate([P[p + "b_q"], P[p + "b_kv"]])))
-        layer.multihead_attn.out_proj.weight.copy_(t(P[p + "W_o2"])); layer.multihead_attn.out_proj.bias.copy_(t(P[p + "b_o2"]))
-        layer.norm3.weight.copy_(t(P[p + "ln3_g"])); layer.norm3.bias.copy_(t(P[p + "ln3_b"]))
-        layer.linear1.weight.copy_(t(P[p + "W_1"])); layer.linear1.bias.copy_(t(P[p + "b_1"]))
-        layer.linear2.weight.copy_(t(P[p + "W_2"])); layer.linear2.bias.copy_(t(P[p + "b_2"]))
-        mask = torch.nn.Transformer.generate_square_subsequent_mask(shape.horizon, dtype=torch.float64)
-        ref = layer(t(h), t(mem), tgt_mask=mask).numpy()
-    np.testing.assert_allclose(ours, ref, rtol=0, atol=1e-12)
+        layer.norm1.weight.copy_(_t(P[p + "ln1_g"])); layer.norm1.bias.copy_(_t(P[p + "ln1_b"]))
+        layer.self_attn.in_proj_weight.copy_(_t(P[p + "W_qkv"])); layer.self_attn.in_proj_bias.copy_(_t(P[p + "b_qkv"]))
+        layer.self_attn.out_proj.weight.copy_(_t(P[p + "W_o"])); layer.self_attn.out_proj.bias.copy_(_t(P[p + "b_o"]))
+        layer.norm2.weight.copy_(_t(P[p + "ln2_g"])); layer.norm2.bias.copy_(_t(P[p + "ln2_b"]))
+        layer.multihead_attn.in_proj_weight.copy_(_t(np.concatenate([P[p + "W_q"], P[p + "W_kv"]])))
+        layer.multihead_attn.in_proj_bias.copy_(_t(np.concatenate([P[p + "b_q"], P[p + "b_kv"]])))
+        layer.multihead_attn.out_proj.weight.copy_(_t(P[p + "W_o2"])); layer.multihead_attn.out_proj.bias.copy_(_t(P[p + "b_o2"]))
+        layer.norm3.weight.copy_(_t(P[p + "ln3_g"])); layer.norm3.bias.copy_(_t(P[p + "ln3_b"]))
+        layer.linear1.weight.copy_(_t(P[p + "W_1"])); layer.linear1.bias.copy_(_t(P[p + "b_1"]))
+        layer.linear2.weight.copy_(_t(P[p + "W_2"])); layer.linear2.bias.copy_(_t(P[p + "b_2"]))
+    return layer
+
+
+def _torch_policy_sample(shape, P, obs, noise):
+    """The uncached policy and sampler rebuilt from torch modules in float64:
+    torch.nn.Linear / TransformerDecoderLayer / LayerNorm for the network,
+    and the DDPM reverse step in its epsilon form (x - beta / sqrt(1 - abar)
+    eps) / sqrt(alpha) + sigma z, with betas from torch's cos of the
+    squared-cosine schedule.  No clipping, so the epsilon form applies."""
+    d, A, T = shape.d_model, shape.action_dim, shape.n_steps
+    lin = lambda W, b: (lambda v: torch.nn.functional.linear(v, _t(W), _t(b)))
+    in_proj, obs_proj, head = lin(P["W_in"], P["b_in"]), lin(P["W_obs"], P["b_obs"]), lin(P["W_out"], P["b_out"])
+    ln_f = torch.nn.LayerNorm(d, eps=1e-5).double()
+    layers = [_torch_layer(shape, P, l) for l in range(shape.n_layers)]
+    mask = torch.nn.Transformer.generate_square_subsequent_mask(shape.horizon, dtype=torch.float64)
+    sq = lambda u: torch.cos(torch.as_tensor((u + 0.008) / 1.008 * math.pi / 2, dtype=torch.float64)) ** 2
+    beta = torch.stack([torch.clamp(1 - sq((i + 1) / T) / sq(i / T), max=0.999) for i in range(T)])
+    abar = torch.cumprod(1 - beta, 0)
+    half = d // 2
+    freq = torch.exp(-math.log(10000.0) * torch.arange(half, dtype=torch.float64) / (half - 1))
+    with torch.no_grad():
+        ln_f.weight.copy_(_t(P["lnf_g"])); ln_f.bias.copy_(_t(P["lnf_b"]))
+        o = obs_proj(_t(obs))                                  # [n][n_obs][d]
+        x = _t(noise[0])
+        n = x.shape[0]
+        for t in range(T):
+            k = T - 1 - t
+            tok = torch.cat([torch.sin(k * freq), torch.cos(k * freq)]).expand(n, 1, d)
+            mem = torch.cat([tok, o], 1) + _t(P["P_mem"])
+            h = in_proj(x) + _t(P["P_act"])
+            for layer in layers:
+                h = layer(h, mem, tgt_mask=mask)
+            eps = head(ln_f(h))
+            ab = abar[k]
+            ab_prev = abar[k - 1] if k > 0 else torch.tensor(1.0, dtype=torch.float64)
+            x = (x - beta[k] / torch.sqrt(1 - ab) * eps) / torch.sqrt(1 - beta[k])
+            if k > 0:
+                x = x + torch.sqrt((1 - ab_prev) / (1 - ab) * beta[k]) * _t(noise[t + 1])
+    return x.numpy()
+
+
+@pytest.mark.parametrize("shape", [TINY, I.PUSHT])
+def test_uncached_sampling_equals_torch_policy(shape):
+    """End to end: the oracle's whole uncached query (embedding, memory
+    tokens, every layer, head, T reverse steps) equals the policy rebuilt from
+    torch modules with the sampler in its epsilon form."""
+    w = I.make_weights(shape, 8, "perturbed")
+    P = O.prepare_params(I.split_weights(shape, w), "fp32")
+    obs, noise = I.make_obs(shape, 2, 8), I.make_noise(shape, 2, 8)
+    ours = O.denoise_group(shape, P, obs, noise, np.ones((3 * shape.n_layers, shape.n_steps), bool),
+                           clip=False, cache=False)
+    ref = _torch_policy_sample(shape, P, obs, noise)
+    np.testing.assert_allclose(ours, ref, rtol=0, atol=1e-9 * max(1.0, float(np.max(np.abs(ref)))))
 
 
 # ------------------------------------------------------------------ sampler
