@@ -423,7 +423,7 @@ int evo_create_encoder(const evo_encoder_desc* desc, const float* host_weights, 
                        evo_encoder** out);
 
 /* Encode `batch` images.  images: device float [batch][height][width]
- * [in_ch] (NHWC), read only.  features_out: device float, row n at
+ * [in_ch] (NHWC), read only, 16-byte aligned (EVO_E_INVALID otherwise).  features_out: device float, row n at
  * features_out + n * out_stride holds widths[n_stages-1] features (so
  * features can be written straight into a policy's observation rows);
  * other elements are not touched.  Asynchronous on hip_stream (NULL = the

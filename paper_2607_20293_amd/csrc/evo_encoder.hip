@@ -738,6 +738,9 @@ int evo_encode(evo_encoder* e, int32_t batch, const float* images, float* featur
   const evo_encoder_desc& d = e->desc;
   if (batch < 1 || batch > d.max_batch) return fail(EVO_E_INVALID, "batch %d outside [1, %d]", batch, d.max_batch);
   if (!images || !features_out) return fail(EVO_E_INVALID, "NULL device pointer");
+  // the convolutions read whole input pixels with 16-byte loads where the channel count allows
+  if (reinterpret_cast<uintptr_t>(images) % 16)
+    return fail(EVO_E_INVALID, "images must be 16-byte aligned");
   const int C_out = d.widths[d.n_stages - 1];
   if (out_stride < C_out) return fail(EVO_E_INVALID, "out_stride %d < feature size %d", out_stride, C_out);
   DeviceGuard guard(e->device);

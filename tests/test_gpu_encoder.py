@@ -106,6 +106,11 @@ def test_encoder_rejects_bad_arguments():
         enc.encode(x)                       # batch above max_batch
     with pytest.raises(evo.EvoError):
         evo.Encoder(e, I.make_encoder_weights(e, 3)[:-1], "fp32")
+    # a misaligned view of the images is refused before anything runs
+    flat = torch.zeros(1 + 2 * e.height * e.width * e.in_ch, device="cuda")
+    view = flat[1:].view(2, e.height, e.width, e.in_ch)
+    with pytest.raises(evo.EvoError, match="aligned"):
+        enc.encode(view)
 
 
 @pytest.mark.parametrize("dtype", ["fp32", "bf16"])
