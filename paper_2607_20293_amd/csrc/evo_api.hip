@@ -296,8 +296,12 @@ int evo_create_policy(const evo_policy_desc* desc, const float* host_weights, si
       // team variants (one sample per tile, `team` workgroups per tile) for
       // batches that fill at most n_cu workgroups; they need cooperative
       // launch.  With teams of 4 and 2 compiled, teams of 4 serve batches up to
-      // n_cu / 16 (latency-bound, the most parallel split wins) and teams of 2
-      // up to n_cu / 2; a single compiled size serves up to n_cu / team.
+      // n_cu / 16 and teams of 2 up to n_cu / 2; a single size serves up to
+      // n_cu / team.  With bf16 operands the automatic choice keeps only the
+      // smallest size: teams of 2 measured faster than teams of 4 at every
+      // batch from 1 to 32 (Push-T shape, 25% density: 4.19-4.25 ms against
+      // 4.37-4.64 ms), while with fp32 operands teams of 4 are far ahead at
+      // small batches (6.7 ms against 9.3 ms).
       // EVO_TEAM=0 switches teams off, EVO_TEAM=<size> keeps only that size.
       const char* env = std::getenv("EVO_TEAM");
       const int team_only = env ? std::atoi(env) : -1;
@@ -311,6 +315,9 @@ int evo_create_policy(const evo_policy_desc* desc, const float* host_weights, si
         for (int i = 0; i < nsz; ++i)
           if (sizes[i] == team_only) sizes[k++] = sizes[i];
         nsz = k;
+      } else if (s.dtype == EVO_BF16 && nsz > 1) {
+        sizes[0] = sizes[nsz - 1];  // sizes are sorted descending
+        nsz = 1;
       }
       int coop = 0;
       (void)hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, p->device);

@@ -112,8 +112,9 @@ def test_pusht_b1_single_workgroup(name):
 def test_team_variant_matches_single_workgroup(dtype, size):
     """Small batches run `size` workgroups per one-sample tile (heads and
     d_ff chunks split among them, partial residuals summed through memory;
-    teams of 4 up to n_cu/16 samples, teams of 2 up to n_cu/2, each forced
-    here with EVO_TEAM=<size>).  Both variants match the oracle on a ragged
+    automatic choice: fp32 teams of 4 up to n_cu/16 samples, then teams of 2
+    up to n_cu/2, bf16 teams of 2 up to n_cu/2; each size forced here with
+    EVO_TEAM=<size>).  Both variants match the oracle on a ragged
     batch with mixed unit-granular schedules, and each other to summation
     order."""
     s = I.PUSHT
@@ -226,7 +227,7 @@ def test_determinism_reset_and_independence():
     """Same inputs -> bitwise-same chunk; a call in between does not leak
     (caches are reset per query); a sample's chunk does not depend on the
     other samples of the batch or on its tile position.  The kernel variant
-    is chosen by batch size (teams of 4 below 17 samples, of 2 above), and
+    is chosen by batch size (for fp32, teams of 4 below 17 samples), and
     variants sum partial residuals in different orders, so the variant is
     fixed here (EVO_TEAM=2 serves both batch sizes)."""
     w = I.WORKLOADS["pusht_bf16_b64_d25"]
