@@ -295,13 +295,13 @@ int evo_create_policy(const evo_policy_desc* desc, const float* host_weights, si
       }
       // team variants (one sample per tile, `team` workgroups per tile) for
       // batches that fill at most n_cu workgroups; they need cooperative
-      // launch.  With teams of 4 and 2 compiled, teams of 4 serve batches up to
-      // n_cu / 16 and teams of 2 up to n_cu / 2; a single size serves up to
-      // n_cu / team.  With bf16 operands the automatic choice keeps only the
-      // smallest size: teams of 2 measured faster than teams of 4 at every
-      // batch from 1 to 32 (Push-T shape, 25% density: 4.19-4.25 ms against
-      // 4.37-4.64 ms), while with fp32 operands teams of 4 are far ahead at
-      // small batches (6.7 ms against 9.3 ms).
+      // launch.  A team size t serves batches up to n_cu / t, the largest
+      // compiled size that fits being chosen.  With bf16 operands the
+      // automatic choice keeps only the smallest size: teams of 2 measured
+      // faster than teams of 4 at every batch (Push-T shape, 25% density,
+      // batch 1 to 64: 4.19-4.31 ms against 4.37-4.85 ms), while with fp32
+      // operands teams of 4 are far ahead wherever they fit (6.7-6.8 ms
+      // against 9.3-9.5 ms up to batch 64).
       // EVO_TEAM=0 switches teams off, EVO_TEAM=<size> keeps only that size.
       const char* env = std::getenv("EVO_TEAM");
       const int team_only = env ? std::atoi(env) : -1;
@@ -327,7 +327,7 @@ int evo_create_policy(const evo_policy_desc* desc, const float* host_weights, si
         for (int i = nsz - 1; i >= 0; --i) {  // smallest team (largest batches) last in `teams`
           const int t = sizes[i];
           if (p->n_cu < t) continue;
-          const int cap = (nsz > 1 && t == sizes[0]) ? p->n_cu / (t * t) : p->n_cu / t;
+          const int cap = p->n_cu / t;
           evo_policy::TeamCfg tc;
           tc.team = t;
           tc.max_batch = std::min(s.max_batch, std::max(cap, 1));

@@ -112,7 +112,7 @@ def test_pusht_b1_single_workgroup(name):
 def test_team_variant_matches_single_workgroup(dtype, size):
     """Small batches run `size` workgroups per one-sample tile (heads and
     d_ff chunks split among them, partial residuals summed through memory;
-    automatic choice: fp32 teams of 4 up to n_cu/16 samples, then teams of 2
+    automatic choice: fp32 teams of 4 up to n_cu/4 samples, then teams of 2
     up to n_cu/2, bf16 teams of 2 up to n_cu/2; each size forced here with
     EVO_TEAM=<size>).  Both variants match the oracle on a ragged
     batch with mixed unit-granular schedules, and each other to summation
@@ -227,7 +227,7 @@ def test_determinism_reset_and_independence():
     """Same inputs -> bitwise-same chunk; a call in between does not leak
     (caches are reset per query); a sample's chunk does not depend on the
     other samples of the batch or on its tile position.  The kernel variant
-    is chosen by batch size (for fp32, teams of 4 below 17 samples), and
+    is chosen by batch size (for fp32, teams of 4 up to n_cu/4 samples), and
     variants sum partial residuals in different orders, so the variant is
     fixed here (EVO_TEAM=2 serves both batch sizes)."""
     w = I.WORKLOADS["pusht_bf16_b64_d25"]
@@ -418,3 +418,26 @@ def test_errors_leave_policy_usable():
     torch.cuda.synchronize()
     assert torch.isfinite(out).all()
     pol.close()
+
+
+def test_automatic_team_choice():
+    """The automatic team size follows the measured crossovers: bf16 runs
+    teams of 2 up to n_cu/2 samples; fp32 runs teams of 4 up to n_cu/4
+    samples, then teams of 2 up to n_cu/2; larger batches run one workgroup
+    per tile (stats report workgroups per tile)."""
+    import torch
+    n_cu = torch.cuda.get_device_properties(0).multi_processor_count
+    s = I.PUSHT
+    wts = I.make_weights(s, 0)
+    lt = I.make_lattice("dirichlet", s.n_layers, s.n_steps, 0.25, 0)
+    cases = [("bf16", 1, 2), ("bf16", n_cu // 4, 2), ("bf16", n_cu // 2, 2), ("bf16", n_cu // 2 + 1, 1),
+             ("fp32", 1, 4), ("fp32", n_cu // 4, 4), ("fp32", n_cu // 4 + 1, 2), ("fp32", n_cu // 2 + 1, 1)]
+    for dtype, B, want in cases:
+        say(f"[gpu] automatic team choice: {dtype} batch {B}")
+        pol = _policy(s, wts, dtype, B, 1)
+        pol.set_schedule(0, lt, O.GRAN_LAYER)
+        _, st = run_gpu(pol, I.make_obs(s, B, 0), I.make_noise(s, B, 0), np.zeros(B, np.int32))
+        pol.close()
+        per = st["n_workgroups"] // st["n_tiles"]
+        assert st["n_tiles"] == B, (dtype, B, st["n_tiles"])
+        assert per == want, f"{dtype} batch {B}: {per} workgroups per tile, expected {want}"
