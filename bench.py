@@ -156,10 +156,20 @@ def bench_encoder(dev):
     wts = I.make_weights(s, 0)
     img1 = imgs[:s.n_obs].contiguous()
     pa = {}
-    for dens in (0.25, 1.0):
-        lt = I.make_lattice("all" if dens == 1.0 else "dirichlet", s.n_layers, s.n_steps, dens, 0)
-        r = Runner(f"image_bf16_b1_{dens}", s, wts, "bf16", [lt], np.zeros(1, np.int32),
-                   I.make_obs(s, 1, 0), I.make_noise(s, 1, 0))
+    # the paper's wall-clock table rows (uncached, EVO at M = 8 and M = 10) in
+    # this policy's terms: the uncached loop, the fixed-interval M = 8 and
+    # M = 10 unit lattices, the printed EVO Push-T lattice (same 8 layers and
+    # 100 steps; M = 10), plus the 25%-density lattice of the headline
+    gold = os.path.join(ROOT, "tests", "golden", "schedules_pusht.txt")
+    U = 3 * s.n_layers
+    lats = {"0.25": (I.make_lattice("dirichlet", s.n_layers, s.n_steps, 0.25, 0), 0),
+            "1.0": (I.make_lattice("all", s.n_layers, s.n_steps, 1.0, 0), 0),
+            "fixed_interval_M8": (I.lattice_fixed_interval(U, s.n_steps, 8), 1),
+            "fixed_interval_M10": (I.lattice_fixed_interval(U, s.n_steps, 10), 1),
+            "printed_evo_M10": (I.printed_lattice(gold, "EVO", s.n_layers, s.n_steps), 1)}
+    for name, (lt, gran) in lats.items():
+        r = Runner(f"image_bf16_b1_{name}", s, wts, "bf16", [lt], np.zeros(1, np.int32),
+                   I.make_obs(s, 1, 0), I.make_noise(s, 1, 0), gran=gran)
         f1 = r.obs.view(s.n_obs, s.obs_dim)[:, :e.out_dim]
 
         def query():
@@ -182,11 +192,13 @@ def bench_encoder(dev):
             le.append((time.perf_counter() - t) * 1e3)
         r.pol.synchronize()
         r.close()
-        pa[str(dens)] = {"p50_ms": round(statistics.median(ls), 4), "encode_p50_ms": round(statistics.median(le), 4)}
+        pa[name] = {"p50_ms": round(statistics.median(ls), 4), "encode_p50_ms": round(statistics.median(le), 4)}
     enc.close()
     extras["encoder_robomimic_bf16_b512"] = {
         "frames_per_s": round(nf / (enc_ms * 1e-3), 1), "ms": round(enc_ms, 4), "TFLOPs": round(enc_tf, 2),
         "frac_peak": round(enc_tf / PEAK["bf16"], 4), "flops_per_frame": flops_frame}
+    for name in pa:
+        pa[name]["speedup_vs_uncached"] = round(pa["1.0"]["p50_ms"] / pa[name]["p50_ms"], 3)
     extras["predict_action_image_bf16_b1"] = pa
     log(f"[bench] encoder_robomimic_bf16_b512: {extras['encoder_robomimic_bf16_b512']}")
     log(f"[bench] predict_action_image_bf16_b1: {pa}")
