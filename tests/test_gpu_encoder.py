@@ -151,8 +151,9 @@ def test_encode_then_denoise_matches_oracle_chain(dtype):
 
 @pytest.mark.parametrize("dtype", ["fp32", "bf16"])
 def test_encoder_large_tiles_sampled_frames(dtype):
-    """A batch large enough for the 128x128 and 128x64 convolution tiles
-    (no K split), checked on sampled frames: frames are independent, so the
+    """A batch large enough that no convolution splits K (thousands of
+    output tiles, ragged in channels nowhere and in pixels at the last
+    stage), checked on sampled frames: frames are independent, so the
     oracle runs on those frames alone."""
     torch = _torch()
     from paper_2607_20293_amd import evo
