@@ -38,8 +38,12 @@ constexpr int kThreads = 256;
 constexpr int kTargetWG = 512;      // split K below this many output tiles
 constexpr int kMaxSplit = 16;
 constexpr long long kWsFloats = 1024ll * 4096;  // split-K partials (>= splits * tiles * 64 * 64)
-constexpr int kGnTarget = 1024;     // GroupNorm workgroups aimed at when chunking pixels
-constexpr int kMaxPart = 16 * 1024; // partial statistics beyond one per (image, group)
+// GroupNorm workgroups aimed at when chunking an image's pixels (statistics
+// and apply passes).  The chunking follows the batch size, so across batch
+// sizes the statistics may be summed in other groupings (last-bit
+// differences); for one batch size an image's result does not depend on the
+// other images.  (Fixed chunks of 64 or 128 pixels measured 3-8% slower.)
+constexpr int kGnTarget = 1024;
 
 template <class AT> struct ConvStep;
 template <> struct ConvStep<__bf16> {
@@ -311,9 +315,14 @@ __global__ void __launch_bounds__(kThreads) gn_stats_kernel(const GnArgs a) {
     const size_t i0 = base + ch * CW + j * a.G;
     if (!split) {
       x0 = a.x[i0];
-    } else {
-      x0 = a.ws[i0];
-      for (int z = 1; z < a.splits; ++z) x0 += a.ws[(long long)z * a.split_stride + i0];
+    } else {  // all partials requested before the first is added (same order of additions)
+      float t[kMaxSplit];
+#pragma unroll
+      for (int z = 0; z < kMaxSplit; ++z) t[z] = z < a.splits ? a.ws[(long long)z * a.split_stride + i0] : 0.f;
+      x0 = t[0];
+#pragma unroll
+      for (int z = 1; z < kMaxSplit; ++z)
+        if (z < a.splits) x0 += t[z];
     }
   }
   float s = 0.f, q = 0.f;
@@ -323,8 +332,15 @@ __global__ void __launch_bounds__(kThreads) gn_stats_kernel(const GnArgs a) {
     if (!split) {
       v = *reinterpret_cast<const f32x4*>(a.x + i);
     } else {
-      v = *reinterpret_cast<const f32x4*>(a.ws + i);
-      for (int z = 1; z < a.splits; ++z) v += *reinterpret_cast<const f32x4*>(a.ws + (long long)z * a.split_stride + i);
+      f32x4 t[kMaxSplit];
+#pragma unroll
+      for (int z = 0; z < kMaxSplit; ++z)
+        t[z] = z < a.splits ? *reinterpret_cast<const f32x4*>(a.ws + (long long)z * a.split_stride + i)
+                            : f32x4{0.f, 0.f, 0.f, 0.f};
+      v = t[0];
+#pragma unroll
+      for (int z = 1; z < kMaxSplit; ++z)
+        if (z < a.splits) v += t[z];
       *reinterpret_cast<f32x4*>(a.x + i) = v;
     }
     const f32x4 d = v - x0;
@@ -364,19 +380,47 @@ __global__ void __launch_bounds__(kThreads) gn_apply_kernel(const GnArgs a) {
   const int tid = threadIdx.x, col = tid % Q, prow = tid / Q;
   const int c = ch * CW + col * 4, j = (col * 4) / a.G;
   const size_t base = (size_t)n * HW * a.C;
+  // merge the partials of each of the gpw groups (a fixed order per chunk
+  // count): one thread per group when there are few, else L = kThreads / gpw
+  // threads per group, thread l summing partials l, l + L, ..., then a tree
+  // over l
   __shared__ float2 st[16];
-  if (tid < a.gpw) {
-    const int g = ch * a.gpw + tid;
-    const double2* pp = a.part + ((size_t)n * groups + g) * a.ps_stats;
-    double S = 0.0, Qs = 0.0;
-    for (int k = 0; k < a.ps_stats; ++k) {
-      S += pp[k].x;
-      Qs += pp[k].y;
-    }
+  __shared__ double2 mrg[kThreads];
+  const auto finish = [&](int jg, double S, double Qs) {
+    const int g = ch * a.gpw + jg;
     const double cnt = (double)HW * a.G, m = S / cnt;
     const double var = std::max(Qs / cnt - m * m, 0.0);
     const float x0 = a.shift[(size_t)n * groups + g];
-    st[tid] = make_float2((float)((double)x0 + m), (float)(1.0 / std::sqrt(var + (double)a.eps)));
+    st[jg] = make_float2((float)((double)x0 + m), (float)(1.0 / std::sqrt(var + (double)a.eps)));
+  };
+  if (a.ps_stats <= 8) {
+    if (tid < a.gpw) {
+      const double2* pp = a.part + ((size_t)n * groups + ch * a.gpw + tid) * a.ps_stats;
+      double S = 0.0, Qs = 0.0;
+      for (int k = 0; k < a.ps_stats; ++k) {
+        S += pp[k].x;
+        Qs += pp[k].y;
+      }
+      finish(tid, S, Qs);
+    }
+  } else {
+    const int L = kThreads / a.gpw, jg = tid / L, l = tid - jg * L;
+    const double2* pp = a.part + ((size_t)n * groups + ch * a.gpw + jg) * a.ps_stats;
+    double S = 0.0, Qs = 0.0;
+    for (int k = l; k < a.ps_stats; k += L) {
+      S += pp[k].x;
+      Qs += pp[k].y;
+    }
+    mrg[tid] = make_double2(S, Qs);
+    __syncthreads();
+    for (int h = L >> 1; h > 0; h >>= 1) {
+      if (l < h) {
+        mrg[tid].x += mrg[tid + h].x;
+        mrg[tid].y += mrg[tid + h].y;
+      }
+      __syncthreads();
+    }
+    if (l == 0) finish(jg, mrg[tid].x, mrg[tid].y);
   }
   __syncthreads();
   const float2 ms = st[j];
@@ -476,7 +520,8 @@ struct evo_encoder {
   float* ws = nullptr;           // split-K partials, kWsFloats
   double2* part = nullptr;       // GroupNorm partial statistics
   size_t part_cap = 0;
-  float* shift = nullptr;        // GroupNorm shifts, part_cap floats
+  float* shift = nullptr;        // GroupNorm shifts [image][group]
+  size_t shift_cap = 0;
   uint64_t flops_per_image = 0;
 };
 
@@ -593,8 +638,8 @@ hipError_t launch_gn(const evo_encoder* e, const ConvLayer& L, GnArgs g, int N, 
   while (gpw * 2 * G <= 64 && groups % (gpw * 2) == 0) gpw *= 2;
   const int chunks = groups / gpw, HW = H * W;
   const int base = N * chunks;
-  int ps = std::max(1, std::min(cdiv(kGnTarget, base), cdiv(HW, 16)));
-  if ((size_t)N * groups * ps > e->part_cap) ps = std::max(1, (int)(e->part_cap / ((size_t)N * groups)));
+  const int ps = std::max(1, std::min(cdiv(kGnTarget, base), cdiv(HW, 16)));
+  if ((size_t)N * groups * ps > e->part_cap) return hipErrorInvalidValue;  // sized at creation
   g.gamma = L.gamma;
   g.beta = L.beta;
   g.res = res;
@@ -656,13 +701,14 @@ int evo_create_encoder(const evo_encoder_desc* desc, const float* host_weights, 
                   hipGetErrorString(e_));                                                      \
   } while (0)
     // activation sizes and FLOPs: walk the network once
-    size_t maxact = 0;
+    size_t maxact = 0, maxpart = 0;  // per image: activation floats, GroupNorm partials
     int maxgroups = 0;
     uint64_t flops = 0;
     {
       int h = out_size(desc->height, 7, 2, 3), w = out_size(desc->width, 7, 2, 3);
       maxact = std::max(maxact, (size_t)h * w * desc->stem_ch);
       maxgroups = desc->stem_ch / desc->gn_group;
+      maxpart = (size_t)maxgroups * cdiv((long long)h * w, 16);
       flops += 2ull * h * w * desc->stem_ch * 49 * desc->in_ch;
       h = out_size(h, 3, 2, 1);
       w = out_size(w, 3, 2, 1);
@@ -674,6 +720,7 @@ int evo_create_encoder(const evo_encoder_desc* desc, const float* host_weights, 
           if (ho < 1 || wo < 1) return fail(EVO_E_INVALID, "the image is too small for the network");
           maxact = std::max(maxact, (size_t)ho * wo * c);
           maxgroups = std::max(maxgroups, c / desc->gn_group);
+          maxpart = std::max(maxpart, (size_t)(c / desc->gn_group) * cdiv((long long)ho * wo, 16));
           flops += 2ull * ho * wo * c * 9 * cin + 2ull * ho * wo * c * 9 * c;
           if (stride != 1 || cin != c) flops += 2ull * ho * wo * c * cin;
           h = ho;
@@ -685,7 +732,8 @@ int evo_create_encoder(const evo_encoder_desc* desc, const float* host_weights, 
       return fail(EVO_E_UNSUPPORTED, "activations of max_batch images exceed 2^31 floats");
     e->flops_per_image = flops;
     e->buf_floats = maxact * desc->max_batch;
-    e->part_cap = (size_t)desc->max_batch * maxgroups + kMaxPart;
+    e->part_cap = (size_t)desc->max_batch * maxpart;
+    e->shift_cap = (size_t)desc->max_batch * maxgroups;
     ENC_TRY(hipMalloc(&e->d_raw, n_floats * sizeof(float)));
     ENC_TRY(hipMemcpy(e->d_raw, host_weights, n_floats * sizeof(float), hipMemcpyHostToDevice));
     e->convs = enc_layers(desc);
@@ -706,7 +754,7 @@ int evo_create_encoder(const evo_encoder_desc* desc, const float* host_weights, 
     for (int i = 0; i < 4; ++i) ENC_TRY(hipMalloc(&e->buf[i], e->buf_floats * sizeof(float)));
     ENC_TRY(hipMalloc(&e->ws, (size_t)kWsFloats * sizeof(float)));
     ENC_TRY(hipMalloc(&e->part, e->part_cap * sizeof(double2)));
-    ENC_TRY(hipMalloc(&e->shift, e->part_cap * sizeof(float)));
+    ENC_TRY(hipMalloc(&e->shift, e->shift_cap * sizeof(float)));
     ENC_TRY(hipDeviceSynchronize());
 #undef ENC_TRY
     *out = e;
