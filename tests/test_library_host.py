@@ -236,3 +236,20 @@ def test_encoder_descriptor_validation():
     assert count(dtype=3) == -1
     assert count(max_batch=0) == -1
     assert count(max_batch=60000, height=4096, width=4096) == -5   # pixel indices beyond 32 bits
+
+
+def test_encoder_calls_reject_null_handles_without_a_device():
+    """Argument checks run before any device work, so they hold on a host
+    without a GPU: NULL encoder handles and output pointers are refused and
+    destroying NULL is a no-op."""
+    L = _lib_or_skip()
+    import ctypes
+    assert L.evo_encode(None, 1, None, None, 512, None) == -1
+    assert "NULL" in L.evo_last_error().decode()
+    v = ctypes.c_uint64()
+    assert L.evo_encoder_flops(None, 1, ctypes.byref(v)) == -1
+    L.evo_destroy_encoder(None)
+    d = evo.make_encoder_desc(I.ENC_TINY, "fp32", 2)
+    out = ctypes.c_void_p()
+    assert L.evo_create_encoder(ctypes.byref(d), None, 10, ctypes.byref(out)) == -1
+    assert out.value is None
