@@ -196,3 +196,36 @@ def test_encoder_odd_shape(dtype):
     else:
         print("odd bf16 rel", _rel(got, want))
         assert _rel(got, want) <= 3e-2
+
+
+def test_image_policy_query_matches_oracle_chain():
+    """The image policy's own configuration: 84x84 frames, 512 features
+    written into observation rows of 521 floats (an odd row stride, the
+    9 proprioceptive columns kept), then the cached loop with a 25% lattice
+    in bf16; two samples against the oracle encoder followed by the oracle
+    loop."""
+    torch = _torch()
+    from paper_2607_20293_amd import evo
+    e, s = I.ENC_ROBOMIMIC, I.IMAGE
+    assert s.obs_dim - e.out_dim == 9
+    B = 2
+    ew, pw = I.make_encoder_weights(e, 41, "perturbed"), I.make_weights(s, 41, "perturbed")
+    imgs = I.make_images(e, B * s.n_obs, 41)
+    obs, noise = I.make_obs(s, B, 41), I.make_noise(s, B, 41)
+    lats = [I.make_lattice("dirichlet", s.n_layers, s.n_steps, 0.25, 41)]
+    ids = np.zeros(B, np.int32)
+    enc = evo.Encoder(e, ew, "bf16", max_batch=B * s.n_obs)
+    pol = evo.Policy(s, pw, dtype="bf16", max_batch=B, max_schedules=1)
+    pol.set_schedule(0, lats[0], evo.GRAN_LAYER)
+    obs_d = torch.from_numpy(obs).cuda()
+    enc.encode(torch.from_numpy(imgs).cuda(), out=obs_d.view(B * s.n_obs, s.obs_dim)[:, :e.out_dim])
+    got = pol.denoise(obs_d, torch.from_numpy(noise).cuda(), ids).cpu().numpy()
+    assert np.array_equal(obs_d[:, :, e.out_dim:].cpu().numpy(), obs[:, :, e.out_dim:])
+    pol.close()
+    enc.close()
+    f = E.encode(e, I.split_encoder_weights(e, ew), imgs, "bf16")
+    obs_ref = obs.astype(np.float64)
+    obs_ref[:, :, :e.out_dim] = f.reshape(B, s.n_obs, e.out_dim)
+    ref, _ = O.denoise(s, I.split_weights(s, pw), obs_ref, noise, lats, ids, granularity=O.GRAN_LAYER,
+                       cold_policy=O.COLD_COMPUTE, clip=True, dtype="bf16")
+    compare(got, ref, "bf16", "image policy query bf16")
