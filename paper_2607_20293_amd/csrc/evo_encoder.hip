@@ -8,9 +8,10 @@
 // padded to the K step).  The A tile is gathered from the input with the
 // convolution's padding on the fly (no im2col buffer), converted to the
 // operand type and double-buffered in LDS with the next step's global loads
-// in flight during the current step's MFMAs, in 64 x 64 output tiles.  Layers with few output tiles
-// (small batches, late stages) split K over workgroups into partial
-// outputs that the GroupNorm statistics pass sums in a fixed order.
+// in flight during the current step's MFMAs, in 64 x 64 output tiles.
+// Layers with few output tiles (small batches, late stages) split K over
+// workgroups into partial outputs that the GroupNorm statistics pass sums
+// in a fixed order.
 //
 // GroupNorm is two passes per layer: partial statistics over pixel chunks
 // (shifted sums, fp64 across threads and chunks), then an apply pass that
