@@ -441,3 +441,31 @@ def test_automatic_team_choice():
         per = st["n_workgroups"] // st["n_tiles"]
         assert st["n_tiles"] == B, (dtype, B, st["n_tiles"])
         assert per == want, f"{dtype} batch {B}: {per} workgroups per tile, expected {want}"
+
+
+def test_replacing_a_schedule_between_calls():
+    """The plan upload is skipped when the plan bytes are unchanged, so a
+    schedule replaced under the same id (same batch, same ids) must still
+    take effect: each call matches the oracle of the schedule registered at
+    the time, also across a layer -> unit granularity change, and returning
+    to the first schedule gives the first call's bits again."""
+    s = I.TINY
+    wts = I.make_weights(s, 7, "perturbed")
+    obs, noise = I.make_obs(s, 3, 7), I.make_noise(s, 3, 7)
+    ids = np.zeros(3, np.int32)
+    rng = np.random.default_rng([7, 3])
+    lat_a = I.lattice_bernoulli(s.n_layers, s.n_steps, 0.3, rng)
+    lat_b = I.lattice_bernoulli(3 * s.n_layers, s.n_steps, 0.6, rng)
+    pol = _policy(s, wts, "fp32", 3, 1)
+    seq = [(lat_a, O.GRAN_LAYER), (lat_b, O.GRAN_UNIT), (lat_a, O.GRAN_LAYER)]
+    outs = []
+    for lat, gran in seq:
+        say(f"[gpu] replace schedule 0: granularity {gran}")
+        pol.set_schedule(0, lat, gran)
+        got, _ = run_gpu(pol, obs, noise, ids)
+        ref, _ = run_oracle(s, wts, obs, noise, [lat], ids, gran, O.COLD_COMPUTE, "fp32")
+        compare(got, ref, "fp32", f"schedule granularity {gran}")
+        outs.append(got)
+    pol.close()
+    assert not np.array_equal(outs[0], outs[1])
+    assert np.array_equal(outs[0], outs[2])
