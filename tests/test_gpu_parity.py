@@ -469,3 +469,32 @@ def test_replacing_a_schedule_between_calls():
     pol.close()
     assert not np.array_equal(outs[0], outs[1])
     assert np.array_equal(outs[0], outs[2])
+
+
+def test_calls_on_two_streams_are_ordered():
+    """A call on another stream than the previous call waits for it (the
+    plan, caches and observation keys/values are per-policy buffers): two
+    back-to-back calls on two streams, with no host synchronisation between
+    them, both match the oracle."""
+    import torch
+    device()
+    s = I.TINY
+    wts = I.make_weights(s, 8, "perturbed")
+    lat = I.lattice_bernoulli(s.n_layers, s.n_steps, 0.5, np.random.default_rng([8, 3]))
+    pol = _policy(s, wts, "fp32", 2, 1)
+    pol.set_schedule(0, lat, O.GRAN_LAYER)
+    ids = np.zeros(2, np.int32)
+    ins = [(I.make_obs(s, 2, 81 + k), I.make_noise(s, 2, 81 + k)) for k in range(2)]
+    dev = torch.device("cuda:0")
+    t_in = [(torch.from_numpy(o).to(dev), torch.from_numpy(n).to(dev)) for o, n in ins]
+    outs = [torch.empty((2, s.horizon, s.action_dim), dtype=torch.float32, device=dev) for _ in range(2)]
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]   # default priority
+    torch.cuda.synchronize()
+    for k in range(2):
+        pol.denoise(t_in[k][0], t_in[k][1], ids, out=outs[k], stream=streams[k])
+    torch.cuda.synchronize()
+    pol.synchronize()
+    for k in range(2):
+        ref, _ = run_oracle(s, wts, ins[k][0], ins[k][1], [lat], ids, O.GRAN_LAYER, O.COLD_COMPUTE, "fp32")
+        compare(outs[k].cpu().numpy(), ref, "fp32", f"stream {k}")
+    pol.close()
