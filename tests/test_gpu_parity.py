@@ -498,3 +498,45 @@ def test_calls_on_two_streams_are_ordered():
         ref, _ = run_oracle(s, wts, ins[k][0], ins[k][1], [lat], ids, O.GRAN_LAYER, O.COLD_COMPUTE, "fp32")
         compare(outs[k].cpu().numpy(), ref, "fp32", f"stream {k}")
     pol.close()
+
+
+@pytest.mark.parametrize("cold", [O.COLD_ZERO, O.COLD_COMPUTE])
+def test_empty_schedule(cold):
+    """K = 0 (Eq. 3 with no pairs): with the zero cold-cache reading no unit
+    is ever evaluated (every residual is zero, the chunk comes from the
+    embedding, head and sampler alone); with the compute reading every unit
+    runs at step 0 only.  Both match the oracle."""
+    s = I.TINY
+    wts = I.make_weights(s, 9, "perturbed")
+    obs, noise = I.make_obs(s, 2, 9), I.make_noise(s, 2, 9)
+    ids = np.zeros(2, np.int32)
+    pol = _policy(s, wts, "fp32", 2, 1, cold=cold)
+    pol.set_schedule_pairs(0, np.zeros((0, 2), np.int32), O.GRAN_UNIT)
+    got, st = run_gpu(pol, obs, noise, ids)
+    empty = np.zeros((3 * s.n_layers, s.n_steps), np.uint8)
+    ref, ost = run_oracle(s, wts, obs, noise, [empty], ids, O.GRAN_UNIT, cold, "fp32")
+    compare(got, ref, "fp32", f"empty schedule, cold {cold}")
+    check_stats(st, ost)
+    assert st["refreshes_effective"] == (0 if cold == O.COLD_ZERO else 2 * 3 * s.n_layers)
+    pol.close()
+
+
+def test_empty_batch_is_refused():
+    """A batch of zero samples (or frames) is refused before any device work."""
+    import torch
+    dev = device()
+    s = I.TINY
+    pol = _policy(s, I.make_weights(s, 0), "fp32", 2, 1)
+    pol.set_schedule(0, np.ones((2, 10), np.uint8), O.GRAN_LAYER)
+    obs = torch.zeros((0, s.n_obs, s.obs_dim), device=dev)
+    noise = torch.zeros((s.n_steps, 0, s.horizon, s.action_dim), device=dev)
+    with pytest.raises(evo.EvoError) as e:
+        pol.denoise(obs, noise, None)
+    assert e.value.code == -1
+    pol.close()
+    en = I.ENC_TINY
+    enc = evo.Encoder(en, I.make_encoder_weights(en, 0), "fp32", max_batch=2)
+    with pytest.raises(evo.EvoError) as e:
+        enc.encode(torch.zeros((0, en.height, en.width, en.in_ch), device=dev))
+    assert e.value.code == -1
+    enc.close()
