@@ -540,3 +540,16 @@ def test_empty_batch_is_refused():
         enc.encode(torch.zeros((0, en.height, en.width, en.in_ch), device=dev))
     assert e.value.code == -1
     enc.close()
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_maximum_step_count(dtype):
+    """170 reverse steps (the largest count the two-sample tiles hold), a
+    ragged batch of 3 and a 30% lattice, against the oracle."""
+    from dataclasses import replace
+    s = replace(I.TINY, n_steps=170)
+    wts = I.make_weights(s, 10, "perturbed")
+    obs, noise = I.make_obs(s, 3, 10), I.make_noise(s, 3, 10)
+    lat = I.lattice_bernoulli(s.n_layers, s.n_steps, 0.3, np.random.default_rng([10, 3]))
+    pol, *_ = _case(f"tiny_T170_{dtype}", s, wts, obs, noise, [lat], np.zeros(3, np.int32), dtype)
+    pol.close()

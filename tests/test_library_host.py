@@ -253,3 +253,13 @@ def test_encoder_calls_reject_null_handles_without_a_device():
     out = ctypes.c_void_p()
     assert L.evo_create_encoder(ctypes.byref(d), None, 10, ctypes.byref(out)) == -1
     assert out.value is None
+
+
+def test_maximum_step_count():
+    """The per-tile step masks live in LDS (341 entries of 3 x u64): with
+    two-sample tiles, 170 steps fit and 171 are refused as unsupported."""
+    _lib_or_skip()
+    from dataclasses import replace
+    assert evo.check_desc(evo.make_desc(replace(I.TINY, n_steps=170), "fp32", 2, 1)) == 0
+    assert evo.check_desc(evo.make_desc(replace(I.TINY, n_steps=171), "fp32", 2, 1)) == -5
+    assert "n_steps 171" in evo.lib().evo_last_error().decode()
