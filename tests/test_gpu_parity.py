@@ -553,3 +553,19 @@ def test_maximum_step_count(dtype):
     lat = I.lattice_bernoulli(s.n_layers, s.n_steps, 0.3, np.random.default_rng([10, 3]))
     pol, *_ = _case(f"tiny_T170_{dtype}", s, wts, obs, noise, [lat], np.zeros(3, np.int32), dtype)
     pol.close()
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+@pytest.mark.parametrize("base", ["tiny", "pusht"])
+def test_maximum_obs_tokens_and_action_dim(base, dtype):
+    """7 observation tokens (8 memory tokens) and 16 action dims, the largest
+    compiled, on a ragged batch of 3 with a mixed pair of schedules (the
+    Push-T shape at batch 3 runs the small-batch team variant)."""
+    from dataclasses import replace
+    s = replace(I.TINY if base == "tiny" else I.PUSHT, n_obs=7, action_dim=16)
+    wts = I.make_weights(s, 11, "perturbed")
+    obs, noise = I.make_obs(s, 3, 11), I.make_noise(s, 3, 11)
+    rng = np.random.default_rng([11, 3])
+    lats = [I.lattice_bernoulli(s.n_layers, s.n_steps, p, rng) for p in (0.3, 0.7)]
+    pol, *_ = _case(f"{base}_obs7_a16_{dtype}", s, wts, obs, noise, lats, np.array([1, 0, 1], np.int32), dtype)
+    pol.close()

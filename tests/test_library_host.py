@@ -263,3 +263,16 @@ def test_maximum_step_count():
     assert evo.check_desc(evo.make_desc(replace(I.TINY, n_steps=170), "fp32", 2, 1)) == 0
     assert evo.check_desc(evo.make_desc(replace(I.TINY, n_steps=171), "fp32", 2, 1)) == -5
     assert "n_steps 171" in evo.lib().evo_last_error().decode()
+
+
+def test_maximum_obs_tokens_and_action_dim():
+    """Memory tokens per sample (1 + n_obs) must fit the compiled slot count
+    and action_dim 16 is the largest head: 7 observation tokens and 16 action
+    dims are accepted, 8 tokens or 17 dims refused as unsupported."""
+    _lib_or_skip()
+    from dataclasses import replace
+    for base in (I.TINY, I.PUSHT):
+        assert evo.check_desc(evo.make_desc(replace(base, n_obs=7, action_dim=16), "bf16", 2, 1)) == 0
+        assert evo.check_desc(evo.make_desc(replace(base, n_obs=8), "bf16", 2, 1)) == -5
+        assert evo.check_desc(evo.make_desc(replace(base, action_dim=17), "bf16", 2, 1)) == -5
+    assert evo.check_desc(evo.make_desc(replace(I.BIMANUAL, n_obs=5), "bf16", 2, 1)) == -5
