@@ -13,6 +13,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libevo.so")
+DEMO = os.path.join(HERE, "evo_demo")
 SOURCES = ["evo_host.cpp", "evo_ga.cpp", "evo_kernels.hip", "evo_redundancy.hip", "evo_search.hip", "evo_encoder.hip",
            "evo_api.hip"]
 ARCH = os.environ.get("EVO_OFFLOAD_ARCH", "gfx950")
@@ -56,6 +57,13 @@ def build(verbose: bool = False) -> str:
     if r.returncode != 0:
         raise RuntimeError(f"link failed: {' '.join(cmd)}\n{r.stderr}")
     os.replace(tmp, LIB)
+    # the C ABI without Python: examples/evo_demo.cpp linked against the library
+    demo = os.path.join(HERE, "examples", "evo_demo.cpp")
+    cmd = [hipcc] + flags() + [demo, "-o", DEMO + ".tmp", "-L", HERE, "-levo", "-Wl,-rpath,$ORIGIN"]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"demo build failed: {' '.join(cmd)}\n{r.stderr}")
+    os.replace(DEMO + ".tmp", DEMO)
     return LIB
 
 
