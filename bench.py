@@ -256,7 +256,7 @@ def main():
     achieved = st["flops_kernel"] / (k_avg_ms * 1e-3) / 1e12
     roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK[w.dtype], "unit": "TFLOP/s",
             "frac": round(achieved / PEAK[w.dtype], 4), "traffic": None,
-            "kernel": "denoise_kernel", "kernel_ms": round(k_avg_ms, 4),
+            "kernel": "obs_fold_kernel + denoise_kernel", "kernel_ms": round(k_avg_ms, 4),
             "flops_per_launch": st["flops_kernel"],
             "weight_stream_GBps": round(st["weight_bytes"] / (k_avg_ms * 1e-3) / 1e9, 1)}
     if os.path.exists(COUNTERS):

@@ -81,7 +81,12 @@ typedef struct {
  * flops_kernel is what this implementation multiplies: the cross-attention
  * key/value products of the observation tokens are done once per query and
  * those of the time token once per policy, so they are not repeated at
- * each refresh.  The byte counters are this implementation's algorithmic
+ * each refresh.  Policies of width 256 whose n_heads x S <= 16 run the
+ * cross-attention folded: W_q and W_o2 are applied once per memory token
+ * (per query for the observation tokens, at creation for the time token)
+ * and an evaluation multiplies only against the S x n_heads folded
+ * columns, so there F_CA counts 2(2 H S n_heads d) per evaluation and the
+ * query adds 4 n_obs d^2 per layer for the fold.  The byte counters are this implementation's algorithmic
  * traffic: cache reads/writes of reused/refreshed residuals, and weight
  * bytes of evaluated units summed over workgroups.  n_tiles counts the
  * sample tiles, n_workgroups the workgroups launched (small batches run

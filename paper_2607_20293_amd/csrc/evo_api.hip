@@ -75,6 +75,7 @@ struct evo_policy {
   LayerOff* d_loff = nullptr;
   PackOff* d_poff = nullptr;
   float* d_tkv = nullptr;
+  float* d_tfold = nullptr;  // time-token fold records (folded cross-attention)
   float* d_ddpm = nullptr;
   float* d_cache = nullptr;
   size_t cache_floats = 0;
@@ -124,6 +125,7 @@ static void release(evo_policy* p) {
   (void)hipFree(p->d_loff);
   (void)hipFree(p->d_poff);
   (void)hipFree(p->d_tkv);
+  (void)hipFree(p->d_tfold);
   (void)hipFree(p->d_ddpm);
   (void)hipFree(p->d_cache);
   (void)hipFree(p->d_okv);
@@ -199,8 +201,22 @@ int evo_create_policy(const evo_policy_desc* desc, const float* host_weights, si
     const int L = s.L, d = s.d, T = s.T, U = s.U();
     const int KF = s.dtype == EVO_BF16 ? 32 : 16;
     // fp32 parameter copy (biases, norms, embeddings, head, and the source of the packed matrices)
-    CREATE_TRY(hipMalloc(&p->d_raw, wo.total * sizeof(float)));
+    // (folded cross-attention: followed by the transpose of every layer's W_o2)
+    const bool fold = s.folds_ca();
+    const size_t tr_off = (wo.total + 63) / 64 * 64;  // 256-byte aligned
+    const size_t raw_floats = fold ? tr_off + (size_t)L * d * d : wo.total;
+    CREATE_TRY(hipMalloc(&p->d_raw, raw_floats * sizeof(float)));
     CREATE_TRY(hipMemcpy(p->d_raw, host_weights, wo.total * sizeof(float), hipMemcpyHostToDevice));
+    if (fold) {
+      std::vector<float> tr((size_t)L * d * d);
+      for (int l = 0; l < L; ++l) {
+        const float* W = static_cast<const float*>(host_weights) + wo.layer[l].W_o2;
+        float* o = tr.data() + (size_t)l * d * d;
+        for (int c = 0; c < d; ++c)
+          for (int e = 0; e < d; ++e) o[(size_t)e * d + c] = W[(size_t)c * d + e];
+      }
+      CREATE_TRY(hipMemcpy(p->d_raw + tr_off, tr.data(), tr.size() * sizeof(float), hipMemcpyHostToDevice));
+    }
 
     // packed projection matrices
     auto frag16 = [&](int N, int Kpad) { return (uint64_t)(N / 16) * (Kpad / KF) * 64; };
@@ -251,7 +267,9 @@ int evo_create_policy(const evo_policy_desc* desc, const float* host_weights, si
       lo.b_q = (uint32_t)y.b_q; lo.b_kv = (uint32_t)y.b_kv; lo.b_o2 = (uint32_t)y.b_o2;
       lo.ln3_g = (uint32_t)y.ln3_g; lo.ln3_b = (uint32_t)y.ln3_b; lo.b_1 = (uint32_t)y.b_1;
       lo.b_2 = (uint32_t)y.b_2;
-      lo.pad_[0] = lo.pad_[1] = lo.pad_[2] = 0;
+      lo.w_q = (uint32_t)y.W_q;
+      lo.w_o2t = fold ? (uint32_t)(tr_off + (size_t)l * d * d) : 0u;
+      lo.pad_ = 0;
       wkv[l] = (uint32_t)y.W_kv;
       bkv[l] = (uint32_t)y.b_kv;
     }
@@ -272,6 +290,9 @@ int evo_create_policy(const evo_policy_desc* desc, const float* host_weights, si
       if (e == hipSuccess) e = hipMemcpy(d_bkv, bkv.data(), L * sizeof(uint32_t), hipMemcpyHostToDevice);
       if (e == hipSuccess)
         e = launch_time_kv(p->d_raw, (uint32_t)wo.P_mem, d_wkv, d_bkv, T, L, d, s.dtype, rows, p->d_tkv, 0);
+      if (e == hipSuccess && fold) e = hipMalloc(&p->d_tfold, (size_t)T * L * s.fold_rec() * sizeof(float));
+      if (e == hipSuccess && fold)
+        e = launch_time_fold(p->d_raw, p->d_loff, p->d_tkv, T, L, d, s.dh(), s.dtype, p->d_tfold, 0);
       if (e == hipSuccess) e = hipDeviceSynchronize();
       (void)hipFree(d_wkv);
       (void)hipFree(d_bkv);
@@ -321,7 +342,8 @@ int evo_create_policy(const evo_policy_desc* desc, const float* host_weights, si
       }
       int coop = 0;
       (void)hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, p->device);
-      const size_t okv_per = (size_t)L * s.n_obs * 2 * d;
+      // observation keys/values, or their fold records
+      const size_t okv_per = (size_t)L * s.n_obs * (fold ? s.fold_rec() : 2 * d);
       size_t okv_floats = (size_t)s.max_batch * okv_per, xchg_rows = 0, ctr_tiles = 0;
       if (coop) {
         for (int i = nsz - 1; i >= 0; --i) {  // smallest team (largest batches) last in `teams`
@@ -334,7 +356,7 @@ int evo_create_policy(const evo_policy_desc* desc, const float* host_weights, si
           tc.okv_stride = (size_t)tc.max_batch * okv_per;
           p->teams.insert(p->teams.begin(), tc);
           rows = std::max(rows, (size_t)tc.max_batch * t * s.H);
-          okv_floats = std::max(okv_floats, tc.okv_stride * t);
+          if (!fold) okv_floats = std::max(okv_floats, tc.okv_stride * t);  // fold records: one shared copy
           xchg_rows = std::max(xchg_rows, (size_t)tc.max_batch * t * s.H);
           ctr_tiles = std::max(ctr_tiles, (size_t)tc.max_batch);
         }
@@ -497,6 +519,8 @@ static int denoise_impl(evo_policy* p, int32_t batch, const float* obs_cond, con
     kp.b_obs = (uint32_t)wo.b_obs; kp.P_mem = (uint32_t)wo.P_mem; kp.lnf_g = (uint32_t)wo.lnf_g;
     kp.lnf_b = (uint32_t)wo.lnf_b; kp.W_out = (uint32_t)wo.W_out; kp.b_out = (uint32_t)wo.b_out;
     kp.tkv = p->d_tkv; kp.ddpm = p->d_ddpm;
+    kp.fold = s.folds_ca() ? 1 : 0;
+    kp.tfold = p->d_tfold;
     kp.tile_sample = reinterpret_cast<const int32_t*>(p->d_plan);
     kp.tile_slot = reinterpret_cast<const int32_t*>(p->d_plan) + p->tiles_cap;
     kp.masks = reinterpret_cast<const uint64_t*>(p->d_plan + codes_off);
@@ -517,6 +541,10 @@ static int denoise_impl(evo_policy* p, int32_t batch, const float* obs_cond, con
       HIP_TRY(launch_zero_u32(p->d_tctr, plan.n_tiles * 16, stream));
     }
     KernelKey key{s.d, s.dh(), s.H, s.dff, s.dtype, spt, team};
+    if (kp.fold) {
+      kp.okv_member_stride = 0;  // one copy of the fold records, read by every team member
+      HIP_TRY(launch_obs_fold(kp, s.dtype, stream));
+    }
     HIP_TRY(launch_denoise(key, kp, stream));
     HIP_TRY(hipEventRecord(p->ev_done, stream));
     p->last_stream = stream;

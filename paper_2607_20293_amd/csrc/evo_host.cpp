@@ -85,6 +85,13 @@ Flops flops_of(const Shape& s) {
   f.always_step = 4 * H * A * d;
   f.always_query = 2 * (uint64_t)s.n_obs * s.obs_dim * d;
   f.query_kernel = f.always_query + 2 * (uint64_t)s.n_obs * (2 * d) * d * s.L;
+  if (s.folds_ca()) {
+    // folded: scores and output against n_heads x S columns; the fold of the
+    // observation tokens (u and w, a d x d product each) once per query
+    const uint64_t nh = s.nh;
+    f.unit_kernel[UNIT_CA] = 2 * (2 * H * S * nh * d);
+    f.query_kernel += 2 * (uint64_t)s.n_obs * (2 * d) * d * s.L;
+  }
   return f;
 }
 
@@ -294,7 +301,13 @@ void call_stats(const Shape& s, const std::vector<Schedule>& reg, const int32_t*
     unit_weight_bytes(s, wb);
     const uint64_t e = s.elt();
     const uint64_t obs_pad = (uint64_t)((s.obs_dim + 31) / 32 * 32);
-    const uint64_t per_query_w = obs_pad * s.d * e + (uint64_t)s.L * 2 * s.d * s.d * e;
+    uint64_t per_query_w = obs_pad * s.d * e + (uint64_t)s.L * 2 * s.d * s.d * e;
+    // folded cross-attention: the fold reads fp32 W_q and W_o2 once per
+    // query; an evaluation reads the fold records (u, w, c) of its samples'
+    // S tokens instead of the unit's weights
+    const bool fold = s.folds_ca();
+    const uint64_t rec_bytes = (uint64_t)s.S() * (2 * s.nh * s.d + s.nh) * 4;
+    if (fold) per_query_w += (uint64_t)s.L * 2 * s.d * s.d * 4;
     st.n_tiles = plan->n_tiles;
     st.n_workgroups = (uint64_t)plan->n_tiles * team;
     st.cache_bytes_read *= team;
@@ -302,14 +315,15 @@ void call_stats(const Shape& s, const std::vector<Schedule>& reg, const int32_t*
     for (int q = 0; q < plan->n_tiles; ++q) {
       st.weight_bytes += per_query_w * team;
       for (int t = 0; t < s.T; ++t) {
-        uint64_t mask = 0;
+        uint64_t mask = 0, live = 0;
         for (int j = 0; j < plan->spt; ++j) {
           const int smp = plan->tile_sample[(size_t)q * plan->spt + j];
           if (smp < 0) continue;
           mask |= reg[ids ? ids[smp] : 0].eval_mask[t];
+          ++live;
         }
         for (int b = 0; b < s.U(); ++b)
-          if (mask >> b & 1) st.weight_bytes += wb[b % 3];
+          if (mask >> b & 1) st.weight_bytes += (fold && b % 3 == UNIT_CA) ? live * rec_bytes * team : wb[b % 3];
       }
     }
   }

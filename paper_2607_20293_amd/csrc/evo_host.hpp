@@ -37,6 +37,11 @@ struct Shape {
   int dh() const { return d / nh; }
   int S() const { return 1 + n_obs; }
   int elt() const { return dtype == EVO_BF16 ? 2 : 4; }
+  // Cross-attention folded into per-token fold records (the kernels of
+  // width 256 compile the folded unit; its n_heads x S score columns must
+  // fit one 16-wide tile).
+  bool folds_ca() const { return d == 256 && dh() == 64 && H >= 16 && nh * S() <= 16; }
+  int fold_rec() const { return 2 * nh * d + 16; }  // floats per fold record
 };
 
 // Validates field ranges; does not check compiled-shape support.

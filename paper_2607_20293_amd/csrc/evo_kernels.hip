@@ -264,7 +264,90 @@ struct Cfg {
   static constexpr int PS = 17;                        // stride of a 16x16 fp32 scratch tile
   static constexpr int PWN = (NJB > RB ? NJB : RB) * 16 * PS;
   static constexpr int NB = (8 / (CBW * RB)) > 0 ? (8 / (CBW * RB)) : 1;  // reuse loads per batch
+  // cross-attention folded into per-token fold records (width 256; one
+  // sample per 16-row block); used when n_heads x memory tokens <= 16
+  static constexpr bool FOLD = D == 256 && HZ >= 16;
+  static constexpr int REC = 2 * NH * D + 16;                              // floats per fold record
+  static constexpr int FOLD_LDS = FOLD ? NW * RB * 256 + 16 * R + RB * 16 * D : 0;
 };
+
+// Cross-attention with few memory tokens, folded.  With q = x W_q^T + b_q
+// (x the LayerNorm output of a row), the score of head h against memory
+// token j is q_h . k_jh = x . u_jh + c_jh with u_jh = W_q,h^T k_jh (W_q,h the
+// head's DH rows of W_q) and c_jh = b_q,h . k_jh, and the unit's output
+// sum_h sum_j p_jh v_jh W_o2,h^T + b_o2 = sum_h sum_j p_jh w_jh + b_o2 with
+// w_jh = W_o2,h v_jh (W_o2,h the head's DH columns of W_o2).  Projecting the
+// S tokens once per (token, layer) replaces the two d x d products of every
+// evaluation by two products with S x n_heads columns.
+//
+// A fold record holds u [NH][D] (for fp32 operands in the fragment column
+// order of the LDS operand, Op<float>::pcol), w [NH][D] and c [NH].  The
+// workgroup folds `nrows` <= MR key/value rows (kv: [row][2D] keys then
+// values, row stride ldkv, in LDS) with the layer's W_q (rows), the
+// transposed W_o2 (row e = column e of W_o2) and b_q; dst(row) is the record
+// of a row or null.  Weights are rounded to bf16 first when BF, as the packed matrices.
+template <int D, int DH, int NT, int MR, bool BF, class DST>
+__device__ void fold_rows(const float* __restrict__ raw, uint32_t wq, uint32_t wo2t,
+                                                    uint32_t bq, const float* kv, int ldkv, int nrows, DST dst,
+                                                    int tid) {
+  constexpr int NH = D / DH, C4 = D / 4, EB = 32;  // EB weight rows requested at once
+  static_assert(DH % EB == 0, "fold batches");
+  // work item = (u or w, head, 4 columns): the head's DH weight rows are
+  // read 16 bytes per lane, EB rows in flight
+  for (int it = tid; it < 2 * NH * C4; it += NT) {
+    const int isw = it / (NH * C4), hd = (it / C4) % NH, c0 = (it % C4) * 4;
+    const float* W = raw + (isw ? wo2t : wq) + (size_t)hd * DH * D + c0;
+    const float* kr = kv + (isw ? D : 0) + hd * DH;
+    f32x4 acc[MR];
+#pragma unroll
+    for (int r = 0; r < MR; ++r) acc[r] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int e0 = 0; e0 < DH; e0 += EB) {
+      f32x4 wv[EB];
+#pragma unroll
+      for (int e = 0; e < EB; ++e) wv[e] = *reinterpret_cast<const f32x4*>(W + (size_t)(e0 + e) * D);
+      if (BF) {
+#pragma unroll
+        for (int e = 0; e < EB; ++e)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) wv[e][q] = __uint_as_float(bf16_rne(wv[e][q]) << 16);
+      }
+#pragma unroll
+      for (int r = 0; r < MR; ++r)
+        if (r < nrows) {
+#pragma unroll
+          for (int e4 = 0; e4 < EB / 4; ++e4) {
+            const f32x4 kk = *reinterpret_cast<const f32x4*>(kr + r * ldkv + e0 + 4 * e4);
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+#pragma unroll
+              for (int t = 0; t < 4; ++t) acc[r][t] = fmaf(wv[4 * e4 + q][t], kk[q], acc[r][t]);
+          }
+        }
+    }
+#pragma unroll
+    for (int r = 0; r < MR; ++r)
+      if (r < nrows) {
+        float* q = dst(r);
+        if (!q) continue;
+        if (isw) {
+          *reinterpret_cast<f32x4*>(q + NH * D + hd * D + c0) = acc[r];
+        } else {
+#pragma unroll
+          for (int t = 0; t < 4; ++t) {
+            const int c = c0 + t;
+            q[hd * D + (BF ? c : ((c & ~15) | ((c & 3) << 2) | ((c >> 2) & 3)))] = acc[r][t];
+          }
+        }
+      }
+  }
+  for (int it = tid; it < nrows * NH; it += NT) {
+    const int r = it / NH, hd = it % NH;
+    float a = 0.f;
+    for (int e = 0; e < DH; ++e) a = fmaf(raw[bq + hd * DH + e], kv[r * ldkv + hd * DH + e], a);
+    float* q = dst(r);
+    if (q) q[2 * NH * D + hd] = a;
+  }
+}
 
 // LayerNorm statistics of the tile rows from the register-resident stream:
 // per-lane (mean, M2) over its columns, merged across the 16 lanes of a row
@@ -365,7 +448,7 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
   static_assert(DH == 64 || DH == 32, "head dim");
 
   __shared__ __attribute__((aligned(16))) AT xa[R * LDA];
-  __shared__ __attribute__((aligned(16))) float ybuf[R * LDY];
+  __shared__ __attribute__((aligned(16))) float ybuf[R * LDY > C::FOLD_LDS ? R * LDY : C::FOLD_LDS];
   __shared__ __attribute__((aligned(16))) AT zbuf[R * LDZ];
   __shared__ __attribute__((aligned(16))) float pw[NW * PWN];
   __shared__ __attribute__((aligned(16))) float kvbuf[SPT * SMAX * 2 * GW];
@@ -391,6 +474,10 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
   __shared__ int s_abort;
   const int L = p.L, A = p.A, T = p.T, U = 3 * L, nobs = p.n_obs, S = 1 + nobs;
   const float* raw = p.raw;
+  // folded cross-attention (n_heads x S <= 16, checked by the host): okv
+  // then holds fold records [batch][L][n_obs][REC] instead of keys/values
+  const bool fold = C::FOLD && p.fold != 0;
+  constexpr int REC = C::REC;
 
   if (tid < SPT) smp[tid] = p.tile_sample[tile * SPT + tid];
   if (tid == 0) s_abort = 0;
@@ -412,7 +499,8 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
   }
 
   // ---- per query: observation tokens and their keys/values in every layer
-  {
+  // (folded: their fold records come from the observation pre-pass)
+  if (!fold) {
     constexpr int MPWO = CB / NW;
     f32x4 acc[MPWO][1];
 #pragma unroll
@@ -904,6 +992,131 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
           gemm_run<AT, RB, CBW, GW / O::KF, INFL, NP2A>(r, zbuf, LDZ, pk + po.o, D / O::KF, g * (GW / O::KF), own, lane,
                                                        b2);
         }
+      } else if (C::FOLD && fold && u == 1) {
+        if constexpr (C::FOLD) {
+          // ---------------- cross-attention unit, folded (time token + observation tokens)
+          // Score columns n = j * NH + h (memory token j, head h) of the row
+          // block's sample, padded to 16 with zero columns.  Every team
+          // member evaluates the whole unit (no partials to exchange).
+          constexpr int KPW = (D / O::KF) / NW, VQ = O::VE / 4, SJ = 16 / NH;
+          static_assert(KPW * NW == D / O::KF && SJ * NH == 16, "folded cross-attention split");
+          const float* trec = p.tfold + ((size_t)k * L + l) * REC;
+          // record of memory token j of the sample in row block rb, and
+          // whether it exists (else the time-token record stands in and the
+          // loaded values are replaced by zeros)
+          const auto rec = [&](int rb, int j, bool& ok) -> const float* {
+            const int s_ = smp[(rb * 16) / HZ];
+            ok = s_ >= 0 && j < S;
+            return (ok && j > 0) ? okv + (((size_t)s_ * L + l) * nobs + (j - 1)) * REC : trec;
+          };
+          const f32x4 zero4 = {0.f, 0.f, 0.f, 0.f};
+          // u columns of this wave's k-range (the B operand of the scores)
+          f32x4 ub[RB][KPW][VQ];
+#pragma unroll
+          for (int rb = 0; rb < RB; ++rb) {
+            bool ok;
+            const float* q = rec(rb, lc / NH, ok) + (lc % NH) * D + w * KPW * O::KF + lq * O::VE;
+#pragma unroll
+            for (int kf = 0; kf < KPW; ++kf)
+#pragma unroll
+              for (int v = 0; v < VQ; ++v) {
+                const f32x4 x = *reinterpret_cast<const f32x4*>(q + kf * O::KF + 4 * v);
+                ub[rb][kf][v] = ok ? x : zero4;
+              }
+          }
+          // w vectors of the row blocks' samples, staged through LDS
+          constexpr int WQN = RB * 16 * D / 4, WQ = (WQN + NT - 1) / NT;
+          f32x4 wv[WQ];
+#pragma unroll
+          for (int q = 0; q < WQ; ++q) {
+            const int it = tid + q * NT;
+            const int f = it * 4, rb = f / (16 * D), n = (f / D) % 16, c = f % D;
+            bool ok = false;
+            const float* src = it < WQN ? rec(rb, n / NH, ok) : trec;
+            const f32x4 x = *reinterpret_cast<const f32x4*>(src + NH * D + (n % NH) * D + c);
+            wv[q] = (it < WQN && ok) ? x : zero4;
+          }
+          // c terms of the softmax thread's (row, head)
+          float cqv[SJ];
+          {
+            const int r = tid / NH, hd = tid % NH;
+#pragma unroll
+            for (int j = 0; j < SJ; ++j) {
+              bool ok = false;
+              const float* src = tid < R * NH ? rec(r >> 4, j, ok) : trec;
+              const float x = src[2 * NH * D + hd];
+              cqv[j] = (tid < R * NH && ok) ? x : 0.f;
+            }
+          }
+          layer_norm_to_xa();
+          // partial scores over this wave's k-range on MFMA
+          float* const sb = ybuf;                    // [NW][RB][64 lanes][4]
+          float* const pb = ybuf + NW * RB * 256;    // [16][R] probabilities (column n, row)
+          float* const wst = pb + 16 * R;            // [RB][16][D] w vectors
+#pragma unroll
+          for (int rb = 0; rb < RB; ++rb) {
+            f32x4 acc = zero4;
+#pragma unroll
+            for (int kf = 0; kf < KPW; ++kf) {
+              const uint4 a =
+                  *reinterpret_cast<const uint4*>(xa + (rb * 16 + lc) * LDA + (w * KPW + kf) * O::KF + lq * O::VE);
+              uint4 bq;
+              if constexpr (sizeof(AT) == 2) {
+                const f32x4 x0 = ub[rb][kf][0], x1 = ub[rb][kf][1];
+                bq.x = bf16_rne(x0[0]) | (bf16_rne(x0[1]) << 16);
+                bq.y = bf16_rne(x0[2]) | (bf16_rne(x0[3]) << 16);
+                bq.z = bf16_rne(x1[0]) | (bf16_rne(x1[1]) << 16);
+                bq.w = bf16_rne(x1[2]) | (bf16_rne(x1[3]) << 16);
+              } else {
+                bq = __builtin_bit_cast(uint4, ub[rb][kf][0]);
+              }
+              O::mma(acc, a, bq);
+            }
+            *reinterpret_cast<f32x4*>(sb + ((w * RB + rb) * 64 + lane) * 4) = acc;
+          }
+#pragma unroll
+          for (int q = 0; q < WQ; ++q)
+            if (tid + q * NT < WQN) *reinterpret_cast<f32x4*>(wst + (tid + q * NT) * 4) = wv[q];
+          __syncthreads();
+          // softmax over the memory tokens of each (row, head)
+          if (tid < R * NH) {
+            const int r = tid / NH, hd = tid % NH, rb = r >> 4, rr = r & 15;
+            float sc[SJ], mx = -INFINITY;
+#pragma unroll
+            for (int j = 0; j < SJ; ++j) {
+              const int n = j * NH + hd;
+              float a = 0.f;
+#pragma unroll
+              for (int ww = 0; ww < NW; ++ww) a += sb[((ww * RB + rb) * 64 + (rr >> 2) * 16 + n) * 4 + (rr & 3)];
+              sc[j] = j < S ? (a + cqv[j]) * (kScale * kLog2e) : -INFINITY;
+              mx = fmaxf(mx, sc[j]);
+            }
+            float den = 0.f;
+#pragma unroll
+            for (int j = 0; j < SJ; ++j) {
+              sc[j] = j < S ? fast_exp2(sc[j] - mx) : 0.f;
+              den += sc[j];
+            }
+            const float inv = fast_rcp(den);
+#pragma unroll
+            for (int j = 0; j < SJ; ++j) pb[(j * NH + hd) * R + r] = sc[j] * inv;
+          }
+          __syncthreads();
+          // output: r = P W over the 16 columns (padding columns are zero)
+#pragma unroll
+          for (int rb = 0; rb < RB; ++rb) {
+#pragma unroll 4
+            for (int n = 0; n < 16; ++n) {
+              const f32x4 pv = *reinterpret_cast<const f32x4*>(pb + n * R + rb * 16 + lq * 4);
+#pragma unroll
+              for (int c = 0; c < CBW; ++c) {
+                const float wc = wst[(rb * 16 + n) * D + (w * CBW + c) * 16 + lc];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) r[c][rb][i] = fmaf(pv[i], wc, r[c][rb][i]);
+              }
+            }
+          }
+        }
       } else if (u == 1) {
         // ---------------- cross-attention unit (time token + observation tokens)
         uint4 b1c[NPC][MPWC];
@@ -1045,7 +1258,7 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
           __syncthreads();
         }
       }
-      if constexpr (TEAM > 1) {
+      if constexpr (TEAM > 1) if (!(fold && u == 1)) {
         // Sum the members' partial residuals in member order, so that every
         // member obtains the same bits.  The partials travel through memory
         // with device-coherent (SC1) buffer stores and loads, which leave no
@@ -1285,6 +1498,82 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
   }
 }
 
+// ---------------------------------------------------------------- observation pre-pass
+// Folded cross-attention: observation tokens, their keys/values and fold
+// records, computed once per query before the denoising launch.  Workgroup
+// (g, l) takes the 16 (sample, token) rows g*16 .. g*16+15 of the flattened
+// [batch][n_obs] tokens and layer l; the tokens' embedding (a product with
+// the observation matrix) is repeated by every layer's workgroup.
+template <class AT>
+__global__ void __launch_bounds__(512) obs_fold_kernel(const KParams p) {
+  using O = Op<AT>;
+  constexpr int D = 256, DH = 64, NW = 8, NT = NW * 64, CB = D / 16, REC = 2 * (D / DH) * D + 16;
+  constexpr int KOBS = 64, LDO = KOBS + O::PAD, LDA = D + O::PAD;
+  __shared__ __attribute__((aligned(16))) AT ob[16 * LDO];
+  __shared__ __attribute__((aligned(16))) AT xa[16 * LDA];
+  __shared__ __attribute__((aligned(16))) float kvr[16 * 2 * D];
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, lc = lane & 15, lq = lane >> 4;
+  const int nobs = p.n_obs, L = p.L, l = blockIdx.y;
+  const int row0 = blockIdx.x * 16, nrows = min(16, p.batch * nobs - row0);
+  const float* raw = p.raw;
+  constexpr int MPWO = CB / NW;
+  f32x4 acc[MPWO][1];
+#pragma unroll
+  for (int m = 0; m < MPWO; ++m) acc[m][0] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const int nch = p.obs_pad / KOBS;
+  for (int c = 0; c < nch; ++c) {
+    __syncthreads();
+    for (int it = tid; it < 16 * KOBS; it += NT) {
+      const int row = it / KOBS, k = it % KOBS, kk = c * KOBS + k;
+      const float v = (row < nrows && kk < p.obs_dim) ? p.obs[(size_t)(row0 + row) * p.obs_dim + kk] : 0.f;
+      O::store(ob, LDO, row, k, v);
+    }
+    __syncthreads();
+    gemm_acc<AT, 1, MPWO, KOBS / O::KF>(acc, ob, LDO, p.pk + p.pk_obs, p.obs_pad / O::KF, c * (KOBS / O::KF),
+                                         [&](int m) { return w + NW * m; }, lane);
+  }
+#pragma unroll
+  for (int m = 0; m < MPWO; ++m) {
+    const int gcol = (w + NW * m) * 16 + lc;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int row = lq * 4 + i, o = (row0 + row) % nobs;
+      const float v = row < nrows ? acc[m][0][i] + raw[p.b_obs + gcol] + raw[p.P_mem + (size_t)(1 + o) * D + gcol] : 0.f;
+      O::store(xa, LDA, row, gcol, v);
+    }
+  }
+  __syncthreads();
+  const LayerOff lo = p.loff[l];
+  constexpr int MPWK = 2 * CB / NW;
+  f32x4 kv[MPWK][1];
+#pragma unroll
+  for (int m = 0; m < MPWK; ++m) kv[m][0] = f32x4{0.f, 0.f, 0.f, 0.f};
+  gemm_acc<AT, 1, MPWK, D / O::KF>(kv, xa, LDA, p.pk + p.poff[l].kv, D / O::KF, 0,
+                                    [&](int m) { return w + NW * m; }, lane);
+#pragma unroll
+  for (int m = 0; m < MPWK; ++m) {
+    const int gcol = (w + NW * m) * 16 + lc;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) kvr[(lq * 4 + i) * (2 * D) + gcol] = kv[m][0][i] + raw[lo.b_kv + gcol];
+  }
+  __syncthreads();
+  fold_rows<D, DH, NT, 16, sizeof(AT) == 2>(
+      raw, lo.w_q, lo.w_o2t, lo.b_q, kvr, 2 * D, nrows,
+      [&](int row) -> float* {
+        const int tok = row0 + row, s = tok / nobs, o = tok % nobs;
+        return p.okv + (((size_t)s * L + l) * nobs + o) * REC;
+      },
+      tid);
+}
+
+hipError_t launch_obs_fold(const KParams& p, int dtype, hipStream_t stream) {
+  const int rows = p.batch * p.n_obs;
+  if (rows <= 0) return hipSuccess;
+  const dim3 grid((unsigned)((rows + 15) / 16), (unsigned)p.L);
+  if (dtype == 1) hipLaunchKernelGGL(obs_fold_kernel<__bf16>, grid, dim3(512), 0, stream, p);
+  else hipLaunchKernelGGL(obs_fold_kernel<float>, grid, dim3(512), 0, stream, p);
+  return hipGetLastError();
+}
 // ---------------------------------------------------------------- creation
 __global__ void pack_kernel(const float* __restrict__ raw, size_t off, int N, int Nvalid, int K, int Kpad, int bf,
                             uint4* __restrict__ dst) {
@@ -1375,6 +1664,30 @@ __global__ void ddpm_kernel(int T, float* tab) {
     r[4] = (float)sqrt(var);
     r[5] = r[6] = r[7] = 0.f;
   }
+}
+
+// fold records of the time token: one workgroup per (timestep, layer)
+template <bool BF>
+__global__ void __launch_bounds__(512) time_fold_kernel(const float* __restrict__ raw, const LayerOff* __restrict__ loff,
+                                                        const float* __restrict__ tkv, int L, float* __restrict__ tfold) {
+  constexpr int D = 256, DH = 64, REC = 2 * (D / DH) * D + 16;
+  __shared__ __attribute__((aligned(16))) float kv[2 * D];
+  const int kl = blockIdx.x, l = kl % L;
+  for (int i = threadIdx.x; i < 2 * D; i += 512) kv[i] = tkv[(size_t)kl * 2 * D + i];
+  __syncthreads();
+  const LayerOff q = loff[l];
+  fold_rows<D, DH, 512, 1, BF>(raw, q.w_q, q.w_o2t, q.b_q, kv, 2 * D, 1,
+                            [&](int) -> float* { return tfold + (size_t)kl * REC; }, (int)threadIdx.x);
+}
+
+hipError_t launch_time_fold(const float* raw, const LayerOff* loff, const float* tkv, int T, int L, int d, int dh,
+                            int dtype, float* tfold, hipStream_t stream) {
+  if (d != 256 || dh != 64) return hipErrorInvalidValue;
+  if (dtype == 1)
+    hipLaunchKernelGGL(time_fold_kernel<true>, dim3(T * L), dim3(512), 0, stream, raw, loff, tkv, L, tfold);
+  else
+    hipLaunchKernelGGL(time_fold_kernel<false>, dim3(T * L), dim3(512), 0, stream, raw, loff, tkv, L, tfold);
+  return hipGetLastError();
 }
 
 hipError_t launch_pack(const float* raw, size_t off, int N, int Nvalid, int K, int Kpad, int dtype, uint4* dst,

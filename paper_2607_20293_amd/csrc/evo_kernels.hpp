@@ -21,7 +21,9 @@ struct DeviceGuard {
 // Float offsets (into the fp32 parameter copy) of one layer's small tensors.
 struct LayerOff {
   uint32_t ln1_g, ln1_b, b_qkv, b_o, ln2_g, ln2_b, b_q, b_kv, b_o2, ln3_g, ln3_b, b_1, b_2;
-  uint32_t pad_[3];
+  uint32_t w_q;    // W_q [d][d] (fp32 parameters), folded cross-attention only
+  uint32_t w_o2t;  // W_o2 transposed [d][d] (appended to the fp32 parameters), folded only
+  uint32_t pad_;
 };
 
 // Offsets (in 16-byte units) of one layer's packed matrices.
@@ -57,6 +59,8 @@ struct KParams {
   int batch, team;
   unsigned spin_limit;       // polls before a team wait gives up (sets *derr)
   int withhold;              // test hook: team member 0 never publishes its partials
+  int fold;                  // cross-attention folded: okv holds fold records [batch][L][n_obs][2 NH d + 16]
+  const float* tfold;        // [T][L][2 NH d + 16] fold records of the time token (folded only)
 };
 
 // Shape key of a compiled kernel instantiation.
@@ -85,6 +89,15 @@ hipError_t launch_time_kv(const float* raw, uint32_t pmem0, const uint32_t* wkv,
                           int T, int L, int D, int dtype, float* rows_scratch, float* tkv,
                           hipStream_t stream);
 hipError_t launch_ddpm_table(int T, float* table, hipStream_t stream);
+// Folded cross-attention: observation tokens, keys/values and fold records
+// of every (sample, token, layer) into p.okv, before the denoising launch
+// (d = 256; fields used: L, n_obs, obs_dim, obs_pad, raw, pk, loff, poff,
+// pk_obs, b_obs, P_mem, obs, okv, batch).
+hipError_t launch_obs_fold(const KParams& p, int dtype, hipStream_t stream);
+// Fold records of the time token for every (timestep, layer) from its
+// keys/values tkv [T][L][2d] (folded cross-attention, d = 256 only).
+hipError_t launch_time_fold(const float* raw, const LayerOff* loff, const float* tkv, int T, int L, int d, int dh,
+                            int dtype, float* tfold, hipStream_t stream);
 
 // team barrier counters must start at zero on every launch (a fill kernel,
 // not a memset node, so that the call may be captured into a graph)

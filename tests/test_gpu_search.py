@@ -199,8 +199,14 @@ def test_pusht_bf16_search_properties_and_sampled_parity():
         x = pol.denoise(obs_q, noise_q, np.zeros(nq, np.int32)).cpu().numpy()
         full = pol.denoise(obs_q, noise_q, np.ones(nq, np.int32)).cpu().numpy()
         pol.synchronize()
-        dv = np.max(np.abs(x - full), axis=(1, 2))
-        assert float(np.count_nonzero(dv.astype(np.float32) <= np.float32(tau))) / nq == got["best_quick"]
+        dv = np.max(np.abs(x - full), axis=(1, 2)).astype(np.float32)
+        # The search scored the schedule in one call of P x nq samples (two-
+        # sample tiles), this re-run has nq samples (small-batch teams): the
+        # two kernel variants round bf16 differently (about 1e-3 relative),
+        # so a deviation within 1% of tau may be classified either way.
+        near = np.abs(dv - np.float32(tau)) <= np.float32(1e-2 * tau)
+        lo = np.count_nonzero((dv <= np.float32(tau)) & ~near)
+        assert lo / nq <= got["best_quick"] <= (lo + np.count_nonzero(near)) / nq
     finally:
         pol.close()
     lat = np.zeros((rows, T), np.uint8)
