@@ -276,3 +276,29 @@ def test_maximum_obs_tokens_and_action_dim():
         assert evo.check_desc(evo.make_desc(replace(base, n_obs=8), "bf16", 2, 1)) == -5
         assert evo.check_desc(evo.make_desc(replace(base, action_dim=17), "bf16", 2, 1)) == -5
     assert evo.check_desc(evo.make_desc(replace(I.BIMANUAL, n_obs=5), "bf16", 2, 1)) == -5
+
+
+@pytest.mark.parametrize("name,n_obs", [("pusht", 2), ("pusht", 3), ("pusht", 4), ("tiny", 2)])
+def test_flops_kernel_of_folded_and_projected_cross_attention(name, n_obs):
+    """flops_kernel of one uncached sample against the closed forms: the
+    cross-attention of width-256 policies with n_heads x (1 + n_obs) <= 16
+    is folded (scores and output against n_heads x S columns, plus the fold
+    of the observation tokens once per query); other shapes project with
+    W_q and W_o2 at every evaluation."""
+    import dataclasses
+    base = I.PUSHT if name == "pusht" else I.TINY
+    s = dataclasses.replace(base, n_obs=n_obs)
+    H, d, L, T, A, nh, dff = s.horizon, s.d_model, s.n_layers, s.n_steps, s.action_dim, s.n_heads, s.d_ff
+    S = 1 + n_obs
+    folded = d == 256 and nh * S <= 16
+    sa = 2 * (4 * H * d * d + 2 * H * H * d)
+    ca = 2 * (2 * H * S * nh * d) if folded else 2 * (2 * H * d * d + 2 * H * S * d)
+    ffn = 4 * H * d * dff
+    query = 2 * n_obs * s.obs_dim * d + 2 * n_obs * (2 * d) * d * L * (2 if folded else 1)
+    want = T * L * (sa + ca + ffn) + query + T * 4 * H * A * d
+    desc = evo.make_desc(s, "bf16", max_batch=1, max_schedules=1)
+    st = evo.schedule_stats(desc, [np.ones((3 * L, T), np.uint8)], np.zeros(1, np.int32), evo.GRAN_UNIT)
+    assert st["flops_kernel"] == want
+    # the paper's convention is the same either way
+    F = O.unit_flops(s)
+    assert st["flops_cacheable"] == T * L * (F["SA"] + F["CA"] + F["FFN"])
