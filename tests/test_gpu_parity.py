@@ -110,8 +110,9 @@ def test_pusht_b1_single_workgroup(name):
 @pytest.mark.parametrize("size", [4, 2])
 @pytest.mark.parametrize("dtype", ["fp32", "bf16"])
 def test_team_variant_matches_single_workgroup(dtype, size):
-    """Small batches run `size` workgroups per one-sample tile (heads and
-    d_ff chunks split among them, partial residuals summed through memory;
+    """Small batches run `size` workgroups per one-sample tile (self-
+    attention heads and d_ff chunks split among them, partial residuals summed
+    through memory; the folded cross-attention is evaluated whole by each;
     automatic choice: fp32 teams of 4 up to n_cu/4 samples, then teams of 2
     up to n_cu/2, bf16 teams of 2 up to n_cu/2; each size forced here with
     EVO_TEAM=<size>).  Both variants match the oracle on a ragged
@@ -568,4 +569,25 @@ def test_maximum_obs_tokens_and_action_dim(base, dtype):
     rng = np.random.default_rng([11, 3])
     lats = [I.lattice_bernoulli(s.n_layers, s.n_steps, p, rng) for p in (0.3, 0.7)]
     pol, *_ = _case(f"{base}_obs7_a16_{dtype}", s, wts, obs, noise, lats, np.array([1, 0, 1], np.int32), dtype)
+    pol.close()
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+@pytest.mark.parametrize("n_obs,batch", [(3, 3), (3, 301), (4, 3)])
+def test_cross_attention_fold_boundary(n_obs, batch, dtype):
+    """Width-256 cross-attention at the boundary of its folded form: 3
+    observation tokens fill all 16 folded score columns (4 heads x 4 memory
+    tokens), 4 fall back to the projected unit.  Batch 3 runs the small-batch
+    teams (every member evaluates the folded unit), batch 301 two-sample
+    tiles with a half-empty last tile (oracle on the first, a middle and the
+    last sample); two schedules mixed."""
+    from dataclasses import replace
+    s = replace(I.PUSHT, n_obs=n_obs)
+    wts = I.make_weights(s, 13, "perturbed")
+    obs, noise = I.make_obs(s, batch, 13), I.make_noise(s, batch, 13)
+    rng = np.random.default_rng([13, n_obs])
+    lats = [I.lattice_bernoulli(s.n_layers, s.n_steps, p, rng) for p in (0.25, 0.6)]
+    ids = (np.arange(batch) % 2).astype(np.int32)
+    samples = None if batch <= 3 else [0, batch // 2, batch - 1]
+    pol, *_ = _case(f"pusht_obs{n_obs}_b{batch}_{dtype}", s, wts, obs, noise, lats, ids, dtype, samples=samples)
     pol.close()
