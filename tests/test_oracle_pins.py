@@ -348,6 +348,87 @@ def test_samples_are_independent():
     assert np.array_equal(full[1:2], one)
 
 
+def _mixed_schedule_case(gran, seed=11):
+    """Three clearly different lattices (densities 0.15 / 0.5 / 0.9, step 0
+    left out of some rows so both cold readings differ), shuffled ids over 7
+    samples."""
+    rng = np.random.default_rng(seed)
+    rows = TINY.n_layers if gran == O.GRAN_LAYER else 3 * TINY.n_layers
+    lats = [I.lattice_bernoulli(rows, TINY.n_steps, p, rng) for p in (0.15, 0.5, 0.9)]
+    for lt in lats:
+        lt[rng.integers(0, rows), 0] = 0
+    ids = rng.permutation(np.array([0, 1, 2, 0, 1, 2, 2], np.int32))
+    return lats, ids
+
+
+@pytest.mark.parametrize("gran", [O.GRAN_LAYER, O.GRAN_UNIT])
+@pytest.mark.parametrize("cold", [O.COLD_COMPUTE, O.COLD_ZERO])
+@pytest.mark.parametrize("samples", [None, [5, 0, 3, 6], [6, 2]])
+def test_denoise_mixed_schedules_per_sample(gran, cold, samples):
+    """Eq. 1 applied per sample: with several lattices, shuffled ids and an
+    unsorted subset of samples, output row i is sample samples[i] denoised
+    alone under its own lattice ids[samples[i]] (expanded to units, then the
+    cold reading), the per-sample loop written out here without the
+    oracle's grouping by schedule id."""
+    lats, ids = _mixed_schedule_case(gran)
+    B = len(ids)
+    wf = I.make_weights(TINY, 0, "perturbed")
+    P = O.prepare_params(I.split_weights(TINY, wf), "fp32")
+    obs, noise = I.make_obs(TINY, B, 3), I.make_noise(TINY, B, 3)
+    got, _ = O.denoise(TINY, I.split_weights(TINY, wf), obs, noise, lats, ids, granularity=gran,
+                       cold_policy=cold, samples=samples)
+    sel = list(range(B)) if samples is None else samples
+    assert got.shape == (len(sel), TINY.horizon, TINY.action_dim)
+    for i, n in enumerate(sel):
+        eff = O.effective_lattice(O.expand_lattice(lats[ids[n]], gran, TINY.n_layers), cold)
+        want = O.denoise_group(TINY, P, obs[n:n + 1], noise[:, n:n + 1], eff)[0]
+        np.testing.assert_allclose(got[i], want, rtol=0, atol=1e-13)
+        # the test has power: another sample's lattice, or another sample's
+        # inputs, give a visibly different chunk
+        other = O.effective_lattice(O.expand_lattice(lats[(ids[n] + 1) % 3], gran, TINY.n_layers), cold)
+        wrong = O.denoise_group(TINY, P, obs[n:n + 1], noise[:, n:n + 1], other)[0]
+        assert np.max(np.abs(wrong - want)) > 1e-6
+        m = (n + 1) % B
+        assert np.max(np.abs(got[i] - O.denoise_group(TINY, P, obs[m:m + 1], noise[:, m:m + 1], eff)[0])) > 1e-6
+
+
+@pytest.mark.parametrize("gran", [O.GRAN_LAYER, O.GRAN_UNIT])
+@pytest.mark.parametrize("cold", [O.COLD_COMPUTE, O.COLD_ZERO])
+def test_bookkeeping_mixed_ids_counts_every_sample(gran, cold):
+    """Integer bookkeeping over mixed ids equals, key by key, the counts taken
+    sample by sample from the positions the loop actually evaluated (trace),
+    from the lattice itself for the requested refreshes, and n x the dense
+    per-sample cost for flops_full."""
+    lats, ids = _mixed_schedule_case(gran, seed=12)
+    B = len(ids)
+    P, obs, noise = _tiny_inputs(batch=B)
+    F = O.unit_flops(TINY)
+    per = [F["SA"], F["CA"], F["FFN"]]
+    st = O.bookkeeping(TINY, lats, ids, gran, cold)
+    req = eff_n = fc = 0
+    for n in range(B):
+        lt = lats[ids[n]]
+        req += int(lt.sum()) * (3 if gran == O.GRAN_LAYER else 1)
+        tr = {}
+        eff = O.effective_lattice(O.expand_lattice(lt, gran, TINY.n_layers), cold)
+        O.denoise_group(TINY, P, obs[n:n + 1], noise[:, n:n + 1], eff, trace=tr)
+        eff_n += int(tr["computed"].sum())
+        fc += sum(per[b % 3] for _, b in zip(*np.nonzero(tr["computed"])))
+    T, L = TINY.n_steps, TINY.n_layers
+    always = B * (T * 4 * TINY.horizon * TINY.action_dim * TINY.d_model
+                  + 2 * TINY.n_obs * TINY.obs_dim * TINY.d_model)
+    assert st["refreshes_requested"] == req
+    assert st["refreshes_effective"] == eff_n
+    assert st["flops_cacheable"] == fc
+    assert st["flops_always"] == always
+    assert st["flops_full"] == B * T * L * sum(per) + always
+    # summing by position instead of by id would count another mix
+    wrong = O.bookkeeping(TINY, lats, np.sort(ids)[::-1].copy(), gran, cold)
+    assert wrong == st   # a permutation of the ids leaves the sums unchanged ...
+    shifted = O.bookkeeping(TINY, lats, (ids + 1) % 3, gran, cold)
+    assert shifted["flops_cacheable"] != st["flops_cacheable"]   # ... another assignment does not
+
+
 def test_pairs_encoding():
     lat = O.pairs_to_lattice([(0, 0), (5, 3), (2, 9)], 6, 10)
     assert lat.sum() == 3 and lat[5, 3] == 1
