@@ -354,6 +354,25 @@ int evo_search(evo_policy* p, const evo_ga_config* cfg, const evo_search_options
 /* Statistics of the last evo_denoise call (host struct). */
 int evo_get_stats(const evo_policy* p, evo_stats* out);
 
+/* Measurement of the denoising kernel alone (Sec. 4.1 reports the cost of
+ * the cached loop; this isolates its kernel from the per-query observation
+ * pre-pass launched before it on the same stream).  With enable != 0, every
+ * later evo_denoise records a pair of timing events on its stream around the
+ * denoising kernel's launch (a ring of 64 pairs created here; a pair still
+ * in use is waited for and harvested before it is recorded again).
+ * enable == 0 stops the recording and destroys the events.  Errors:
+ * EVO_E_INVALID for a NULL policy, EVO_E_HIP if an event cannot be created
+ * (timing then stays off). */
+int evo_set_kernel_timing(evo_policy* p, int32_t enable);
+
+/* Waits for every recorded pair, then returns in *ms_total the summed
+ * duration (milliseconds) and in *launches the number of denoising-kernel
+ * launches timed since the last call of this function, and restarts both
+ * sums at zero.  ms_total and launches are host pointers (either may be
+ * NULL).  Errors: EVO_E_INVALID for a NULL policy, EVO_E_HIP from an event
+ * query. */
+int evo_kernel_time(evo_policy* p, double* ms_total, int64_t* launches);
+
 /* Host-only bookkeeping for lattices without a policy: n_lat lattices
  * (host uint8[n_lat][rows][T]) of one granularity, per-sample ids (host
  * int32[batch]).  Fills refreshes and the FLOP fields of `out` as

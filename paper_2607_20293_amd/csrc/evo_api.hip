@@ -110,6 +110,14 @@ struct evo_policy {
   Plan last_plan;
   int last_threads = 0;
   int last_team = 1;
+  // optional timing of the denoising kernel alone: a ring of event pairs
+  // recorded around its launch, harvested into t_ms / t_n
+  static constexpr int kTimingPairs = 64;
+  std::vector<hipEvent_t> tev;  // [2 * kTimingPairs] start, end
+  std::vector<char> tev_busy;
+  int tev_next = 0;
+  double t_ms = 0.0;
+  int64_t t_n = 0;
 };
 
 namespace evo {
@@ -119,7 +127,9 @@ int policy_device(const evo_policy* p) { return p->device; }
 
 static void release(evo_policy* p) {
   if (!p) return;
-  (void)hipDeviceSynchronize();
+  // the policy's own launches end before its buffers are freed (ev_done is
+  // recorded after every launch; no device-wide wait)
+  if (p->launched && p->ev_done) (void)hipEventSynchronize(p->ev_done);
   (void)hipFree(p->d_raw);
   (void)hipFree(p->d_pk);
   (void)hipFree(p->d_loff);
@@ -139,7 +149,30 @@ static void release(evo_policy* p) {
     if (p->ev[i]) (void)hipEventDestroy(p->ev[i]);
   }
   if (p->ev_done) (void)hipEventDestroy(p->ev_done);
+  for (hipEvent_t e : p->tev)
+    if (e) (void)hipEventDestroy(e);
   delete p;
+}
+
+// Adds the duration of timing pair i (which must be recorded) to the sums.
+static hipError_t harvest_pair(evo_policy* p, int i) {
+  hipError_t e = hipEventSynchronize(p->tev[2 * i + 1]);
+  float ms = 0.f;
+  if (e == hipSuccess) e = hipEventElapsedTime(&ms, p->tev[2 * i], p->tev[2 * i + 1]);
+  p->tev_busy[i] = 0;
+  if (e == hipSuccess) {
+    p->t_ms += ms;
+    p->t_n += 1;
+  }
+  return e;
+}
+
+static void drop_timing_events(evo_policy* p) {
+  for (hipEvent_t e : p->tev)
+    if (e) (void)hipEventDestroy(e);
+  p->tev.clear();
+  p->tev_busy.clear();
+  p->tev_next = 0;
 }
 
 extern "C" {
@@ -545,7 +578,17 @@ static int denoise_impl(evo_policy* p, int32_t batch, const float* obs_cond, con
       kp.okv_member_stride = 0;  // one copy of the fold records, read by every team member
       HIP_TRY(launch_obs_fold(kp, s.dtype, stream));
     }
+    const int tslot = p->tev.empty() ? -1 : p->tev_next;
+    if (tslot >= 0) {
+      if (p->tev_busy[tslot]) HIP_TRY(harvest_pair(p, tslot));
+      HIP_TRY(hipEventRecord(p->tev[2 * tslot], stream));
+    }
     HIP_TRY(launch_denoise(key, kp, stream));
+    if (tslot >= 0) {
+      HIP_TRY(hipEventRecord(p->tev[2 * tslot + 1], stream));
+      p->tev_busy[tslot] = 1;
+      p->tev_next = (tslot + 1) % evo_policy::kTimingPairs;
+    }
     HIP_TRY(hipEventRecord(p->ev_done, stream));
     p->last_stream = stream;
     p->launched = true;
@@ -625,6 +668,44 @@ int evo_guided_sample(const double* probs, int32_t rows, int32_t n_steps, int32_
     if (!probs || !uniforms || !pairs_out || rows < 1 || n_steps < 1) return fail(EVO_E_INVALID, "bad arguments");
     return guided_sample(probs, rows, n_steps, K, uniforms, pairs_out);
   });
+}
+
+int evo_set_kernel_timing(evo_policy* p, int32_t enable) {
+  clear_error();
+  if (!p) return fail(EVO_E_INVALID, "policy is NULL");
+  DeviceGuard guard(p->device);
+  if (!enable) {
+    drop_timing_events(p);
+    return EVO_OK;
+  }
+  if (!p->tev.empty()) return EVO_OK;
+  return guarded([&]() -> int {
+    p->tev.assign(2 * evo_policy::kTimingPairs, nullptr);
+    p->tev_busy.assign(evo_policy::kTimingPairs, 0);
+    for (auto& e : p->tev) {
+      const hipError_t r = hipEventCreate(&e);
+      if (r != hipSuccess) {
+        drop_timing_events(p);
+        return fail(EVO_E_HIP, "hipEventCreate failed: %s", hipGetErrorString(r));
+      }
+    }
+    p->t_ms = 0.0;
+    p->t_n = 0;
+    return EVO_OK;
+  });
+}
+
+int evo_kernel_time(evo_policy* p, double* ms_total, int64_t* launches) {
+  clear_error();
+  if (!p) return fail(EVO_E_INVALID, "policy is NULL");
+  DeviceGuard guard(p->device);
+  for (int i = 0; i < (int)p->tev_busy.size(); ++i)
+    if (p->tev_busy[i]) HIP_TRY(harvest_pair(p, i));
+  if (ms_total) *ms_total = p->t_ms;
+  if (launches) *launches = p->t_n;
+  p->t_ms = 0.0;
+  p->t_n = 0;
+  return EVO_OK;
 }
 
 int evo_get_stats(const evo_policy* p, evo_stats* out) {

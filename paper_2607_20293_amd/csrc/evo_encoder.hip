@@ -524,6 +524,8 @@ struct evo_encoder {
   float* shift = nullptr;        // GroupNorm shifts [image][group]
   size_t shift_cap = 0;
   uint64_t flops_per_image = 0;
+  hipEvent_t ev_done = nullptr;  // recorded after the last encode's launches
+  bool launched = false;
 };
 
 namespace {
@@ -756,6 +758,7 @@ int evo_create_encoder(const evo_encoder_desc* desc, const float* host_weights, 
     ENC_TRY(hipMalloc(&e->ws, (size_t)kWsFloats * sizeof(float)));
     ENC_TRY(hipMalloc(&e->part, e->part_cap * sizeof(double2)));
     ENC_TRY(hipMalloc(&e->shift, e->shift_cap * sizeof(float)));
+    ENC_TRY(hipEventCreateWithFlags(&e->ev_done, hipEventDisableTiming));
     ENC_TRY(hipDeviceSynchronize());
 #undef ENC_TRY
     *out = e;
@@ -825,6 +828,8 @@ int evo_encode(evo_encoder* e, int32_t batch, const float* images, float* featur
       W = W3;
       cin = c;
     }
+  ENC_HIP(hipEventRecord(e->ev_done, st));
+  e->launched = true;
 #undef ENC_HIP
   return EVO_OK;
 }
@@ -839,13 +844,16 @@ int evo_encoder_flops(const evo_encoder* e, int32_t batch, uint64_t* flops_out) 
 void evo_destroy_encoder(evo_encoder* e) {
   if (!e) return;
   DeviceGuard guard(e->device);
-  (void)hipDeviceSynchronize();
+  // the encoder's own launches end before its buffers are freed (no
+  // device-wide wait: other work on the device is not this encoder's)
+  if (e->launched && e->ev_done) (void)hipEventSynchronize(e->ev_done);
   for (ConvLayer& L : e->convs) (void)hipFree(L.w);
   for (int i = 0; i < 4; ++i) (void)hipFree(e->buf[i]);
   (void)hipFree(e->ws);
   (void)hipFree(e->part);
   (void)hipFree(e->shift);
   (void)hipFree(e->d_raw);
+  if (e->ev_done) (void)hipEventDestroy(e->ev_done);
   delete e;
 }
 

@@ -8,6 +8,7 @@ from __future__ import annotations
 
 import ctypes
 import os
+import sys
 from typing import Optional, Sequence
 
 import numpy as np
@@ -26,7 +27,7 @@ EXPORTED = ("evo_weight_count", "evo_check_desc", "evo_create_policy", "evo_set_
             "evo_last_error", "evo_collect_activations", "evo_redundancy_scores", "evo_guided_probabilities",
             "evo_guided_sample", "evo_ga_initial_population", "evo_ga_next_generation", "evo_ga_search",
             "evo_search", "evo_encoder_weight_count", "evo_create_encoder", "evo_encode", "evo_encoder_flops",
-            "evo_destroy_encoder")
+            "evo_destroy_encoder", "evo_set_kernel_timing", "evo_kernel_time")
 
 
 def guided_probabilities(scores, eps: float, gamma: float) -> np.ndarray:
@@ -238,6 +239,10 @@ def lib() -> ctypes.CDLL:
         L.evo_search.argtypes = [P, ctypes.POINTER(GAConfig), ctypes.POINTER(SearchOptions), P, P, P, P, P,
                                  ctypes.POINTER(SearchResult), P, P, P, P]
         L.evo_search.restype = ctypes.c_int
+        L.evo_set_kernel_timing.argtypes = [P, I32]
+        L.evo_set_kernel_timing.restype = ctypes.c_int
+        L.evo_kernel_time.argtypes = [P, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)]
+        L.evo_kernel_time.restype = ctypes.c_int
         L.evo_synchronize.argtypes = [P]
         L.evo_synchronize.restype = ctypes.c_int
         L.evo_destroy_policy.argtypes = [P]
@@ -334,6 +339,10 @@ class Policy:
             self._h = None
 
     def __del__(self):
+        # at interpreter shutdown the HIP runtime may already be torn down:
+        # release nothing then (the process is ending)
+        if sys is None or sys.is_finalizing():
+            return
         try:
             self.close()
         except Exception:
@@ -432,6 +441,16 @@ class Policy:
                                 ctypes.c_void_p(st.cuda_stream)))
         return _search_out(cfg, res, best, ph, fh)
 
+    def set_kernel_timing(self, enable: bool = True):
+        """Record timing events around every later denoising-kernel launch."""
+        _check(lib().evo_set_kernel_timing(self._h, 1 if enable else 0))
+
+    def kernel_time(self):
+        """(summed ms, launches) of the denoising kernel since the last call."""
+        ms, n = ctypes.c_double(), ctypes.c_int64()
+        _check(lib().evo_kernel_time(self._h, ctypes.byref(ms), ctypes.byref(n)))
+        return float(ms.value), int(n.value)
+
     def synchronize(self):
         """Wait for the last denoise call; raise if its kernel reported a
         device-side failure (a timed-out team barrier)."""
@@ -493,6 +512,10 @@ class Encoder:
             self._h = None
 
     def __del__(self):
+        # at interpreter shutdown the HIP runtime may already be torn down:
+        # release nothing then (the process is ending)
+        if sys is None or sys.is_finalizing():
+            return
         try:
             self.close()
         except Exception:

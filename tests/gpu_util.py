@@ -43,15 +43,30 @@ def run_oracle(shape, weights, obs, noise, lattices, ids, gran, cold, dtype, sam
 
 
 def compare(got, ref, dtype, what=""):
+    """what=None: check quietly (the caller reports)."""
     err = float(np.max(np.abs(got - ref)))
     if dtype == "fp32":
-        say(f"  {what}: max-abs err {err:.3e} (tol {TOL_FP32})")
+        if what is not None:
+            say(f"  {what}: max-abs err {err:.3e} (tol {TOL_FP32})")
         assert err <= TOL_FP32, f"{what}: max-abs {err} > {TOL_FP32}"
         return err
     rel = err / max(float(np.max(np.abs(ref))), 1e-6)
-    say(f"  {what}: rel err {rel:.3e} (max-abs {err:.3e}, tol {TOL_BF16})")
+    if what is not None:
+        say(f"  {what}: rel err {rel:.3e} (max-abs {err:.3e}, tol {TOL_BF16})")
     assert rel <= TOL_BF16, f"{what}: relative {rel} > {TOL_BF16}"
     return rel
+
+
+def load_stored(name):
+    """The oracle's chunks of a full-size workload written by
+    tests/golden/make_oracle_outputs.py (samples, chunks, workload, seed,
+    source_sha)."""
+    import os
+    p = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", f"oracle_{name}.npz")
+    with np.load(p, allow_pickle=False) as z:
+        g = {k: z[k] for k in z.files}
+    assert str(g["workload"]) == name and int(g["seed"]) == 0
+    return g
 
 
 def check_stats(got, want):

@@ -12,7 +12,7 @@ from oracle import evo_oracle as O
 from paper_2607_20293_amd import evo
 from paper_2607_20293_amd import inputs as I
 from tests.conftest import printed_unit_lattice
-from tests.gpu_util import check_stats, compare, device, run_gpu, run_oracle, say
+from tests.gpu_util import check_stats, compare, device, load_stored, run_gpu, run_oracle, say
 
 pytestmark = pytest.mark.gpu
 
@@ -182,45 +182,50 @@ def test_team_wait_timeout_is_reported(size):
     pol2.close()
 
 
+def _case_stored(name, expect_tiles=None):
+    """A full-size workload on the GPU against the oracle's chunks stored by
+    tests/golden/make_oracle_outputs.py (every sample of the batch, or the
+    stored spread subset), each sample checked on its own against the bar;
+    bookkeeping against the oracle's integer counts."""
+    w = I.WORKLOADS[name]
+    inp = I.make_inputs(w)
+    g = load_stored(name)
+    samples = [int(j) for j in g["samples"]]
+    say(f"[gpu] {name}: dtype={w.dtype} batch={w.batch}, {len(samples)} stored oracle samples")
+    pol = _policy(w.shape, inp.weights, w.dtype, w.batch, len(inp.lattices))
+    for j, lt in enumerate(inp.lattices):
+        pol.set_schedule(j, lt, O.GRAN_LAYER)
+    got, gst = run_gpu(pol, inp.obs, inp.noise, inp.ids)
+    errs = [compare(got[j], g["chunks"][i], w.dtype, None) for i, j in enumerate(samples)]
+    worst = int(np.argmax(errs))
+    say(f"  {name}: worst sample {samples[worst]}: {'max-abs' if w.dtype == 'fp32' else 'rel'} "
+        f"{errs[worst]:.3e}; median {float(np.median(errs)):.3e}")
+    check_stats(gst, O.bookkeeping(w.shape, inp.lattices, inp.ids))
+    if expect_tiles is not None:
+        assert gst["n_tiles"] == expect_tiles
+    pol.close()
+    return errs
+
+
 @pytest.mark.parametrize("name", ["pusht_fp32_b64_d25", "pusht_bf16_b64_d25", "pusht_bf16_b64_all"])
-def test_pusht_b64_sampled(name):
-    w = I.WORKLOADS[name]
-    inp = I.make_inputs(w)
-    samples = [0, 1, 17, 42, 63]
-    pol, *_ = _case(name, w.shape, inp.weights, inp.obs, inp.noise, inp.lattices, inp.ids, w.dtype,
-                    samples=samples)
-    pol.close()
+def test_pusht_b64_every_sample(name):
+    _case_stored(name)
 
 
-def test_image_b256_sampled():
-    w = I.WORKLOADS["image_bf16_b256_d12"]
-    inp = I.make_inputs(w)
-    pol, *_ = _case("image_bf16_b256_d12", w.shape, inp.weights, inp.obs, inp.noise, inp.lattices, inp.ids,
-                    "bf16", samples=[0, 5, 128, 255])
-    pol.close()
+def test_image_b256_every_sample():
+    _case_stored("image_bf16_b256_d12")
 
 
-@pytest.mark.parametrize("name,samples", [("bimanual_bf16_b128_d20", [0, 127]),
-                                          ("bimanual_bf16_b128_all", [64])])
-def test_bimanual_b128_sampled(name, samples):
-    w = I.WORKLOADS[name]
-    inp = I.make_inputs(w)
-    pol, *_ = _case(name, w.shape, inp.weights, inp.obs, inp.noise, inp.lattices, inp.ids, "bf16",
-                    samples=samples)
-    pol.close()
+@pytest.mark.parametrize("name", ["bimanual_bf16_b128_d20", "bimanual_bf16_b128_all"])
+def test_bimanual_b128_spread_samples(name):
+    """32 (20% lattice) and 16 (all-refresh) samples spread over the batch:
+    every XCD's tile range and every residue of the sample index mod 8."""
+    _case_stored(name)
 
 
-def test_population_b512_sampled():
-    """512 samples, 64 schedules (10-40% density), per-sample ids: two
-    samples per workgroup tile."""
-    w = I.WORKLOADS["population_bf16_b512"]
-    inp = I.make_inputs(w)
-    ids = inp.ids
-    samples = [0, 1, 2, 100, 255, 256, 300, 511]
-    pol, got, gst, _ = _case("population_bf16_b512", w.shape, inp.weights, inp.obs, inp.noise, inp.lattices,
-                             ids, "bf16", samples=samples)
-    assert gst["n_tiles"] == 256
-    pol.close()
+def test_population_b512_every_sample():
+    """512 samples, 64 schedules (10-40% density), per-sample ids."""
+    _case_stored("population_bf16_b512")
 
 
 # ---------------------------------------------------------------- invariants
