@@ -110,6 +110,8 @@ struct evo_policy {
   Plan last_plan;
   int last_threads = 0;
   int last_team = 1;
+  unsigned* last_derr = nullptr;  // error flag of the last call's team barriers (NULL: no team)
+  PlanSpace plan_ws;              // plan arrays, sized at creation
   // optional timing of the denoising kernel alone: a ring of event pairs
   // recorded around its launch, harvested into t_ms / t_n
   static constexpr int kTimingPairs = 64;
@@ -406,7 +408,8 @@ int evo_create_policy(const evo_policy_desc* desc, const float* host_weights, si
       }
       p->tiles_cap = tiles * spt_max;
       p->codes_cap = (size_t)std::min(s.max_sched, s.max_batch) * T * 3 * sizeof(uint64_t);
-      p->plan_bytes = (2 * p->tiles_cap * sizeof(int32_t) + 255) / 256 * 256 + p->codes_cap;
+      // (room for both tile arrays, each rounded up to 256 bytes)
+      p->plan_bytes = 2 * ((p->tiles_cap * sizeof(int32_t) + 255) / 256 * 256) + p->codes_cap;
       CREATE_TRY(hipMalloc(&p->d_plan, p->plan_bytes));
       for (int i = 0; i < 2; ++i) {
         CREATE_TRY(hipHostMalloc((void**)&p->h_stage[i], p->plan_bytes, hipHostMallocDefault));
@@ -417,6 +420,7 @@ int evo_create_policy(const evo_policy_desc* desc, const float* host_weights, si
     CREATE_TRY(hipDeviceSynchronize());
 #undef CREATE_TRY
     p->reg.assign(s.max_sched, Schedule());
+    p->plan_ws.reserve(s.max_batch, s.max_sched);
     *out = p;
     return EVO_OK;
   };
@@ -468,6 +472,20 @@ int evo_set_schedule_pairs(evo_policy* p, int32_t schedule_id, const int32_t* pa
   });
 }
 
+namespace {
+// Where a call's kernels keep their working data.
+struct CallBuffers {
+  float* cache = nullptr;
+  float* okv = nullptr;
+  float* xchg = nullptr;
+  unsigned* tctr = nullptr;
+  unsigned* derr = nullptr;
+  uint8_t* plan = nullptr;  // tile samples, tile slots, schedule masks
+  size_t plan_tiles = 0;    // entries reserved for each tile array in `plan`
+  size_t okv_stride = 0;    // floats between team members' observation keys/values
+};
+}  // namespace
+
 static int denoise_impl(evo_policy* p, int32_t batch, const float* obs_cond, const float* noise,
                         const int32_t* schedule_ids, float* actions_out, float* acts_out, void* hip_stream) {
   return guarded([&]() -> int {
@@ -511,33 +529,57 @@ static int denoise_impl(evo_policy* p, int32_t batch, const float* obs_cond, con
         break;
       }
     }
-    Plan plan;
-    int rc = build_plan(s, p->reg, schedule_ids, batch, spt, 8, &plan);
+    PlanSpace& ps = p->plan_ws;
+    int rc = plan_into(p->reg, schedule_ids, batch, spt, 8, &ps);
     if (rc) return rc;
-    const size_t ntile_ent = (size_t)plan.n_tiles * spt;
-    const size_t codes_off = (2 * p->tiles_cap * sizeof(int32_t) + 255) / 256 * 256;
+    const size_t ntile_ent = (size_t)ps.n_tiles * spt;
     const size_t ucodes = (size_t)s.T * 3 * sizeof(uint64_t);
-    if (ntile_ent > p->tiles_cap || plan.used.size() * ucodes > p->codes_cap)
+    if (ntile_ent > p->tiles_cap || (size_t)ps.n_used * ucodes > p->codes_cap)
       return fail(EVO_E_STATE, "plan exceeds the policy's buffers");
+    if (team > 1 && ps.n_tiles > tc->max_batch) return fail(EVO_E_STATE, "team plan exceeds the buffers");
+    const bool fold = s.folds_ca();
+    const size_t R = (size_t)spt * s.H, D = s.d;
+    CallBuffers cb;
+    cb.cache = p->d_cache;
+    cb.okv = p->d_okv;
+    cb.xchg = p->d_xchg;
+    cb.tctr = p->d_tctr;
+    cb.derr = p->d_derr;
+    cb.plan = p->d_plan;
+    cb.plan_tiles = p->tiles_cap;
+    cb.okv_stride = team > 1 ? tc->okv_stride : 0;
     // Calls on a different stream than the previous one wait for it: the
     // plan, caches and observation keys/values are per-policy buffers.
     if (p->launched && stream != p->last_stream) HIP_TRY(hipStreamWaitEvent(stream, p->ev_done, 0));
-    // Stage the plan in pinned memory and upload it, unless the device copy
-    // already holds exactly these bytes (repeated calls with the same ids).
-    const size_t nbytes = codes_off + plan.used.size() * ucodes;
+    // Plan bytes: tile samples, tile slots (each array cb.plan_tiles
+    // entries), then the used schedules' step masks.  Staged in pinned
+    // memory and uploaded; the policy's own plan buffer is not re-uploaded
+    // when it already holds exactly these bytes (repeated calls).
+    const size_t codes_off = (2 * cb.plan_tiles * sizeof(int32_t) + 255) / 256 * 256;
+    const size_t nbytes = codes_off + (size_t)ps.n_used * ucodes;
+    if (nbytes > p->plan_bytes) return fail(EVO_E_STATE, "plan exceeds the staging buffer");
+    const auto fill = [&](uint8_t* dst) {
+      std::memset(dst, 0, codes_off);
+      std::memcpy(dst, ps.tile_sample.data(), ntile_ent * sizeof(int32_t));
+      std::memcpy(dst + cb.plan_tiles * sizeof(int32_t), ps.tile_slot.data(), ntile_ent * sizeof(int32_t));
+      for (int i = 0; i < ps.n_used; ++i)
+        std::memcpy(dst + codes_off + i * ucodes, p->reg[ps.used[i]].masks.data(), ucodes);
+    };
+    const auto upload = [&](const uint8_t* src) -> int {
+      const int st = p->stage;
+      if (hipEventSynchronize(p->ev[st]) != hipSuccess) return fail(EVO_E_HIP, "event synchronize failed");
+      if (src) std::memcpy(p->h_stage[st], src, nbytes);
+      else fill(p->h_stage[st]);
+      HIP_TRY(hipMemcpyAsync(cb.plan, p->h_stage[st], nbytes, hipMemcpyHostToDevice, stream));
+      HIP_TRY(hipEventRecord(p->ev[st], stream));
+      p->stage ^= 1;
+      return EVO_OK;
+    };
     {
       std::vector<uint8_t> bytes(nbytes, 0);
-      std::memcpy(bytes.data(), plan.tile_sample.data(), ntile_ent * sizeof(int32_t));
-      std::memcpy(bytes.data() + p->tiles_cap * sizeof(int32_t), plan.tile_slot.data(), ntile_ent * sizeof(int32_t));
-      for (size_t i = 0; i < plan.used.size(); ++i)
-        std::memcpy(bytes.data() + codes_off + i * ucodes, p->reg[plan.used[i]].masks.data(), ucodes);
+      fill(bytes.data());
       if (bytes != p->uploaded) {
-        const int st = p->stage;
-        if (hipEventSynchronize(p->ev[st]) != hipSuccess) return fail(EVO_E_HIP, "event synchronize failed");
-        std::memcpy(p->h_stage[st], bytes.data(), nbytes);
-        HIP_TRY(hipMemcpyAsync(p->d_plan, p->h_stage[st], nbytes, hipMemcpyHostToDevice, stream));
-        HIP_TRY(hipEventRecord(p->ev[st], stream));
-        p->stage ^= 1;
+        if ((rc = upload(bytes.data()))) return rc;
         p->uploaded.swap(bytes);
       }
     }
@@ -545,39 +587,36 @@ static int denoise_impl(evo_policy* p, int32_t batch, const float* obs_cond, con
     KParams kp;
     std::memset(&kp, 0, sizeof(kp));
     kp.L = s.L; kp.A = s.A; kp.n_obs = s.n_obs; kp.obs_dim = s.obs_dim; kp.obs_pad = p->obs_pad;
-    kp.T = s.T; kp.clip = s.clip; kp.n_tiles = plan.n_tiles;
+    kp.T = s.T; kp.clip = s.clip; kp.n_tiles = ps.n_tiles;
     kp.raw = p->d_raw; kp.pk = p->d_pk; kp.loff = p->d_loff; kp.poff = p->d_poff; kp.pk_obs = p->pk_obs;
     const WeightOffsets& wo = p->wo;
     kp.W_in = (uint32_t)wo.W_in; kp.b_in = (uint32_t)wo.b_in; kp.P_act = (uint32_t)wo.P_act;
     kp.b_obs = (uint32_t)wo.b_obs; kp.P_mem = (uint32_t)wo.P_mem; kp.lnf_g = (uint32_t)wo.lnf_g;
     kp.lnf_b = (uint32_t)wo.lnf_b; kp.W_out = (uint32_t)wo.W_out; kp.b_out = (uint32_t)wo.b_out;
     kp.tkv = p->d_tkv; kp.ddpm = p->d_ddpm;
-    kp.fold = s.folds_ca() ? 1 : 0;
+    kp.fold = fold ? 1 : 0;
     kp.tfold = p->d_tfold;
-    kp.tile_sample = reinterpret_cast<const int32_t*>(p->d_plan);
-    kp.tile_slot = reinterpret_cast<const int32_t*>(p->d_plan) + p->tiles_cap;
-    kp.masks = reinterpret_cast<const uint64_t*>(p->d_plan + codes_off);
+    kp.tile_sample = reinterpret_cast<const int32_t*>(cb.plan);
+    kp.tile_slot = reinterpret_cast<const int32_t*>(cb.plan) + cb.plan_tiles;
+    kp.masks = reinterpret_cast<const uint64_t*>(cb.plan + codes_off);
     kp.pk_win = p->pk_win;
     kp.pk_wout = p->pk_wout;
-    kp.obs = obs_cond; kp.noise = noise; kp.out = actions_out; kp.okv = p->d_okv; kp.cache = p->d_cache;
+    kp.obs = obs_cond; kp.noise = noise; kp.out = actions_out; kp.okv = cb.okv; kp.cache = cb.cache;
     kp.acts = acts_out;
     kp.batch = batch;
     kp.team = team;
+    kp.okv_member_stride = fold ? 0 : cb.okv_stride;  // fold records: one copy read by every team member
     if (team > 1) {
-      if (plan.n_tiles > tc->max_batch) return fail(EVO_E_STATE, "team plan exceeds the buffers");
-      kp.xchg = p->d_xchg;
-      kp.tctr = p->d_tctr;
-      kp.derr = p->d_derr;
-      kp.okv_member_stride = tc->okv_stride;
+      kp.xchg = cb.xchg;
+      kp.tctr = cb.tctr;
+      kp.derr = cb.derr;
       kp.spin_limit = p->team_spin_limit;
       kp.withhold = p->team_withhold;
-      HIP_TRY(launch_zero_u32(p->d_tctr, plan.n_tiles * 16, stream));
     }
+    // team counters start at zero: a fill kernel, not a memset node
+    if (team > 1) HIP_TRY(launch_zero_u32(cb.tctr, ps.n_tiles * 16, stream));
     KernelKey key{s.d, s.dh(), s.H, s.dff, s.dtype, spt, team};
-    if (kp.fold) {
-      kp.okv_member_stride = 0;  // one copy of the fold records, read by every team member
-      HIP_TRY(launch_obs_fold(kp, s.dtype, stream));
-    }
+    if (kp.fold) HIP_TRY(launch_obs_fold(kp, s.dtype, stream));
     const int tslot = p->tev.empty() ? -1 : p->tev_next;
     if (tslot >= 0) {
       if (p->tev_busy[tslot]) HIP_TRY(harvest_pair(p, tslot));
@@ -592,10 +631,18 @@ static int denoise_impl(evo_policy* p, int32_t batch, const float* obs_cond, con
     HIP_TRY(hipEventRecord(p->ev_done, stream));
     p->last_stream = stream;
     p->launched = true;
+    p->last_derr = team > 1 ? cb.derr : nullptr;
 
-    call_stats(s, p->reg, schedule_ids, batch, &plan, team, &p->last);
+    call_stats(s, p->reg, schedule_ids, batch, ps.tile_sample.data(), ps.n_tiles, spt, team, &p->last);
     p->has_last = true;
-    p->last_plan = std::move(plan);
+    {
+      Plan& lp = p->last_plan;
+      lp.spt = spt;
+      lp.n_tiles = ps.n_tiles;
+      lp.tile_sample.assign(ps.tile_sample.begin(), ps.tile_sample.begin() + ntile_ent);
+      lp.tile_slot.assign(ps.tile_slot.begin(), ps.tile_slot.begin() + ntile_ent);
+      lp.used.assign(ps.used.begin(), ps.used.begin() + ps.n_used);
+    }
     p->last_threads = threads;
     p->last_team = team;
     return EVO_OK;
@@ -607,11 +654,11 @@ int evo_synchronize(evo_policy* p) {
   if (!p) return fail(EVO_E_INVALID, "policy is NULL");
   DeviceGuard guard(p->device);
   if (p->launched) HIP_TRY(hipEventSynchronize(p->ev_done));
-  if (p->d_derr) {
+  if (p->last_derr) {
     unsigned flag = 0;
-    HIP_TRY(hipMemcpy(&flag, p->d_derr, sizeof(unsigned), hipMemcpyDeviceToHost));
+    HIP_TRY(hipMemcpy(&flag, p->last_derr, sizeof(unsigned), hipMemcpyDeviceToHost));
     if (flag) {
-      HIP_TRY(hipMemset(p->d_derr, 0, sizeof(unsigned)));
+      HIP_TRY(hipMemset(p->last_derr, 0, sizeof(unsigned)));
       return fail(EVO_E_HIP, "a team barrier timed out on the device; outputs of that call are invalid");
     }
   }
@@ -733,7 +780,7 @@ int evo_schedule_stats(const evo_policy_desc* desc, const uint8_t* lattices, int
       const int id = ids ? ids[n] : 0;
       if (id < 0 || id >= n_lat) return fail(EVO_E_INVALID, "id %d of sample %d out of range", id, n);
     }
-    call_stats(s, reg, ids, batch, nullptr, 1, out);
+    call_stats(s, reg, ids, batch, nullptr, 0, 1, 1, out);
     return EVO_OK;
   });
 }

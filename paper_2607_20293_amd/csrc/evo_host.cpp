@@ -170,65 +170,96 @@ int build_schedule(const Shape& s, const uint8_t* lattice, int rows, int granula
   return EVO_OK;
 }
 
-int build_plan(const Shape& s, const std::vector<Schedule>& reg, const int32_t* ids, int batch,
-               int spt, int n_xcd, Plan* out) {
-  (void)s;
+void PlanSpace::reserve(int max_batch, int max_sched) {
+  const size_t B = (size_t)std::max(max_batch, 1), S = (size_t)std::max(max_sched, 1);
+  order.assign(B, 0);
+  count.assign(S + 1, 0);
+  slot_of.assign(S, -1);
+  merged.assign(B + 8, -1);  // tiles of up to 8 samples, the last one padded
+  tile_sample.assign(B + 8, -1);
+  tile_slot.assign(B + 8, 0);
+  used.assign(S, 0);
+}
+
+int plan_into(const std::vector<Schedule>& reg, const int32_t* ids, int batch, int spt, int n_xcd, PlanSpace* ps) {
   if (spt < 1) spt = 1;
   if (n_xcd < 1) n_xcd = 1;
-  std::vector<int32_t> order(batch);
-  std::iota(order.begin(), order.end(), 0);
+  const int S = (int)reg.size();
+  if (spt > 8 || batch < 0 || (size_t)batch > ps->order.size() || ps->count.size() < (size_t)S + 1 ||
+      ps->slot_of.size() < (size_t)S || ps->used.size() < (size_t)S)
+    return fail(EVO_E_STATE, "plan workspace too small");
   auto id_of = [&](int n) { return ids ? ids[n] : 0; };
-  std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return id_of(a) < id_of(b); });
-  // tiles in sorted order; a tile never mixes schedules unless a schedule's
-  // sample count is not a multiple of spt (then the remainder shares a tile)
-  std::vector<std::vector<int32_t>> tiles;
+  // samples sorted by schedule id, stable (counting sort)
+  std::fill(ps->count.begin(), ps->count.begin() + S + 1, 0);
+  for (int n = 0; n < batch; ++n) ++ps->count[id_of(n) + 1];
+  for (int i = 0; i < S; ++i) ps->count[i + 1] += ps->count[i];
+  for (int n = 0; n < batch; ++n) ps->order[ps->count[id_of(n)]++] = n;
+  // tiles in sorted order, a tile never mixing schedules; short tiles (a
+  // schedule's sample count not a multiple of spt) are then merged in order
+  // to avoid idle slots (correct for any mix: the kernel evaluates the
+  // union and selects per sample).  Emitted tiles land in `merged`.
+  int32_t cur[8];
+  int ncur = 0, nt = 0;
+  const auto emit = [&](const int32_t* t, int len) {
+    for (int j = 0; j < spt; ++j) ps->merged[(size_t)nt * spt + j] = j < len ? t[j] : -1;
+    ++nt;
+  };
   for (int i = 0; i < batch;) {
-    std::vector<int32_t> t;
-    const int sid = id_of(order[i]);
-    while (i < batch && (int)t.size() < spt && id_of(order[i]) == sid) t.push_back(order[i++]);
-    // fill a partially used tile with the next schedule's samples only when
-    // the tile would otherwise stay short and no further tiles are needed
-    tiles.push_back(std::move(t));
-  }
-  // merge short tiles pairwise to avoid idle slots (correct for any mix:
-  // the kernel evaluates the union and selects per sample)
-  {
-    std::vector<std::vector<int32_t>> merged;
-    std::vector<int32_t> cur;
-    for (auto& t : tiles) {
-      if ((int)t.size() == spt) { merged.push_back(t); continue; }
-      for (int x : t) {
-        cur.push_back(x);
-        if ((int)cur.size() == spt) { merged.push_back(cur); cur.clear(); }
+    const int sid = id_of(ps->order[i]);
+    const int i0 = i;
+    while (i < batch && i - i0 < spt && id_of(ps->order[i]) == sid) ++i;
+    if (i - i0 == spt) {
+      emit(&ps->order[i0], spt);
+      continue;
+    }
+    for (int k = i0; k < i; ++k) {
+      cur[ncur++] = ps->order[k];
+      if (ncur == spt) {
+        emit(cur, spt);
+        ncur = 0;
       }
     }
-    if (!cur.empty()) merged.push_back(cur);
-    tiles.swap(merged);
   }
-  const int n = (int)tiles.size();
-  Plan p;
-  p.spt = spt;
-  p.n_tiles = n;
-  p.tile_sample.assign((size_t)n * spt, -1);
-  p.tile_slot.assign((size_t)n * spt, 0);
-  // used schedule list
-  std::vector<int> slot_of(reg.size(), -1);
-  for (int i = 0; i < batch; ++i) {
-    const int sid = id_of(i);
-    if (slot_of[sid] < 0) { slot_of[sid] = (int)p.used.size(); p.used.push_back(sid); }
+  if (ncur) emit(cur, ncur);
+  // schedules referenced by the call, in order of first use
+  std::fill(ps->slot_of.begin(), ps->slot_of.begin() + S, -1);
+  int nu = 0;
+  for (int n = 0; n < batch; ++n) {
+    const int sid = id_of(n);
+    if (ps->slot_of[sid] < 0) {
+      ps->slot_of[sid] = nu;
+      ps->used[nu++] = sid;
+    }
   }
   // XCD-aware placement: position q runs on XCD q % n_xcd; the tiles of
   // XCD x are a contiguous run of the sorted order
   int next = 0;
-  for (int x = 0; x < n_xcd && x < n; ++x) {
-    for (int q = x; q < n; q += n_xcd) {
-      const auto& t = tiles[next++];
-      for (int j = 0; j < (int)t.size(); ++j) {
-        p.tile_sample[(size_t)q * spt + j] = t[j];
-        p.tile_slot[(size_t)q * spt + j] = slot_of[id_of(t[j])];
+  for (int x = 0; x < n_xcd && x < nt; ++x)
+    for (int q = x; q < nt; q += n_xcd, ++next)
+      for (int j = 0; j < spt; ++j) {
+        const int32_t smp = ps->merged[(size_t)next * spt + j];
+        ps->tile_sample[(size_t)q * spt + j] = smp;
+        ps->tile_slot[(size_t)q * spt + j] = smp >= 0 ? ps->slot_of[id_of(smp)] : 0;
       }
-    }
-  }
+  ps->spt = spt;
+  ps->n_tiles = nt;
+  ps->n_used = nu;
+  return EVO_OK;
+}
+
+int build_plan(const Shape& s, const std::vector<Schedule>& reg, const int32_t* ids, int batch,
+               int spt, int n_xcd, Plan* out) {
+  (void)s;
+  PlanSpace ps;
+  ps.reserve(batch, (int)reg.size());
+  const int rc = plan_into(reg, ids, batch, spt, n_xcd, &ps);
+  if (rc) return rc;
+  Plan p;
+  p.spt = ps.spt;
+  p.n_tiles = ps.n_tiles;
+  p.tile_sample.assign(ps.tile_sample.begin(), ps.tile_sample.begin() + (size_t)ps.n_tiles * ps.spt);
+  p.tile_slot.assign(ps.tile_slot.begin(), ps.tile_slot.begin() + (size_t)ps.n_tiles * ps.spt);
+  p.used.assign(ps.used.begin(), ps.used.begin() + ps.n_used);
   *out = std::move(p);
   return EVO_OK;
 }
@@ -279,7 +310,7 @@ int guided_sample(const double* p, int rows, int T, int K, const double* u, int3
 }
 
 void call_stats(const Shape& s, const std::vector<Schedule>& reg, const int32_t* ids, int batch,
-                const Plan* plan, int team, evo_stats* out) {
+                const int32_t* tile_sample, int n_tiles, int spt, int team, evo_stats* out) {
   evo_stats st;
   std::memset(&st, 0, sizeof(st));
   const Flops f = flops_of(s);
@@ -296,7 +327,7 @@ void call_stats(const Shape& s, const std::vector<Schedule>& reg, const int32_t*
   }
   st.flops_always = (uint64_t)batch * ((uint64_t)s.T * f.always_step + f.always_query);
   st.flops_full = (uint64_t)batch * s.T * s.L * F_layer + st.flops_always;
-  if (plan) {
+  if (tile_sample) {
     uint64_t wb[3];
     unit_weight_bytes(s, wb);
     const uint64_t e = s.elt();
@@ -308,16 +339,16 @@ void call_stats(const Shape& s, const std::vector<Schedule>& reg, const int32_t*
     const bool fold = s.folds_ca();
     const uint64_t rec_bytes = (uint64_t)s.S() * (2 * s.nh * s.d + s.nh) * 4;
     if (fold) per_query_w += (uint64_t)s.L * 2 * s.d * s.d * 4;
-    st.n_tiles = plan->n_tiles;
-    st.n_workgroups = (uint64_t)plan->n_tiles * team;
+    st.n_tiles = n_tiles;
+    st.n_workgroups = (uint64_t)n_tiles * team;
     st.cache_bytes_read *= team;
     st.cache_bytes_written *= team;
-    for (int q = 0; q < plan->n_tiles; ++q) {
+    for (int q = 0; q < n_tiles; ++q) {
       st.weight_bytes += per_query_w * team;
       for (int t = 0; t < s.T; ++t) {
         uint64_t mask = 0, live = 0;
-        for (int j = 0; j < plan->spt; ++j) {
-          const int smp = plan->tile_sample[(size_t)q * plan->spt + j];
+        for (int j = 0; j < spt; ++j) {
+          const int smp = tile_sample[(size_t)q * spt + j];
           if (smp < 0) continue;
           mask |= reg[ids ? ids[smp] : 0].eval_mask[t];
           ++live;

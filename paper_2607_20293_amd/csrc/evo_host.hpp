@@ -109,6 +109,17 @@ struct Plan {
 int build_plan(const Shape& s, const std::vector<Schedule>& reg, const int32_t* ids, int batch,
                int spt, int n_xcd, Plan* out);
 
+// The same plan built without allocating: every array is sized once by
+// reserve() (a batch of up to max_batch samples, schedule ids below
+// max_sched, up to 8 samples per tile); plan_into only writes into them.
+struct PlanSpace {
+  std::vector<int32_t> order, count, slot_of, merged;  // work arrays
+  std::vector<int32_t> tile_sample, tile_slot, used;   // the plan (first n_tiles*spt / n_used entries)
+  int spt = 1, n_tiles = 0, n_used = 0;
+  void reserve(int max_batch, int max_sched);
+};
+int plan_into(const std::vector<Schedule>& reg, const int32_t* ids, int batch, int spt, int n_xcd, PlanSpace* ps);
+
 // Eq. 7 (Sec. 3.3): min-max normalise n scores into w and return
 // p_i = (eps + w_i)^gamma / sum_j (eps + w_j)^gamma in fp64.
 int guided_probabilities(const float* scores, size_t n, double eps, double gamma, double* p_out);
@@ -153,7 +164,9 @@ int ga_next(const evo_ga_config& c, int rows, int T, int gen, const int32_t* pop
 int ga_search(const evo_ga_config& c, int rows, int T, const double* probs, const SearchEval& ev, double q_base,
               double delta_acc, evo_search_result* res, int32_t* best_out, int32_t* pop_hist, double* fit_hist);
 
+// tile_sample: the call's plan ([n_tiles][spt], -1 = empty), or NULL for
+// the counts that do not depend on it.  Allocates nothing.
 void call_stats(const Shape& s, const std::vector<Schedule>& reg, const int32_t* ids, int batch,
-                const Plan* plan, int team, evo_stats* out);
+                const int32_t* tile_sample, int n_tiles, int spt, int team, evo_stats* out);
 
 }  // namespace evo

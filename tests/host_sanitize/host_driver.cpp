@@ -78,6 +78,13 @@ void schedules_and_plans(std::mt19937_64& rng) {
     std::vector<uint8_t> two((size_t)s.L * s.T, 2);
     EXPECT(build_schedule(s, two.data(), s.L, EVO_GRAN_LAYER, &bad) != EVO_OK);
     // plans: ragged batches, mixed and shuffled ids, one and two samples per tile
+    {
+      // a workspace too small for the batch is refused
+      PlanSpace small;
+      small.reserve(4, 8);
+      std::vector<int32_t> ids(5, 0);
+      EXPECT(plan_into(reg, ids.data(), 5, 1, 8, &small) != EVO_OK);
+    }
     for (int batch : {1, 2, 3, 63, 64, 65, 255, 256, 257, 511, 512}) {
       std::vector<int32_t> ids(batch);
       std::uniform_int_distribution<int> u(0, 7);
@@ -96,8 +103,17 @@ void schedules_and_plans(std::mt19937_64& rng) {
         }
         for (int v : seen) EXPECT(v == 1);
         evo_stats st{};
-        call_stats(s, reg, ids.data(), batch, &pl, 1, &st);
+        call_stats(s, reg, ids.data(), batch, pl.tile_sample.data(), pl.n_tiles, spt, 1, &st);
         EXPECT(st.flops_cacheable <= st.flops_full);
+        // the allocation-free builder, in arrays sized for a larger batch,
+        // gives the same plan
+        PlanSpace ps;
+        ps.reserve(512, 8);
+        EXPECT(plan_into(reg, ids.data(), batch, spt, 8, &ps) == EVO_OK);
+        EXPECT(ps.n_tiles == pl.n_tiles && ps.n_used == (int)pl.used.size());
+        for (size_t i = 0; i < pl.tile_sample.size(); ++i)
+          EXPECT(ps.tile_sample[i] == pl.tile_sample[i] && ps.tile_slot[i] == pl.tile_slot[i]);
+        for (size_t i = 0; i < pl.used.size(); ++i) EXPECT(ps.used[i] == pl.used[i]);
       }
     }
   }
@@ -118,7 +134,7 @@ void bookkeeping_print() {
   build_schedule(s, all.data(), s.L, EVO_GRAN_LAYER, &reg[1]);
   const int32_t ids[4] = {1, 0, 0, 1};
   evo_stats st{};
-  call_stats(s, reg, ids, 4, nullptr, 1, &st);
+  call_stats(s, reg, ids, 4, nullptr, 0, 1, 1, &st);
   std::printf("stats %llu %llu %llu %llu %llu\n", (unsigned long long)st.refreshes_requested,
               (unsigned long long)st.refreshes_effective, (unsigned long long)st.flops_cacheable,
               (unsigned long long)st.flops_always, (unsigned long long)st.flops_full);
