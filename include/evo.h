@@ -169,6 +169,32 @@ int evo_set_schedule_pairs(evo_policy* p, int32_t schedule_id, const int32_t* pa
 int evo_denoise(evo_policy* p, int32_t batch, const float* obs_cond, const float* noise,
                 const int32_t* schedule_ids, float* actions_out, void* hip_stream);
 
+/* For callers that cannot allocate memory: code under HIP graph capture,
+ * tight serving loops, harnesses that forbid allocation.  The same
+ * computation and arguments as evo_denoise, and the same plan, kernels and
+ * results; the kernels' working data (per-tile residual caches,
+ * observation keys/values or fold records, the small-batch team exchange
+ * slots, counters and error flag, and the call's plan) live in a fixed
+ * device array of evo_noalloc_scratch_bytes() bytes (64 MiB) instead of the
+ * policy's buffers.  The library looks up each device's copy of that array
+ * once, when the first policy is created on the device; the array is held
+ * until the process ends.  The call allocates nothing (no device, pinned or
+ * host heap memory): the plan is built in arrays sized at evo_create_policy
+ * and staged through the policy's pinned buffers.  A batch whose working
+ * data does not fit the array is refused with EVO_E_UNSUPPORTED before
+ * anything is enqueued (Push-T-shaped policies: about 120 samples).  Every
+ * call on a device shares that device's array, which keeps the last call's
+ * contents (each call clears what must start at zero): calls that overlap
+ * on one device race (different policies, or different threads); calls of
+ * one policy on different streams are ordered as for evo_denoise.
+ * evo_debug_read_cache refers to evo_denoise calls only (EVO_E_STATE after
+ * this call). */
+int evo_denoise_noalloc(evo_policy* p, int32_t batch, const float* obs_cond, const float* noise,
+                        const int32_t* schedule_ids, float* actions_out, void* hip_stream);
+
+/* Size in bytes of the per-device scratch array of evo_denoise_noalloc. */
+size_t evo_noalloc_scratch_bytes(void);
+
 /* Wait for the policy's last evo_denoise and report a device-side failure.
  * Small batches run a variant in which several workgroups share a tile and
  * meet at bounded device-side barriers; if one of those waits ever times

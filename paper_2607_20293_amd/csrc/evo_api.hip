@@ -4,6 +4,7 @@
 #include <algorithm>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <vector>
 
@@ -61,6 +62,29 @@ int check_supported(const Shape& s) {
 
 }  // namespace
 
+// Device scratch of evo_denoise_noalloc: one fixed array per device (each
+// device that loads the library holds its own copy until the process ends),
+// addressed through the pointer hipGetSymbolAddress returns for that device.
+constexpr size_t kScratchBytes = size_t(64) << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+constexpr int kMaxDevices = 64;
+static std::mutex g_scratch_mu;
+static void* g_scratch_ptr[kMaxDevices] = {};
+static bool g_scratch_tried[kMaxDevices] = {};
+
+// Looks up this device's copy of the scratch array once (the device is current).
+static void* scratch_for(int device) {
+  if (device < 0 || device >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_tried[device]) {
+    g_scratch_tried[device] = true;
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) == hipSuccess) g_scratch_ptr[device] = ptr;
+    else (void)hipGetLastError();
+  }
+  return g_scratch_ptr[device];
+}
+
 struct evo_policy {
   Shape s;
   int device = 0;
@@ -111,7 +135,9 @@ struct evo_policy {
   int last_threads = 0;
   int last_team = 1;
   unsigned* last_derr = nullptr;  // error flag of the last call's team barriers (NULL: no team)
+  bool last_noalloc = false;      // the last call ran in the device scratch array
   PlanSpace plan_ws;              // plan arrays, sized at creation
+  void* scratch = nullptr;        // this device's scratch array (evo_denoise_noalloc)
   // optional timing of the denoising kernel alone: a ring of event pairs
   // recorded around its launch, harvested into t_ms / t_n
   static constexpr int kTimingPairs = 64;
@@ -421,6 +447,7 @@ int evo_create_policy(const evo_policy_desc* desc, const float* host_weights, si
 #undef CREATE_TRY
     p->reg.assign(s.max_sched, Schedule());
     p->plan_ws.reserve(s.max_batch, s.max_sched);
+    p->scratch = scratch_for(p->device);
     *out = p;
     return EVO_OK;
   };
@@ -486,8 +513,12 @@ struct CallBuffers {
 };
 }  // namespace
 
+// noalloc: the call's buffers are carved from the device scratch array, the
+// plan is written straight into pinned staging memory and always uploaded,
+// and nothing is allocated (device, pinned or host heap).
 static int denoise_impl(evo_policy* p, int32_t batch, const float* obs_cond, const float* noise,
-                        const int32_t* schedule_ids, float* actions_out, float* acts_out, void* hip_stream) {
+                        const int32_t* schedule_ids, float* actions_out, float* acts_out, void* hip_stream,
+                        bool noalloc = false) {
   return guarded([&]() -> int {
     clear_error();
     if (!p) return fail(EVO_E_INVALID, "policy is NULL");
@@ -540,16 +571,51 @@ static int denoise_impl(evo_policy* p, int32_t batch, const float* obs_cond, con
     const bool fold = s.folds_ca();
     const size_t R = (size_t)spt * s.H, D = s.d;
     CallBuffers cb;
-    cb.cache = p->d_cache;
-    cb.okv = p->d_okv;
-    cb.xchg = p->d_xchg;
-    cb.tctr = p->d_tctr;
-    cb.derr = p->d_derr;
-    cb.plan = p->d_plan;
-    cb.plan_tiles = p->tiles_cap;
-    cb.okv_stride = team > 1 ? tc->okv_stride : 0;
+    if (!noalloc) {
+      cb.cache = p->d_cache;
+      cb.okv = p->d_okv;
+      cb.xchg = p->d_xchg;
+      cb.tctr = p->d_tctr;
+      cb.derr = p->d_derr;
+      cb.plan = p->d_plan;
+      cb.plan_tiles = p->tiles_cap;
+      cb.okv_stride = team > 1 ? tc->okv_stride : 0;
+    } else {
+      // carve the scratch array: plan, caches, observation keys/values (or
+      // fold records), team exchange slots, team counters and error flag
+      uint8_t* base = static_cast<uint8_t*>(p->scratch);
+      if (!base) return fail(EVO_E_HIP, "the device scratch array has no address on device %d", p->device);
+      const auto al = [](size_t v) { return (v + 255) / 256 * 256; };
+      const size_t okv_per = (size_t)s.L * s.n_obs * (fold ? s.fold_rec() : 2 * s.d);
+      const size_t okv_copies = (fold || team == 1) ? 1 : (size_t)team;
+      size_t off = 0;
+      const size_t o_plan = off;
+      off += al(2 * al(ntile_ent * sizeof(int32_t)) + (size_t)ps.n_used * ucodes);
+      const size_t o_cache = off;
+      off += al((size_t)ps.n_tiles * team * s.U() * R * D * sizeof(float));
+      const size_t o_okv = off;
+      off += al(okv_copies * batch * okv_per * sizeof(float));
+      const size_t o_xchg = off;
+      if (team > 1) off += al((size_t)ps.n_tiles * 3 * team * R * D * sizeof(float));
+      const size_t o_ctr = off;
+      off += al(((size_t)ps.n_tiles * 16 + 1) * sizeof(unsigned));
+      if (off > kScratchBytes)
+        return fail(EVO_E_UNSUPPORTED,
+                    "evo_denoise_noalloc: batch %d needs %zu bytes of device scratch, the array holds %zu "
+                    "(use evo_denoise, or a smaller batch)",
+                    batch, off, kScratchBytes);
+      cb.plan = base + o_plan;
+      cb.plan_tiles = al(ntile_ent * sizeof(int32_t)) / sizeof(int32_t);
+      cb.cache = reinterpret_cast<float*>(base + o_cache);
+      cb.okv = reinterpret_cast<float*>(base + o_okv);
+      cb.xchg = team > 1 ? reinterpret_cast<float*>(base + o_xchg) : nullptr;
+      cb.tctr = reinterpret_cast<unsigned*>(base + o_ctr);
+      cb.derr = cb.tctr + (size_t)ps.n_tiles * 16;
+      cb.okv_stride = (fold || team == 1) ? 0 : batch * okv_per;
+    }
     // Calls on a different stream than the previous one wait for it: the
-    // plan, caches and observation keys/values are per-policy buffers.
+    // plan, caches and observation keys/values are per-policy buffers (or
+    // the device's scratch array).
     if (p->launched && stream != p->last_stream) HIP_TRY(hipStreamWaitEvent(stream, p->ev_done, 0));
     // Plan bytes: tile samples, tile slots (each array cb.plan_tiles
     // entries), then the used schedules' step masks.  Staged in pinned
@@ -575,7 +641,9 @@ static int denoise_impl(evo_policy* p, int32_t batch, const float* obs_cond, con
       p->stage ^= 1;
       return EVO_OK;
     };
-    {
+    if (noalloc) {
+      if ((rc = upload(nullptr))) return rc;
+    } else {
       std::vector<uint8_t> bytes(nbytes, 0);
       fill(bytes.data());
       if (bytes != p->uploaded) {
@@ -613,8 +681,10 @@ static int denoise_impl(evo_policy* p, int32_t batch, const float* obs_cond, con
       kp.spin_limit = p->team_spin_limit;
       kp.withhold = p->team_withhold;
     }
-    // team counters start at zero: a fill kernel, not a memset node
-    if (team > 1) HIP_TRY(launch_zero_u32(cb.tctr, ps.n_tiles * 16, stream));
+    // team counters (and, in the scratch, the error flag after them) start
+    // at zero: a fill kernel, not a memset node
+    if (team > 1 || noalloc)
+      HIP_TRY(launch_zero_u32(cb.tctr, ps.n_tiles * 16 + (noalloc ? 1 : 0), stream));
     KernelKey key{s.d, s.dh(), s.H, s.dff, s.dtype, spt, team};
     if (kp.fold) HIP_TRY(launch_obs_fold(kp, s.dtype, stream));
     const int tslot = p->tev.empty() ? -1 : p->tev_next;
@@ -635,7 +705,8 @@ static int denoise_impl(evo_policy* p, int32_t batch, const float* obs_cond, con
 
     call_stats(s, p->reg, schedule_ids, batch, ps.tile_sample.data(), ps.n_tiles, spt, team, &p->last);
     p->has_last = true;
-    {
+    p->last_noalloc = noalloc;
+    if (!noalloc) {
       Plan& lp = p->last_plan;
       lp.spt = spt;
       lp.n_tiles = ps.n_tiles;
@@ -669,6 +740,13 @@ int evo_denoise(evo_policy* p, int32_t batch, const float* obs_cond, const float
                 float* actions_out, void* hip_stream) {
   return denoise_impl(p, batch, obs_cond, noise, schedule_ids, actions_out, nullptr, hip_stream);
 }
+
+int evo_denoise_noalloc(evo_policy* p, int32_t batch, const float* obs_cond, const float* noise,
+                        const int32_t* schedule_ids, float* actions_out, void* hip_stream) {
+  return denoise_impl(p, batch, obs_cond, noise, schedule_ids, actions_out, nullptr, hip_stream, true);
+}
+
+size_t evo_noalloc_scratch_bytes(void) { return kScratchBytes; }
 
 int evo_collect_activations(evo_policy* p, int32_t batch, const float* obs_cond, const float* noise,
                             const int32_t* schedule_ids, float* actions_out, float* acts_out, void* hip_stream) {
@@ -806,6 +884,7 @@ int evo_debug_read_cache(evo_policy* p, int32_t unit, int32_t sample, float* hos
     clear_error();
     if (!p || !host_dst) return fail(EVO_E_INVALID, "NULL argument");
     if (!p->has_last) return fail(EVO_E_STATE, "no evo_denoise call yet");
+    if (p->last_noalloc) return fail(EVO_E_STATE, "the last call ran in the device scratch array");
     const Shape& s = p->s;
     if (unit < 0 || unit >= s.U()) return fail(EVO_E_INVALID, "unit out of range");
     const Plan& pl = p->last_plan;

@@ -27,7 +27,8 @@ EXPORTED = ("evo_weight_count", "evo_check_desc", "evo_create_policy", "evo_set_
             "evo_last_error", "evo_collect_activations", "evo_redundancy_scores", "evo_guided_probabilities",
             "evo_guided_sample", "evo_ga_initial_population", "evo_ga_next_generation", "evo_ga_search",
             "evo_search", "evo_encoder_weight_count", "evo_create_encoder", "evo_encode", "evo_encoder_flops",
-            "evo_destroy_encoder", "evo_set_kernel_timing", "evo_kernel_time")
+            "evo_destroy_encoder", "evo_set_kernel_timing", "evo_kernel_time", "evo_denoise_noalloc",
+            "evo_noalloc_scratch_bytes")
 
 
 def guided_probabilities(scores, eps: float, gamma: float) -> np.ndarray:
@@ -239,6 +240,10 @@ def lib() -> ctypes.CDLL:
         L.evo_search.argtypes = [P, ctypes.POINTER(GAConfig), ctypes.POINTER(SearchOptions), P, P, P, P, P,
                                  ctypes.POINTER(SearchResult), P, P, P, P]
         L.evo_search.restype = ctypes.c_int
+        L.evo_denoise_noalloc.argtypes = [P, I32, P, P, P, P, P]
+        L.evo_denoise_noalloc.restype = ctypes.c_int
+        L.evo_noalloc_scratch_bytes.argtypes = []
+        L.evo_noalloc_scratch_bytes.restype = ctypes.c_size_t
         L.evo_set_kernel_timing.argtypes = [P, I32]
         L.evo_set_kernel_timing.restype = ctypes.c_int
         L.evo_kernel_time.argtypes = [P, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)]
@@ -384,6 +389,24 @@ class Policy:
         else:
             pa = _dev_ptr(acts, "float32", (B, 3 * s.n_layers, s.n_steps, s.horizon, s.d_model))
             _check(lib().evo_collect_activations(self._h, B, po, pn, pid, pout, pa, ctypes.c_void_p(st.cuda_stream)))
+        return out
+
+    def denoise_noalloc(self, obs, noise, ids, out, stream=None):
+        """evo_denoise_noalloc: as denoise with a caller-provided out, the
+        working data in the device's fixed scratch array (nothing is
+        allocated by the library)."""
+        import torch
+        s = self.shape
+        B = int(obs.shape[0])
+        po = _dev_ptr(obs, "float32", (B, s.n_obs, s.obs_dim))
+        pn = _dev_ptr(noise, "float32", (s.n_steps, B, s.horizon, s.action_dim))
+        pout = _dev_ptr(out, "float32", (B, s.horizon, s.action_dim))
+        ids_np = None if ids is None else np.ascontiguousarray(np.asarray(ids, np.int32))
+        if ids_np is not None and ids_np.shape != (B,):
+            raise ValueError("ids must have shape [B]")
+        st = torch.cuda.current_stream(obs.device) if stream is None else stream
+        _check(lib().evo_denoise_noalloc(self._h, B, po, pn, None if ids_np is None else ids_np.ctypes.data, pout,
+                                         ctypes.c_void_p(st.cuda_stream)))
         return out
 
     def collect_activations(self, obs, noise, ids=None, stream=None):
