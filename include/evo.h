@@ -87,7 +87,8 @@ typedef struct {
  * and an evaluation multiplies only against the S x n_heads folded
  * columns, so there F_CA counts 2(2 H S n_heads d) per evaluation and the
  * query adds 4 n_obs d^2 per layer for the fold.  The byte counters are this implementation's algorithmic
- * traffic: cache reads/writes of reused/refreshed residuals, and weight
+ * traffic: cache reads/writes of reused/refreshed residuals (fp32 values,
+ * bf16 for policies of width above 256 with bf16 operands), and weight
  * bytes of evaluated units summed over workgroups.  n_tiles counts the
  * sample tiles, n_workgroups the workgroups launched (small batches run
  * several workgroups per one-sample tile; each keeps its own caches, so the

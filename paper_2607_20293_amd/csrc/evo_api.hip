@@ -422,8 +422,8 @@ int evo_create_policy(const evo_policy_desc* desc, const float* host_weights, si
           ctr_tiles = std::max(ctr_tiles, (size_t)tc.max_batch);
         }
       }
-      p->cache_floats = (size_t)U * rows * d;
-      CREATE_TRY(hipMalloc(&p->d_cache, p->cache_floats * sizeof(float)));
+      p->cache_floats = (size_t)U * rows * d;  // values (bytes per value: cache_elt)
+      CREATE_TRY(hipMalloc(&p->d_cache, p->cache_floats * s.cache_elt()));
       CREATE_TRY(hipMalloc(&p->d_okv, okv_floats * sizeof(float)));
       CREATE_TRY(hipMalloc(&p->d_rpart, (size_t)s.max_batch * U * T * sizeof(float)));
       if (!p->teams.empty()) {
@@ -592,7 +592,7 @@ static int denoise_impl(evo_policy* p, int32_t batch, const float* obs_cond, con
       const size_t o_plan = off;
       off += al(2 * al(ntile_ent * sizeof(int32_t)) + (size_t)ps.n_used * ucodes);
       const size_t o_cache = off;
-      off += al((size_t)ps.n_tiles * team * s.U() * R * D * sizeof(float));
+      off += al((size_t)ps.n_tiles * team * s.U() * R * D * s.cache_elt());
       const size_t o_okv = off;
       off += al(okv_copies * batch * okv_per * sizeof(float));
       const size_t o_xchg = off;
@@ -896,10 +896,23 @@ int evo_debug_read_cache(evo_policy* p, int32_t unit, int32_t sample, float* hos
     DeviceGuard guard(p->device);
     HIP_TRY(hipDeviceSynchronize());
     const int R = pl.spt * s.H, d = s.d, NW = p->last_threads / 64, RB = R / 16, CBW = d / 16 / NW;
+    const size_t elt = s.cache_elt();
+    std::vector<uint8_t> raw((size_t)R * d * elt);
+    HIP_TRY(hipMemcpy(raw.data(),
+                      reinterpret_cast<const uint8_t*>(p->d_cache) +
+                          ((size_t)tile * p->last_team * s.U() + unit) * R * d * elt,
+                      raw.size(), hipMemcpyDeviceToHost));
     std::vector<float> buf((size_t)R * d);
-    HIP_TRY(hipMemcpy(buf.data(), p->d_cache + ((size_t)tile * p->last_team * s.U() + unit) * R * d,
-                      buf.size() * sizeof(float),
-                      hipMemcpyDeviceToHost));
+    for (size_t i = 0; i < buf.size(); ++i) {
+      if (elt == 2) {
+        uint16_t h;
+        std::memcpy(&h, raw.data() + 2 * i, 2);
+        const uint32_t u = (uint32_t)h << 16;
+        std::memcpy(&buf[i], &u, 4);
+      } else {
+        std::memcpy(&buf[i], raw.data() + 4 * i, 4);
+      }
+    }
     for (int i = 0; i < s.H; ++i) {
       const int row = slot * s.H + i, rb = row / 16, rr = row % 16;
       for (int col = 0; col < d; ++col) {

@@ -315,7 +315,7 @@ void call_stats(const Shape& s, const std::vector<Schedule>& reg, const int32_t*
   std::memset(&st, 0, sizeof(st));
   const Flops f = flops_of(s);
   uint64_t F_layer = f.unit[0] + f.unit[1] + f.unit[2];
-  const uint64_t rowbytes = (uint64_t)s.H * s.d * 4;  // fp32 cache of one sample and unit
+  const uint64_t rowbytes = (uint64_t)s.H * s.d * s.cache_elt();  // cache of one sample and unit
   for (int n = 0; n < batch; ++n) {
     const Schedule& sc = reg[ids ? ids[n] : 0];
     st.refreshes_requested += sc.requested;

@@ -442,6 +442,7 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
   constexpr bool PB_LDS = EMB_LDS && (TEAM > 1 || D <= 64);  // else the row biases stay in registers
   // layer-merged residual sum accumulated in registers, else in its cache slot
   constexpr bool MAC_REG = CBW * RB <= 4;
+  static_assert(MAC_REG || SPT == 1 || sizeof(AT) == 4, "bf16 layer sums in memory need one sample per tile");
   // weight fragments in flight per wave in the unit products
   constexpr int INFL = (TEAM > 1 && RB == 1) ? 16 : (RB == 1 && CBW <= 2 ? 12 : 6);
   constexpr float kScale = (DH == 64) ? 0.125f : (DH == 32 ? 0.17677669529663688f : 0.0f);
@@ -567,7 +568,13 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
   int jrow[RB];
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) jrow[rb] = (rb * 16 + lq * 4) / HZ;
-  float* cbase = p.cache + (size_t)(tile * TEAM + member) * U * (R * D);
+  // residual caches of this workgroup: [3L][R*D] values in fragment order.
+  // bf16 for the width-768 policy with bf16 operands (rounded once per
+  // stored residual; the stream and the layer sums stay fp32), fp32
+  // otherwise: at width 256 bf16 caches measured no faster and took the
+  // population workload's worst sample past the bf16 error bar.
+  constexpr int CE = (sizeof(AT) == 2 && D > 256) ? 2 : 4;
+  unsigned char* const cbase = reinterpret_cast<unsigned char*>(p.cache) + (size_t)(tile * TEAM + member) * U * (R * D) * CE;
   // Team exchange slots: [tile][3][TEAM][R*D] floats, slot n % 3 carries
   // the partials of the n-th evaluated unit.  A slot word that still holds
   // the sentinel has not been written yet; every member resets its own slot
@@ -610,9 +617,26 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
     __syncthreads();
     if (s_abort) return;
   }
-  const auto cfrag = [&](int unit, int c, int rb) {
-    return reinterpret_cast<f32x4*>(cbase + (size_t)unit * (R * D) +
-                                    ((size_t)((w * RB + rb) * CBW + c) * 64 + lane) * 4);
+  // element index of this lane's fragment (c, rb) in a unit's cache slot
+  const auto cidx = [&](int unit, int c, int rb) {
+    return (size_t)unit * (R * D) + ((size_t)((w * RB + rb) * CBW + c) * 64 + lane) * 4;
+  };
+  const auto cload = [&](int unit, int c, int rb) -> f32x4 {
+    if constexpr (CE == 2) {
+      const uint2 x = *reinterpret_cast<const uint2*>(cbase + cidx(unit, c, rb) * 2);
+      return f32x4{__uint_as_float(x.x << 16), __uint_as_float(x.x & 0xFFFF0000u), __uint_as_float(x.y << 16),
+                   __uint_as_float(x.y & 0xFFFF0000u)};
+    } else {
+      return *reinterpret_cast<const f32x4*>(cbase + cidx(unit, c, rb) * 4);
+    }
+  };
+  const auto cstore = [&](int unit, int c, int rb, f32x4 v) {
+    if constexpr (CE == 2) {
+      *reinterpret_cast<uint2*>(cbase + cidx(unit, c, rb) * 2) =
+          make_uint2(bf16_rne(v[0]) | (bf16_rne(v[1]) << 16), bf16_rne(v[2]) | (bf16_rne(v[3]) << 16));
+    } else {
+      *reinterpret_cast<f32x4*>(cbase + cidx(unit, c, rb) * 4) = v;
+    }
   };
   const uint4* pk = p.pk;
 
@@ -701,7 +725,7 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
   // needed reads past the end of a buffer resource, which returns zeros
   // without a memory access), so that they are all in flight before the
   // first is consumed.
-  const auto crs = __builtin_amdgcn_make_buffer_rsrc(cbase, (short)0, U * (R * D) * 4, 0x00020000);
+  const auto crs = __builtin_amdgcn_make_buffer_rsrc(cbase, (short)0, U * (R * D) * CE, 0x00020000);
   const auto issue_batch = [&](uint64_t& um, auto& ub, auto& v) {
 #pragma unroll
     for (int q = 0; q < NB; ++q) {
@@ -719,8 +743,14 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
           for (int jj = 1; jj < SPT; ++jj)
             if (jrow[rb] == jj) mj = mru_cur[jj];
           const bool use = ub[q] >= 0 && ((mj >> ub[q]) & 1ull);
-          const int off = use ? (ub[q] * (R * D) + (((w * RB + rb) * CBW + c) * 64 + lane) * 4) * 4 : 0x7FFFFFF0;
-          v[q][c][rb] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(crs, off, 0, 0));
+          const int off = use ? (ub[q] * (R * D) + (((w * RB + rb) * CBW + c) * 64 + lane) * 4) * CE : 0x7FFFFFF0;
+          if constexpr (CE == 2) {
+            const auto x = __builtin_amdgcn_raw_buffer_load_b64(crs, off, 0, 0);
+            v[q][c][rb] = f32x4{__uint_as_float(x[0] << 16), __uint_as_float(x[0] & 0xFFFF0000u),
+                                __uint_as_float(x[1] << 16), __uint_as_float(x[1] & 0xFFFF0000u)};
+          } else {
+            v[q][c][rb] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(crs, off, 0, 0));
+          }
         }
   };
 
@@ -1397,15 +1427,21 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
             const f32x4 v = r[c][rb];
             if constexpr (MAC_REG) {
               if (mg) mac[c][rb] = (u == 0) ? v : mac[c][rb] + v;
-              if (pick(mst, j) & bit) *cfrag(e, c, rb) = mg ? mac[c][rb] : v;
-            } else {
-              // layer sum kept in the layer's cache slot (the FFN position)
-              if (mg) {
-                f32x4* slot = cfrag(3 * l + 2, c, rb);
-                *slot = (u == 0) ? v : *slot + v;
-              } else if (pick(mst, j) & bit) {
-                *cfrag(e, c, rb) = v;
-              }
+              if (pick(mst, j) & bit) cstore(e, c, rb, mg ? mac[c][rb] : v);
+            } else if (mg) {
+              // layer sum accumulated in memory, in fp32: in the FFN
+              // position's slot (fp32 caches) or across the SA and CA slots,
+              // which a merged layer leaves unused (bf16 caches; one sample
+              // per tile, so no other sample's rows share them); the sum of
+              // the three residuals is stored at the FFN position
+              f32x4* acc = CE == 4 ? reinterpret_cast<f32x4*>(cbase + cidx(3 * l + 2, c, rb) * 4)
+                                   : reinterpret_cast<f32x4*>(cbase + (size_t)(3 * l) * (R * D) * 2 +
+                                                              (cidx(0, c, rb)) * 4);
+              const f32x4 sum = (u == 0) ? v : *acc + v;
+              if (CE == 4 || u < 2) *acc = sum;
+              else if (pick(mst, j) & bit) cstore(e, c, rb, sum);
+            } else if (pick(mst, j) & bit) {
+              cstore(e, c, rb, v);
             }
             h[c][rb] += v;
             if (p.acts != nullptr && member == 0) {
@@ -1415,7 +1451,7 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
               for (int i = 0; i < 4; ++i) ap[(size_t)((rb * 16 + lq * 4 + i) % HZ) * D] = v[i];
             }
           } else if (pick(mru, j) & bit) {
-            h[c][rb] += *cfrag(e, c, rb);
+            h[c][rb] += cload(e, c, rb);
           }
         }
       b = e + 1;

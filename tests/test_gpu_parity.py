@@ -301,7 +301,8 @@ def test_step0_only_cache_holds_step0_residuals(dtype):
         assert (e <= 1e-4) if dtype == "fp32" else (e / scale <= 3e-2), (b, e)
     say(f"  cache readback worst relative error {worst:.2e}")
     per_wg = gst["n_workgroups"] // gst["n_tiles"]
-    assert gst["cache_bytes_written"] == 3 * s.n_layers * s.horizon * s.d_model * 4 * per_wg
+    elt = 4   # fp32 caches at width 256 (bf16 only at width 768 with bf16 operands)
+    assert gst["cache_bytes_written"] == 3 * s.n_layers * s.horizon * s.d_model * elt * per_wg
     pol.close()
 
 
