@@ -372,7 +372,12 @@ typedef struct {
  * histories as evo_ga_search.  Needs pop_size <= max_schedules; the search
  * overwrites schedule ids 0 .. pop_size-1 (their contents afterwards are
  * unspecified).  Allocates and frees its own device workspace; synchronous
- * (returns when the search is done); runs on hip_stream. */
+ * (returns when the search is done); runs on hip_stream.  Every denoising
+ * call of the search runs one workgroup per sample tile, whatever its
+ * batch (no small-batch teams): those variants give a sample the same bits
+ * at any batch size, so a schedule's fitness does not depend on how many
+ * schedules its generation evaluates.  A policy created with EVO_TEAM=0
+ * reproduces a search's chunks bit for bit through evo_denoise. */
 int evo_search(evo_policy* p, const evo_ga_config* cfg, const evo_search_options* opt, const float* obs_quick,
                const float* noise_quick, const float* obs_formal, const float* noise_formal, const double* probs,
                evo_search_result* result, int32_t* best_out, int32_t* pop_history, double* fit_history,

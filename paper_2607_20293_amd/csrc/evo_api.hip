@@ -516,9 +516,13 @@ struct CallBuffers {
 // noalloc: the call's buffers are carved from the device scratch array, the
 // plan is written straight into pinned staging memory and always uploaded,
 // and nothing is allocated (device, pinned or host heap).
+// allow_team = false: one workgroup per tile whatever the batch (the
+// single- and two-sample-tile variants sum in the same order, so results do
+// not depend on the batch size; the small-batch teams sum their partial
+// residuals in another order).
 static int denoise_impl(evo_policy* p, int32_t batch, const float* obs_cond, const float* noise,
                         const int32_t* schedule_ids, float* actions_out, float* acts_out, void* hip_stream,
-                        bool noalloc = false) {
+                        bool noalloc = false, bool allow_team = true) {
   return guarded([&]() -> int {
     clear_error();
     if (!p) return fail(EVO_E_INVALID, "policy is NULL");
@@ -549,7 +553,7 @@ static int denoise_impl(evo_policy* p, int32_t batch, const float* obs_cond, con
     // small batches: several workgroups per one-sample tile
     const evo_policy::TeamCfg* tc = nullptr;
     for (const auto& c : p->teams) {
-      if (batch > c.max_batch) continue;
+      if (!allow_team || batch > c.max_batch) continue;
       KernelKey k{s.d, s.dh(), s.H, s.dff, s.dtype, 1, c.team};
       int th;
       if (kernel_available(k, &th)) {
@@ -719,6 +723,17 @@ static int denoise_impl(evo_policy* p, int32_t batch, const float* obs_cond, con
     return EVO_OK;
   });
 }
+
+}  // extern "C"
+
+namespace evo {
+int denoise_one_workgroup_per_tile(evo_policy* p, int32_t batch, const float* obs_cond, const float* noise,
+                                   const int32_t* schedule_ids, float* actions_out, void* hip_stream) {
+  return denoise_impl(p, batch, obs_cond, noise, schedule_ids, actions_out, nullptr, hip_stream, false, false);
+}
+}  // namespace evo
+
+extern "C" {
 
 int evo_synchronize(evo_policy* p) {
   clear_error();

@@ -138,6 +138,10 @@ int guided_sample(const double* p, int rows, int T, int K, const double* u, int3
 // shape and device of a policy (evo_api.hip)
 const Shape& policy_shape(const evo_policy* p);
 int policy_device(const evo_policy* p);
+// evo_denoise with one workgroup per tile at every batch size: results do
+// not depend on the batch (evo_api.hip)
+int denoise_one_workgroup_per_tile(evo_policy* p, int32_t batch, const float* obs_cond, const float* noise,
+                                   const int32_t* schedule_ids, float* actions_out, void* hip_stream);
 
 // Runs an ABI call's body and turns C++ exceptions (host allocation
 // failures of vectors sized by the caller's arguments) into error codes, so

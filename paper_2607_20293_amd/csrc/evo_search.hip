@@ -3,7 +3,10 @@
 // schedule id per candidate, each candidate on the same n_quick episodes;
 // the deviation of every chunk from the uncached chunk of its episode is
 // reduced on the device and only [batch] floats come back to the host,
-// where the GA (evo_ga.cpp) ranks, selects and breeds.
+// where the GA (evo_ga.cpp) ranks, selects and breeds.  Every call runs
+// one workgroup per tile (no small-batch teams), whose results do not
+// depend on the batch size, so a schedule's fitness does not depend on how
+// many new schedules its generation has.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -116,10 +119,10 @@ extern "C" int evo_search(evo_policy* p, const evo_ga_config* cfg, const evo_sea
     rc = evo_set_schedule(p, 0, all.data(), rows, T, opt->granularity);
     if (rc) return rc;
     std::vector<int32_t> ids((size_t)bmax, 0);
-    rc = evo_denoise(p, nq, obs_quick, noise_quick, ids.data(), w.ref_q, stream);
+    rc = denoise_one_workgroup_per_tile(p, nq, obs_quick, noise_quick, ids.data(), w.ref_q, stream);
     if (rc) return rc;
     if (nf > 0) {
-      rc = evo_denoise(p, nf, obs_formal, noise_formal, ids.data(), w.ref_f, stream);
+      rc = denoise_one_workgroup_per_tile(p, nf, obs_formal, noise_formal, ids.data(), w.ref_f, stream);
       if (rc) return rc;
     }
     std::vector<float> dev((size_t)bmax);
@@ -156,7 +159,7 @@ extern "C" int evo_search(evo_policy* p, const evo_ga_config* cfg, const evo_sea
         built_for = n;
       }
       for (int i = 0; i < batch; ++i) ids[i] = i / nq;
-      int r = evo_denoise(p, batch, w.obs, w.noise, ids.data(), w.out, stream);
+      int r = denoise_one_workgroup_per_tile(p, batch, w.obs, w.noise, ids.data(), w.out, stream);
       if (r) return r;
       r = deviations(batch, w.ref_q, nq);
       if (r) return r;
@@ -172,7 +175,7 @@ extern "C" int evo_search(evo_policy* p, const evo_ga_config* cfg, const evo_sea
         int r = set_pairs(0, sch);
         if (r) return r;
         std::fill(ids.begin(), ids.begin() + nf, 0);
-        r = evo_denoise(p, nf, obs_formal, noise_formal, ids.data(), w.out, stream);
+        r = denoise_one_workgroup_per_tile(p, nf, obs_formal, noise_formal, ids.data(), w.out, stream);
         if (r) return r;
         r = deviations(nf, w.ref_f, nf);
         if (r) return r;

@@ -450,6 +450,39 @@ def test_automatic_team_choice():
         assert per == want, f"{dtype} batch {B}: {per} workgroups per tile, expected {want}"
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+def test_one_workgroup_per_tile_is_batch_independent(dtype):
+    """With one workgroup per tile (teams switched off), a sample's chunk is
+    the same bits at batch 8 and n_cu - 1 (one-sample tiles) and at
+    n_cu + 64 (two-sample tiles, the sample's partner differing with the
+    batch): the variants sum every product in the same order.  The
+    schedule search runs this way."""
+    import torch
+    n_cu = torch.cuda.get_device_properties(0).multi_processor_count
+    s = I.PUSHT
+    wts = I.make_weights(s, 6, "perturbed")
+    Bmax = n_cu + 64
+    obs, noise = I.make_obs(s, Bmax, 6), I.make_noise(s, Bmax, 6)
+    rng = np.random.default_rng([6, 3])
+    lats = [I.lattice_bernoulli(s.n_layers, s.n_steps, p, rng) for p in (0.2, 0.5)]
+    ids = rng.integers(0, 2, Bmax).astype(np.int32)
+    outs = {}
+    for B in (8, n_cu - 1, Bmax):
+        say(f"[gpu] one workgroup per tile: {dtype} batch {B}")
+        pol = _policy(s, wts, dtype, B, 2, team=False)
+        for j, lt in enumerate(lats):
+            pol.set_schedule(j, lt, O.GRAN_LAYER)
+        got, st = run_gpu(pol, obs[:B], noise[:, :B], ids[:B])
+        pol.close()
+        assert st["n_workgroups"] == st["n_tiles"] == (B if B < n_cu else (B + 1) // 2)
+        outs[B] = got
+    for B in (n_cu - 1, Bmax):
+        assert np.array_equal(outs[B][:8], outs[8]), B
+    assert np.array_equal(outs[Bmax][:n_cu - 1], outs[n_cu - 1])
+    ref, _ = run_oracle(s, wts, obs[:8], noise[:, :8], lats, ids[:8], O.GRAN_LAYER, O.COLD_COMPUTE, dtype)
+    compare(outs[8], ref, dtype, f"{dtype} batch 8, one workgroup per tile")
+
+
 def test_replacing_a_schedule_between_calls():
     """The plan upload is skipped when the plan bytes are unchanged, so a
     schedule replaced under the same id (same batch, same ids) must still
