@@ -40,11 +40,16 @@ constexpr uint64_t kMergedBit = 1ull << 63;
 constexpr int kMaskEntries = 341;  // (T x samples per tile) entries of 3 x u64 in LDS (8 KiB)
 constexpr int kMaxLayers = 21;     // 3L <= 63 units (one 64-bit mask per step)
 
-// float -> bfloat16 bits, round to nearest even (finite inputs)
+// float -> bfloat16 bits, round to nearest even: gfx950's conversion
+// instruction (v_cvt_pk_bf16_f32), two values at a time where possible
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ uint32_t bf16_rne(float f) {
-  uint32_t u = __float_as_uint(f);
-  u += 0x7FFFu + ((u >> 16) & 1u);
-  return u >> 16;
+  return __builtin_bit_cast(uint16_t, (__bf16)f);
+}
+// (bf16(lo) | bf16(hi) << 16)
+__device__ __forceinline__ uint32_t bf16x2_rne(float lo, float hi) {
+  const bf16x2_t v = {(__bf16)lo, (__bf16)hi};
+  return __builtin_bit_cast(uint32_t, v);
 }
 
 __device__ __forceinline__ f32x4 mfma4(float a, float b, f32x4 c) {
@@ -633,7 +638,7 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
   const auto cstore = [&](int unit, int c, int rb, f32x4 v) {
     if constexpr (CE == 2) {
       *reinterpret_cast<uint2*>(cbase + cidx(unit, c, rb) * 2) =
-          make_uint2(bf16_rne(v[0]) | (bf16_rne(v[1]) << 16), bf16_rne(v[2]) | (bf16_rne(v[3]) << 16));
+          make_uint2(bf16x2_rne(v[0], v[1]), bf16x2_rne(v[2], v[3]));
     } else {
       *reinterpret_cast<f32x4*>(cbase + cidx(unit, c, rb) * 4) = v;
     }
@@ -1093,10 +1098,10 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
               uint4 bq;
               if constexpr (sizeof(AT) == 2) {
                 const f32x4 x0 = ub[rb][kf][0], x1 = ub[rb][kf][1];
-                bq.x = bf16_rne(x0[0]) | (bf16_rne(x0[1]) << 16);
-                bq.y = bf16_rne(x0[2]) | (bf16_rne(x0[3]) << 16);
-                bq.z = bf16_rne(x1[0]) | (bf16_rne(x1[1]) << 16);
-                bq.w = bf16_rne(x1[2]) | (bf16_rne(x1[3]) << 16);
+                bq.x = bf16x2_rne(x0[0], x0[1]);
+                bq.y = bf16x2_rne(x0[2], x0[3]);
+                bq.z = bf16x2_rne(x1[0], x1[1]);
+                bq.w = bf16x2_rne(x1[2], x1[3]);
               } else {
                 bq = __builtin_bit_cast(uint4, ub[rb][kf][0]);
               }
