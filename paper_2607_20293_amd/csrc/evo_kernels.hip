@@ -455,7 +455,11 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
 
   __shared__ __attribute__((aligned(16))) AT xa[R * LDA];
   __shared__ __attribute__((aligned(16))) float ybuf[R * LDY > C::FOLD_LDS ? R * LDY : C::FOLD_LDS];
-  __shared__ __attribute__((aligned(16))) AT zbuf[R * LDZ];
+  // the feed-forward chunks alternate between two operand buffers, so a
+  // chunk's GELU outputs never overwrite the previous chunk's while a wave
+  // may still read them, and no barrier ends a chunk (where LDS allows)
+  constexpr bool ZB2 = D <= 256 && !(sizeof(AT) == 4 && SPT > 1);
+  __shared__ __attribute__((aligned(16))) AT zbuf[(ZB2 ? 2 : 1) * R * LDZ];
   __shared__ __attribute__((aligned(16))) float pw[NW * PWN];
   __shared__ __attribute__((aligned(16))) float kvbuf[SPT * SMAX * 2 * GW];
   __shared__ float red[NW][R][2];
@@ -1265,6 +1269,7 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
         layer_norm_to_xa();
         for (int ch = member; ch < DFF / FC; ch += TEAM) {
           asm volatile("" : "+v"(lane), "+v"(lc), "+v"(lq));
+          AT* const zb = zbuf + (ZB2 ? (((ch - member) / TEAM) & 1) * (R * LDZ) : 0);
           f32x4 y[MPWF][RB];
 #pragma unroll
           for (int m = 0; m < MPWF; ++m)
@@ -1283,14 +1288,16 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
             for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
               for (int i = 0; i < 4; ++i)
-                O::store(zbuf, LDZ, rb * 16 + lq * 4 + i, loc, gelu_erf(y[m][rb][i] + b1v[m]));
+                O::store(zb, LDZ, rb * 16 + lq * 4 + i, loc, gelu_erf(y[m][rb][i] + b1v[m]));
           }
           // the next chunk's first stage-1 k-steps stream in during this chunk's second product
           if (ch + TEAM < DFF / FC) gemm_pref<NPF, MPWF>(b1f, pk + po.w1, D / O::KF, 0, gcb_ff(ch + TEAM), lane);
           __syncthreads();
-          gemm_run<AT, RB, CBW, FC / O::KF, INFL, NP2F>(r, zbuf, LDZ, pk + po.w2, DFF / O::KF, ch * (FC / O::KF), own,
+          gemm_run<AT, RB, CBW, FC / O::KF, INFL, NP2F>(r, zb, LDZ, pk + po.w2, DFF / O::KF, ch * (FC / O::KF), own,
                                                         lane, b2);
-          __syncthreads();
+          // (with one buffer, the next chunk's GELU outputs wait for every
+          // wave's reads of this one)
+          if constexpr (!ZB2) __syncthreads();
         }
       }
       if constexpr (TEAM > 1) if (!(fold && u == 1)) {
