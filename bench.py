@@ -27,7 +27,7 @@ sys.path.insert(0, ROOT)
 METRIC = "action chunks/sec at batch 256 + p50 latency/chunk at batch 1, 25%-density schedule"
 PEAK = {"bf16": 2500.0, "fp32": 157.3}           # dense MFMA TFLOP/s of MI355X
 HBM_PEAK_GBS = 8000.0
-COUNTERS = os.path.join(ROOT, "profiles", "denoise_kernel_image_b256_counters.json")
+COUNTERS = os.path.join(ROOT, "profiles", "denoise_kernel_counters.json")
 
 
 def log(*a):
@@ -330,9 +330,14 @@ def main():
     if os.path.exists(COUNTERS):
         try:
             c = json.load(open(COUNTERS))
-            if c.get("source_sha") == kernel_source_sha() and c.get("workload") == w.name:
-                roof["traffic"] = c["hbm_bytes_per_launch"]
-                roof["mfma_util_pct_counter"] = c.get("mfma_util_pct")
+            cw = c.get("workloads", {}).get(w.name)
+            if c.get("source_sha") == kernel_source_sha() and cw:
+                # HBM bytes of one denoise_kernel launch (FETCH_SIZE and
+                # WRITE_SIZE scaled by a 256 MiB copy), taken while this
+                # kernel source was current
+                roof["traffic"] = cw["hbm_bytes_per_launch"]
+                roof["traffic_GBps"] = round(cw["hbm_bytes_per_launch"] / (den_ms * 1e-3) / 1e9, 1)
+                roof["mfma_util_pct_counter"] = cw.get("mfma_util_pct")
         except Exception:
             pass
 
