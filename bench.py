@@ -210,6 +210,10 @@ def bench_encoder(dev):
     enc_ms = ev[0].elapsed_time(ev[1]) / reps
     enc_tf = enc.flops(nf) / (enc_ms * 1e-3) / 1e12
     flops_frame = enc.flops(1)
+    enc.close()
+    # the batch-1 query runs on an encoder planned for its own batch (the
+    # work split follows max_batch)
+    enc = evo.Encoder(e, I.make_encoder_weights(e, 0), "bf16", max_batch=s.n_obs)
     wts = I.make_weights(s, 0)
     img1 = imgs[:s.n_obs].contiguous()
     pa = {}

@@ -484,7 +484,12 @@ int evo_create_encoder(const evo_encoder_desc* desc, const float* host_weights, 
  * features can be written straight into a policy's observation rows);
  * other elements are not touched.  Asynchronous on hip_stream (NULL = the
  * null stream); uses the encoder's activation buffers, so calls on one
- * encoder must not overlap. */
+ * encoder must not overlap.  The work split (convolution K splits,
+ * GroupNorm statistics chunks) is planned for max_batch, so an image's
+ * features are bitwise the same at every batch size of one encoder and do
+ * not depend on the other images; encoders created with different
+ * max_batch may differ in the last bits.  A batch well below max_batch runs
+ * that plan on fewer workgroups. */
 int evo_encode(evo_encoder* e, int32_t batch, const float* images, float* features_out, int32_t out_stride,
                void* hip_stream);
 

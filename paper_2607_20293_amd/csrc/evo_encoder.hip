@@ -40,10 +40,15 @@ constexpr int kTargetWG = 512;      // split K below this many output tiles
 constexpr int kMaxSplit = 16;
 constexpr long long kWsFloats = 1024ll * 4096;  // split-K partials (>= splits * tiles * 64 * 64)
 // GroupNorm workgroups aimed at when chunking an image's pixels (statistics
-// and apply passes).  The chunking follows the batch size, so across batch
-// sizes the statistics may be summed in other groupings (last-bit
-// differences); for one batch size an image's result does not depend on the
-// other images.  (Fixed chunks of 64 or 128 pixels measured 3-8% slower.)
+// and apply passes).  The K splits of the convolutions and the pixel chunks
+// of the GroupNorm statistics are planned for the encoder's max_batch, not
+// for the batch of a call: every call then sums an image's products and
+// statistics in the same groupings, so an image's features do not depend on
+// the batch size or on the other images.  A smaller batch runs the same
+// per-image plan on fewer workgroups (an encoder meant for small batches is
+// created with a small max_batch).  The apply pass is elementwise, so its
+// chunking follows the call's batch.  (Fixed chunks of 64 or 128 pixels
+// measured 3-8% slower.)
 constexpr int kGnTarget = 1024;
 
 template <class AT> struct ConvStep;
@@ -614,7 +619,9 @@ hipError_t launch_conv(const evo_encoder* e, const ConvLayer& L, const float* x,
   a.Kp = L.Kp;
   a.M = N * a.Ho * a.Wo;
   const int KS = e->bf ? ConvStep<__bf16>::KS : ConvStep<float>::KS;
-  const ConvPlan pl = plan_conv(a.M, L.cout, L.Kp / KS);
+  // K splits of the max_batch plan; tiles for this call's pixels
+  ConvPlan pl = plan_conv(e->desc.max_batch * a.Ho * a.Wo, L.cout, L.Kp / KS);
+  pl.mt = cdiv(a.M, kBM);
   a.mt = pl.mt;
   a.nt = pl.nt;
   a.splits = pl.splits;
@@ -641,7 +648,8 @@ hipError_t launch_gn(const evo_encoder* e, const ConvLayer& L, GnArgs g, int N, 
   while (gpw * 2 * G <= 64 && groups % (gpw * 2) == 0) gpw *= 2;
   const int chunks = groups / gpw, HW = H * W;
   const int base = N * chunks;
-  const int ps = std::max(1, std::min(cdiv(kGnTarget, base), cdiv(HW, 16)));
+  // statistics chunks of the max_batch plan (see kGnTarget)
+  const int ps = std::max(1, std::min(cdiv(kGnTarget, e->desc.max_batch * chunks), cdiv(HW, 16)));
   if ((size_t)N * groups * ps > e->part_cap) return hipErrorInvalidValue;  // sized at creation
   g.gamma = L.gamma;
   g.beta = L.beta;

@@ -84,10 +84,10 @@ def test_encoder_robomimic_bf16_default_affine():
 
 
 def test_encoder_batch_independent():
-    """For one batch size, an image's features do not depend on the other
-    images of the batch or on its position in it (bit-exact, with maps large
-    enough for several GroupNorm chunks).  Across batch sizes the GroupNorm
-    chunking may differ, so only the last bits may change."""
+    """An image's features do not depend on the other images of the batch,
+    on its position in it or on the batch size (bit-exact, one encoder, with
+    maps large enough for several GroupNorm chunks and late layers whose
+    convolutions split K)."""
     torch = _torch()
     from paper_2607_20293_amd import evo
     e = I.ENC_PUSHT
@@ -99,11 +99,13 @@ def test_encoder_batch_independent():
     c = run([1, 7, 8, 9])
     assert np.array_equal(a[1], b[1]) and np.array_equal(a[1], c[0])
     enc.close()
-    enc = evo.Encoder(e, I.make_encoder_weights(e, 3, "perturbed"), "fp32", max_batch=10)
-    one = run([1])[0]
-    ten = run(list(range(10)))[1]
-    np.testing.assert_allclose(one, ten, rtol=1e-5, atol=1e-6)
-    enc.close()
+    for dtype in ("fp32", "bf16"):
+        enc = evo.Encoder(e, I.make_encoder_weights(e, 3, "perturbed"), dtype, max_batch=10)
+        one = run([1])[0]
+        three = run([5, 1, 7])[1]
+        ten = run(list(range(10)))[1]
+        assert np.array_equal(one, ten) and np.array_equal(one, three), dtype
+        enc.close()
 
 
 def test_encoder_rejects_bad_arguments():
