@@ -1141,19 +1141,18 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
             for (int j = 0; j < SJ; ++j) pb[(j * NH + hd) * R + r] = sc[j] * inv;
           }
           __syncthreads();
-          // output: r = P W over the 16 columns (padding columns are zero)
+          // output: r = P W over the 16 columns (padding columns are zero),
+          // four k-steps of fp32 MFMA per column block
 #pragma unroll
           for (int rb = 0; rb < RB; ++rb) {
-#pragma unroll 4
-            for (int n = 0; n < 16; ++n) {
-              const f32x4 pv = *reinterpret_cast<const f32x4*>(pb + n * R + rb * 16 + lq * 4);
+            float pa[4];
 #pragma unroll
-              for (int c = 0; c < CBW; ++c) {
-                const float wc = wst[(rb * 16 + n) * D + (w * CBW + c) * 16 + lc];
+            for (int kk = 0; kk < 4; ++kk) pa[kk] = pb[(4 * kk + lq) * R + rb * 16 + lc];
 #pragma unroll
-                for (int i = 0; i < 4; ++i) r[c][rb][i] = fmaf(pv[i], wc, r[c][rb][i]);
-              }
-            }
+            for (int c = 0; c < CBW; ++c)
+#pragma unroll
+              for (int kk = 0; kk < 4; ++kk)
+                r[c][rb] = mfma4(pa[kk], wst[(rb * 16 + 4 * kk + lq) * D + (w * CBW + c) * 16 + lc], r[c][rb]);
           }
         }
       } else if (u == 1) {
