@@ -205,7 +205,8 @@ size_t evo_noalloc_scratch_bytes(void);
  * evo_create_policy: EVO_TEAM=0 disables that variant, EVO_TEAM=<n> keeps
  * only teams of n workgroups (of those compiled); EVO_TEAM_SPIN_LIMIT
  * sets the number of polls before a wait gives up (default 2^20, about a
- * second); EVO_TEAM_TEST_WITHHOLD=1 is a test hook that makes team member 0
+ * second; checked every 32 polls, so smaller values act as 32);
+ * EVO_TEAM_TEST_WITHHOLD=1 is a test hook that makes team member 0
  * withhold its partial residuals, so that the other members' waits time out
  * and this error path can be exercised (outputs are then invalid). */
 int evo_synchronize(evo_policy* p);

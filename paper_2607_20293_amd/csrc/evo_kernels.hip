@@ -1320,17 +1320,19 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
             if (!(p.withhold && member == 0))
               __builtin_amdgcn_raw_buffer_store_b128(v, xr, xoff(cur, member, c, rb), 0, kCoherent);
           }
-        // bounded wait for every word of `v` (loaded by `load`) to be written
+        // bounded wait for every word of `v` (loaded by `load`) to be written;
+        // polls back to back (each is a memory round trip), the error flag
+        // and the limit are checked every 32 polls
         const auto poll = [&](auto& v, auto load, auto ready) {
           unsigned spins = 0;
           while (true) {
             load(v);
             if (ready(v)) break;
-            if (__hip_atomic_load(p.derr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u || ++spins > p.spin_limit) {
+            if ((++spins & 31u) == 0u &&
+                (__hip_atomic_load(p.derr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u || spins > p.spin_limit)) {
               __hip_atomic_store(p.derr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
               break;
             }
-            __builtin_amdgcn_s_sleep(1);
           }
         };
         const auto full = [&](const u32x4& x) {
