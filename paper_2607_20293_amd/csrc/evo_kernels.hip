@@ -356,13 +356,12 @@ __device__ void fold_rows(const float* __restrict__ raw, uint32_t wq, uint32_t w
 
 // LayerNorm statistics of the tile rows from the register-resident stream:
 // per-lane (mean, M2) over its columns, merged across the 16 lanes of a row
-// group with shuffles; the waves' partials of row r are merged by thread r
-// alone (one dependent chain per row instead of every lane merging all of
-// its rows) and broadcast through LDS (two barriers).
+// group with shuffles; the waves' partials meet in LDS (one barrier) and
+// every wave merges them for all rows in a fixed tree (pairwise, equal
+// counts), so all waves hold the same bits.
 template <class C>
 __device__ __forceinline__ void ln_stats(const f32x4 (&h)[C::CBW][C::RB], float (*red)[C::R][2],
-                                         float (*fin)[2], float (&mu)[C::RB][4], float (&rs)[C::RB][4], int w,
-                                         int lc, int lq, int tid) {
+                                         float (&mu)[C::RB][4], float (&rs)[C::RB][4], int w, int lc, int lq) {
   constexpr int D = C::CB * 16;
   constexpr float nw = 16.0f * C::CBW;
 #pragma unroll
@@ -398,29 +397,39 @@ __device__ __forceinline__ void ln_stats(const f32x4 (&h)[C::CBW][C::RB], float 
       }
     }
   __syncthreads();
-  if (tid < C::R) {
-    const int row = tid;
-    float M = red[0][row][0], Q = red[0][row][1], n = nw;
+  // every wave merges the wave partials itself (no second barrier): the
+  // four lanes of a quad take one row, each its share of the waves, then
+  // two symmetric quad merges give all four the same bits; lane l then
+  // holds the statistics of row l / 4 of the row block
+  static_assert(C::NWV % 4 == 0, "waves per quad lane");
+  constexpr int WPL = C::NWV / 4;
+  const int lane = lc + 16 * lq, qrow = lane >> 2, qp = lane & 3;
 #pragma unroll
-    for (int ww = 1; ww < C::NWV; ++ww) {
-      const float mb = red[ww][row][0], qb = red[ww][row][1];
-      const float d = mb - M, tot = n + nw;
-      M += d * (nw / tot);
-      Q += qb + d * d * (n * nw / tot);
-      n = tot;
-    }
-    fin[row][0] = M;
-    fin[row][1] = fast_rsqrt(Q * (1.0f / D) + 1e-5f);
+  for (int rb = 0; rb < C::RB; ++rb) {
+    const int row = rb * 16 + qrow;
+    float m = red[qp * WPL][row][0], q = red[qp * WPL][row][1], n = nw;
+    const auto merge = [&](float mo, float qo) {
+      const float d = mo - m;
+      m = 0.5f * (m + mo);
+      q = q + qo + d * d * (0.5f * n);
+      n *= 2.f;
+    };
+#pragma unroll
+    for (int x = 1; x < WPL; ++x) merge(red[qp * WPL + x][row][0], red[qp * WPL + x][row][1]);
+    merge(dpp_mov<0xB1>(m), dpp_mov<0xB1>(q));
+    merge(dpp_mov<0x4E>(m), dpp_mov<0x4E>(q));
+    const float r_ = fast_rsqrt(q * (1.0f / D) + 1e-5f);
+    // rows lq * 4 + i sit in lanes 16 lq + 4 i: a swizzle inside each
+    // 32-lane half keeps lane bit 4 and sets bits 2..3 to i
+#define EVO_LN_PICK(i)                                                                              \
+    mu[rb][i] = __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(m), 0x10 | ((4 * (i)) << 5))); \
+    rs[rb][i] = __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(r_), 0x10 | ((4 * (i)) << 5)));
+    EVO_LN_PICK(0)
+    EVO_LN_PICK(1)
+    EVO_LN_PICK(2)
+    EVO_LN_PICK(3)
+#undef EVO_LN_PICK
   }
-  __syncthreads();
-#pragma unroll
-  for (int rb = 0; rb < C::RB; ++rb)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int row = rb * 16 + lq * 4 + i;
-      mu[rb][i] = fin[row][0];
-      rs[rb][i] = fin[row][1];
-    }
 }
 
 template <class AT, int D, int DH, int HZ, int SPT, int DFF, int NW, int HG, int FC, int SMAX, int TEAM>
@@ -463,7 +472,6 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
   __shared__ __attribute__((aligned(16))) float pw[NW * PWN];
   __shared__ __attribute__((aligned(16))) float kvbuf[SPT * SMAX * 2 * GW];
   __shared__ float red[NW][R][2];
-  __shared__ float fin[R][2];
   __shared__ __attribute__((aligned(16))) float xs[R * 16];
   __shared__ uint64_t msk[kMaskEntries * 3];
   __shared__ LayerOff s_loff[kMaxLayers];
@@ -921,7 +929,7 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
       // LayerNorm of the unit's input into the stage-1 operand buffer
       const auto layer_norm_to_xa = [&]() {
         float mu[RB][4], rs[RB][4];
-        ln_stats<C>(h, red, fin, mu, rs, w, lc, lq, tid);
+        ln_stats<C>(h, red, mu, rs, w, lc, lq);
 #pragma unroll
         for (int c = 0; c < CBW; ++c) {
           const int col = (w * CBW + c) * 16 + lc;
@@ -1473,7 +1481,7 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
     // ---- head (final LayerNorm + linear on fp32 MFMA) and DDPM update
     {
       float mu[RB][4], rs[RB][4];
-      ln_stats<C>(h, red, fin, mu, rs, w, lc, lq, tid);
+      ln_stats<C>(h, red, mu, rs, w, lc, lq);
       f32x4 eacc[RB];
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb) eacc[rb] = f32x4{0.f, 0.f, 0.f, 0.f};
