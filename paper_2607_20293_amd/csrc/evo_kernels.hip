@@ -1058,41 +1058,43 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
           };
           const f32x4 zero4 = {0.f, 0.f, 0.f, 0.f};
           // u columns of this wave's k-range (the B operand of the scores)
+          // (loaded values are zeroed where they do not exist only at their
+          // use, after the LayerNorm, so that no wait for them sits before
+          // its barriers)
           f32x4 ub[RB][KPW][VQ];
+          bool ubok[RB];
 #pragma unroll
           for (int rb = 0; rb < RB; ++rb) {
-            bool ok;
-            const float* q = rec(rb, lc / NH, ok) + (lc % NH) * D + w * KPW * O::KF + lq * O::VE;
+            const float* q = rec(rb, lc / NH, ubok[rb]) + (lc % NH) * D + w * KPW * O::KF + lq * O::VE;
 #pragma unroll
             for (int kf = 0; kf < KPW; ++kf)
 #pragma unroll
-              for (int v = 0; v < VQ; ++v) {
-                const f32x4 x = *reinterpret_cast<const f32x4*>(q + kf * O::KF + 4 * v);
-                ub[rb][kf][v] = ok ? x : zero4;
-              }
+              for (int v = 0; v < VQ; ++v) ub[rb][kf][v] = *reinterpret_cast<const f32x4*>(q + kf * O::KF + 4 * v);
           }
           // w vectors of the row blocks' samples, staged through LDS
           constexpr int WQN = RB * 16 * D / 4, WQ = (WQN + NT - 1) / NT;
           f32x4 wv[WQ];
+          bool wvok[WQ];
 #pragma unroll
           for (int q = 0; q < WQ; ++q) {
             const int it = tid + q * NT;
             const int f = it * 4, rb = f / (16 * D), n = (f / D) % 16, c = f % D;
             bool ok = false;
             const float* src = it < WQN ? rec(rb, n / NH, ok) : trec;
-            const f32x4 x = *reinterpret_cast<const f32x4*>(src + NH * D + (n % NH) * D + c);
-            wv[q] = (it < WQN && ok) ? x : zero4;
+            wv[q] = *reinterpret_cast<const f32x4*>(src + NH * D + (n % NH) * D + c);
+            wvok[q] = it < WQN && ok;
           }
           // c terms of the softmax thread's (row, head)
           float cqv[SJ];
+          bool cqok[SJ];
           {
             const int r = tid / NH, hd = tid % NH;
 #pragma unroll
             for (int j = 0; j < SJ; ++j) {
               bool ok = false;
               const float* src = tid < R * NH ? rec(r >> 4, j, ok) : trec;
-              const float x = src[2 * NH * D + hd];
-              cqv[j] = (tid < R * NH && ok) ? x : 0.f;
+              cqv[j] = src[2 * NH * D + hd];
+              cqok[j] = tid < R * NH && ok;
             }
           }
           layer_norm_to_xa();
@@ -1109,13 +1111,13 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
                   *reinterpret_cast<const uint4*>(xa + (rb * 16 + lc) * LDA + (w * KPW + kf) * O::KF + lq * O::VE);
               uint4 bq;
               if constexpr (sizeof(AT) == 2) {
-                const f32x4 x0 = ub[rb][kf][0], x1 = ub[rb][kf][1];
+                const f32x4 x0 = ubok[rb] ? ub[rb][kf][0] : zero4, x1 = ubok[rb] ? ub[rb][kf][1] : zero4;
                 bq.x = bf16x2_rne(x0[0], x0[1]);
                 bq.y = bf16x2_rne(x0[2], x0[3]);
                 bq.z = bf16x2_rne(x1[0], x1[1]);
                 bq.w = bf16x2_rne(x1[2], x1[3]);
               } else {
-                bq = __builtin_bit_cast(uint4, ub[rb][kf][0]);
+                bq = __builtin_bit_cast(uint4, ubok[rb] ? ub[rb][kf][0] : zero4);
               }
               O::mma(acc, a, bq);
             }
@@ -1123,7 +1125,7 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
           }
 #pragma unroll
           for (int q = 0; q < WQ; ++q)
-            if (tid + q * NT < WQN) *reinterpret_cast<f32x4*>(wst + (tid + q * NT) * 4) = wv[q];
+            if (tid + q * NT < WQN) *reinterpret_cast<f32x4*>(wst + (tid + q * NT) * 4) = wvok[q] ? wv[q] : zero4;
           __syncthreads();
           // softmax over the memory tokens of each (row, head)
           if (tid < R * NH) {
@@ -1135,7 +1137,7 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
               float a = 0.f;
 #pragma unroll
               for (int ww = 0; ww < NW; ++ww) a += sb[((ww * RB + rb) * 64 + (rr >> 2) * 16 + n) * 4 + (rr & 3)];
-              sc[j] = j < S ? (a + cqv[j]) * (kScale * kLog2e) : -INFINITY;
+              sc[j] = j < S ? (a + (cqok[j] ? cqv[j] : 0.f)) * (kScale * kLog2e) : -INFINITY;
               mx = fmaxf(mx, sc[j]);
             }
             float den = 0.f;
@@ -1170,6 +1172,7 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
         // memory keys/values of a head group: time token + observation tokens
         constexpr int KVN = SPT * SMAX * 2 * GW, KVQ = (KVN + NT - 1) / NT;
         float kvv[KVQ];
+        bool kvok[KVQ];
         // branch-free: every lane loads (entries outside the memory tokens
         // read the time-token row and are zeroed), so the loads issue back
         // to back instead of one guarded branch each
@@ -1185,8 +1188,8 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
             const bool obs_tok = ok && sm_ > 0;
             // 32-bit offsets: the observation K/V of a member is below 2^31 floats
             const int off = obs_tok ? ((s_ * L + l) * nobs + (sm_ - 1)) * (2 * D) + gcol : gcol;
-            const float v = (obs_tok ? okv : trow)[off];
-            kvv[q] = ok ? v : 0.f;
+            kvv[q] = (obs_tok ? okv : trow)[off];
+            kvok[q] = ok;
           }
         };
         load_kv(member);
@@ -1215,7 +1218,7 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
           }
 #pragma unroll
           for (int q = 0; q < KVQ; ++q)
-            if (tid + q * NT < KVN) kvbuf[tid + q * NT] = kvv[q];
+            if (tid + q * NT < KVN) kvbuf[tid + q * NT] = kvok[q] ? kvv[q] : 0.f;
           __syncthreads();
           // Each row attends to the S = 1 + n_obs memory tokens of its own
           // sample: few keys, so the products run on the vector ALUs (fp32
