@@ -705,6 +705,11 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
   // LayerNorm gain/shift and output bias of the next unit to evaluate, for
   // this lane's columns (loaded one unit ahead)
   float nlg[CBW], nlb[CBW], nrb[CBW];
+  // Width 256: every prefetch below is issued unconditionally (a merge of
+  // an in-flight load with an older register value costs a wait for the
+  // load at the merge).  Width 768 keeps the conditional form, which its
+  // register allocation favours.
+  constexpr bool UNCOND = D <= 256;
   int loaded_t = -1, loaded_u = -1;  // (step, unit) the prefetched parameters belong to
   const auto load_unit_params = [&](int tt, int unit) {
     loaded_t = tt;
@@ -810,31 +815,42 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
       return v;
     };
     // noise added by this step's update (prefetched)
+    // (unconditional form: loaded from an existing slice; entries of dead
+    // slots and of the last step are never added)
     float zpre[ZPT];
 #pragma unroll
     for (int q = 0; q < ZPT; ++q) {
       const int it = tid + q * NT;
-      zpre[q] = 0.f;
-      if (k > 0 && it < R * A) {
-        const int row = it / A, a = it % A, s = smp[row / HZ];
-        if (s >= 0) zpre[q] = p.noise[(((size_t)(t + 1) * p.batch + s) * HZ + (row % HZ)) * A + a];
+      if constexpr (UNCOND) {
+        const int itc = it < R * A ? it : 0;
+        const int row = itc / A, a = itc % A, s = smp[row / HZ];
+        const int tn = t + 1 < T ? t + 1 : T - 1;
+        zpre[q] = p.noise[(((size_t)tn * p.batch + (s >= 0 ? s : 0)) * HZ + (row % HZ)) * A + a];
+      } else {
+        zpre[q] = 0.f;
+        if (k > 0 && it < R * A) {
+          const int row = it / A, a = it % A, s = smp[row / HZ];
+          if (s >= 0) zpre[q] = p.noise[(((size_t)(t + 1) * p.batch + s) * HZ + (row % HZ)) * A + a];
+        }
       }
     }
-    // parameters of this step's first evaluated unit, unless the previous
-    // step already requested them
-    {
+    // parameters of this step's first evaluated unit (unconditional form:
+    // always, unit 0 if none; else unless the previous step requested them)
+    if constexpr (UNCOND) {
+      load_unit_params(t, evT ? __builtin_ctzll(evT) : 0);
+    } else {
       const int f = evT ? __builtin_ctzll(evT) : U;
       if (f < U && !(loaded_t == t && loaded_u == f)) load_unit_params(t, f);
     }
     // sampler constants and head bias of this step's update (prefetched)
     // (a lane-indexed vector load: a uniform scalar load would be waited for
     // by the next LDS access)
-    const float ddl = lane < 5 ? p.ddpm[(size_t)k * 8 + lane] : 0.f;
+    const float ddl = UNCOND ? p.ddpm[(size_t)k * 8 + (lane & 7)] : (lane < 5 ? p.ddpm[(size_t)k * 8 + lane] : 0.f);
     float bout[ZPT];
 #pragma unroll
     for (int q = 0; q < ZPT; ++q) {
       const int it = tid + q * NT;
-      bout[q] = it < R * A ? raw[p.b_out + it % A] : 0.f;
+      bout[q] = UNCOND ? raw[p.b_out + it % A] : (it < R * A ? raw[p.b_out + it % A] : 0.f);
     }
     // ---- embedding of the current sample on fp32 MFMA: h = (b_in + P_act) + x W_in^T
     {
@@ -905,7 +921,11 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
       // next) now, so that they have the whole unit to arrive
       const auto request_next_params = [&]() {
         const uint64_t later = (e + 1 < 64) ? (evT >> (e + 1)) : 0ull;
-        if (later) load_unit_params(t, e + 1 + __builtin_ctzll(later));
+        if constexpr (UNCOND) {
+          // this unit's own parameters again when no later unit of the
+          // step is evaluated (the next step loads its first)
+          load_unit_params(t, later ? e + 1 + __builtin_ctzll(later) : e);
+        } else if (later) load_unit_params(t, e + 1 + __builtin_ctzll(later));
         else if (t + 1 < T) {
           const int f = first_eval(t + 1);
           if (f < U) load_unit_params(t + 1, f);
