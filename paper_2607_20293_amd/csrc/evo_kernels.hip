@@ -35,6 +35,7 @@ namespace evo {
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
 
 constexpr uint64_t kMergedBit = 1ull << 63;
 constexpr int kMaskEntries = 341;  // (T x samples per tile) entries of 3 x u64 in LDS (8 KiB)
@@ -602,9 +603,11 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
   int nbar = 0;                             // evaluated units exchanged so far
   float* const xb = TEAM > 1 ? p.xchg + (size_t)tile * (3 * TEAM) * (R * D) : nullptr;
   const auto xr = __builtin_amdgcn_make_buffer_rsrc(xb, (short)0, TEAM > 1 ? 3 * TEAM * R * D * 4 : 0, 0x00020000);
-  const auto xoff = [&](int slot, int m, int c, int rb) {
-    return ((slot * TEAM + m) * (R * D) + (((w * RB + rb) * CBW + c) * 64 + lane) * 4) * 4;
-  };
+  // byte offset of this lane's fragment (c, rb) in a member's slot, split
+  // into a per-lane part (VGPR) and a constant part (SGPR), so that a wide
+  // tile does not hold one offset register per fragment
+  const auto xoff = [&](int slot, int m) { return ((slot * TEAM + m) * (R * D) + (w * RB * CBW * 64 + lane) * 4) * 4; };
+  const auto xcst = [](int c, int rb) { return (rb * CBW + c) * 1024; };
   if constexpr (TEAM > 1) {
     // all three slots of this member start empty; one counter barrier makes
     // sure no member reads a slot before its owner has emptied it
@@ -615,7 +618,7 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
       for (int c = 0; c < CBW; ++c)
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb)
-          __builtin_amdgcn_raw_buffer_store_b128(empty, xr, xoff(sl, member, c, rb), 0, kCoherent);
+          __builtin_amdgcn_raw_buffer_store_b128(empty, xr, xoff(sl, member), xcst(c, rb), kCoherent);
     __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
     __syncthreads();
     if (tid == 0) {
@@ -765,13 +768,14 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
           for (int jj = 1; jj < SPT; ++jj)
             if (jrow[rb] == jj) mj = mru_cur[jj];
           const bool use = ub[q] >= 0 && ((mj >> ub[q]) & 1ull);
-          const int off = use ? (ub[q] * (R * D) + (((w * RB + rb) * CBW + c) * 64 + lane) * 4) * CE : 0x7FFFFFF0;
+          const int off = use ? (ub[q] * (R * D) + (w * RB * CBW * 64 + lane) * 4) * CE : 0x7FFFFFF0;
+          const int cst = (rb * CBW + c) * 256 * CE;
           if constexpr (CE == 2) {
-            const auto x = __builtin_amdgcn_raw_buffer_load_b64(crs, off, 0, 0);
+            const auto x = __builtin_amdgcn_raw_buffer_load_b64(crs, off, cst, 0);
             v[q][c][rb] = f32x4{__uint_as_float(x[0] << 16), __uint_as_float(x[0] & 0xFFFF0000u),
                                 __uint_as_float(x[1] << 16), __uint_as_float(x[1] & 0xFFFF0000u)};
           } else {
-            v[q][c][rb] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(crs, off, 0, 0));
+            v[q][c][rb] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(crs, off, cst, 0));
           }
         }
   };
@@ -815,8 +819,9 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
       return v;
     };
     // noise added by this step's update (prefetched)
-    // (unconditional form: loaded from an existing slice; entries of dead
-    // slots and of the last step are never added)
+    // (unconditional form: always loaded from an existing slice; the last
+    // step adds none, and a dead slot's rows, which read sample 0's noise,
+    // are never output)
     float zpre[ZPT];
 #pragma unroll
     for (int q = 0; q < ZPT; ++q) {
@@ -1349,7 +1354,7 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
 #pragma unroll
             for (int q = 0; q < 4; ++q) v[q] = v[q] == kEmpty ? 0x7FC00000u : v[q];
             if (!(p.withhold && member == 0))
-              __builtin_amdgcn_raw_buffer_store_b128(v, xr, xoff(cur, member, c, rb), 0, kCoherent);
+              __builtin_amdgcn_raw_buffer_store_b128(v, xr, xoff(cur, member), xcst(c, rb), kCoherent);
           }
         // bounded wait for every word of `v` (loaded by `load`) to be written;
         // polls back to back (each is a memory round trip), the error flag
@@ -1385,7 +1390,7 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
                    for (int c = 0; c < XC; ++c)
 #pragma unroll
                      for (int rb = 0; rb < RB; ++rb)
-                       v[c][rb] = __builtin_amdgcn_raw_buffer_load_b128(xr, xoff(cur, other, c0 + c, rb), 0, kCoherent);
+                       v[c][rb] = __builtin_amdgcn_raw_buffer_load_b128(xr, xoff(cur, other), xcst(c0 + c, rb), kCoherent);
                  },
                  [&](const u32x4 (&v)[XC][RB]) {
                    bool ok = true;
@@ -1413,7 +1418,7 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
                      for (int c = 0; c < CBW; ++c)
 #pragma unroll
                        for (int rb = 0; rb < RB; ++rb)
-                         v[m][c][rb] = __builtin_amdgcn_raw_buffer_load_b128(xr, xoff(cur, m, c, rb), 0, kCoherent);
+                         v[m][c][rb] = __builtin_amdgcn_raw_buffer_load_b128(xr, xoff(cur, m), xcst(c, rb), kCoherent);
                    }
                },
                [&](const u32x4 (&v)[TEAM][CBW][RB]) {
@@ -1447,7 +1452,7 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
         for (int c = 0; c < CBW; ++c)
 #pragma unroll
           for (int rb = 0; rb < RB; ++rb)
-            __builtin_amdgcn_raw_buffer_store_b128(empty, xr, xoff(prev, member, c, rb), 0, kCoherent);
+            __builtin_amdgcn_raw_buffer_store_b128(empty, xr, xoff(prev, member), xcst(c, rb), kCoherent);
         ++nbar;
       }
 #pragma unroll
@@ -1455,6 +1460,29 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb) r[c][rb] += rbias[c];
 
+      // Layer sums kept in memory (tiles too wide for registers): the
+      // unit's partial layer sums are read in one batch through the cache's
+      // buffer resource before any is written (element by element, every
+      // load would wait for the store before it); an entry that is not
+      // needed reads past the end of the resource (zeros, no memory access)
+      const int lacc_base = CE == 4 ? (int)(cidx(3 * l + 2, 0, 0) * 4) : (int)((size_t)(3 * l) * (R * D) * 2 + cidx(0, 0, 0) * 4);
+      const auto lacc_cst = [](int c, int rb) { return (rb * CBW + c) * 1024; };
+      f32x4 lsum[MAC_REG ? 1 : CBW][MAC_REG ? 1 : RB];
+      if constexpr (!MAC_REG) {
+#pragma unroll
+        for (int c = 0; c < CBW; ++c)
+#pragma unroll
+          for (int rb = 0; rb < RB; ++rb) {
+            const int j = jrow[rb];
+            bool mg = mmg[0];
+#pragma unroll
+            for (int jj = 1; jj < SPT; ++jj)
+              if (j == jj) mg = mmg[jj];
+            const bool need = u > 0 && mg && ((pick(mev, j) >> e) & 1ull);
+            lsum[c][rb] = __builtin_bit_cast(
+                f32x4, __builtin_amdgcn_raw_buffer_load_b128(crs, need ? lacc_base : 0x7FFFFFF0, lacc_cst(c, rb), 0));
+          }
+      }
       // Eq. 1 per sample at unit e: evaluated residual (and cache refresh) or
       // the residual cached at the unit's most recent refresh.
 #pragma unroll
@@ -1478,12 +1506,16 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
               // which a merged layer leaves unused (bf16 caches; one sample
               // per tile, so no other sample's rows share them); the sum of
               // the three residuals is stored at the FFN position
-              f32x4* acc = CE == 4 ? reinterpret_cast<f32x4*>(cbase + cidx(3 * l + 2, c, rb) * 4)
-                                   : reinterpret_cast<f32x4*>(cbase + (size_t)(3 * l) * (R * D) * 2 +
-                                                              (cidx(0, c, rb)) * 4);
-              const f32x4 sum = (u == 0) ? v : *acc + v;
-              if (CE == 4 || u < 2) *acc = sum;
-              else if (pick(mst, j) & bit) cstore(e, c, rb, sum);
+              const f32x4 sum = (u == 0) ? v : lsum[c][rb] + v;
+              if (CE == 4 || u < 2) {
+                __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, sum), crs, lacc_base, lacc_cst(c, rb), 0);
+              } else if (pick(mst, j) & bit) {
+                if constexpr (CE == 2)
+                  __builtin_amdgcn_raw_buffer_store_b64(u32x2{bf16x2_rne(sum[0], sum[1]), bf16x2_rne(sum[2], sum[3])}, crs,
+                                                        (int)(cidx(e, 0, 0) * 2), (rb * CBW + c) * 512, 0);
+                else
+                  cstore(e, c, rb, sum);
+              }
             } else if (pick(mst, j) & bit) {
               cstore(e, c, rb, v);
             }
