@@ -205,10 +205,8 @@ size_t evo_noalloc_scratch_bytes(void);
  * evo_create_policy: EVO_TEAM=0 disables that variant, EVO_TEAM=<n> keeps
  * only teams of n workgroups (of those compiled); EVO_TEAM_SPIN_LIMIT
  * sets the number of polls before a wait gives up (default 2^20, about a
- * second; checked every 32 polls, so smaller values act as 32);
- * EVO_TEAM_TEST_WITHHOLD=1 is a test hook that makes team member 0
- * withhold its partial residuals, so that the other members' waits time out
- * and this error path can be exercised (outputs are then invalid). */
+ * second; checked every 32 polls, so smaller values act as 32).  The test
+ * hook evo_debug_team_withhold forces this error path from the host. */
 int evo_synchronize(evo_policy* p);
 
 /* ---- Redundancy-aware initialisation of the schedule search (Sec. 3.3,
@@ -419,6 +417,13 @@ int evo_schedule_stats(const evo_policy_desc* desc, const uint8_t* lattices, int
  * bit 2: add the cached residual; bit 3: layer-merged cache.  For tests. */
 int evo_schedule_codes(const evo_policy_desc* desc, const uint8_t* lattice, int32_t rows,
                        int32_t granularity, uint8_t* out);
+
+/* Test hook: enable != 0 makes team member 0 of later evo_denoise calls
+ * withhold its partial residuals, so that the other members' bounded waits
+ * time out and the error path of evo_synchronize can be exercised (the
+ * outputs of those calls are invalid); 0 restores normal calls.  Errors:
+ * EVO_E_INVALID for a NULL policy. */
+int evo_debug_team_withhold(evo_policy* p, int32_t enable);
 
 /* Test hook: synchronise the policy's device and copy the cached residual
  * of `unit` for `sample` of the last evo_denoise into host float[H][d]

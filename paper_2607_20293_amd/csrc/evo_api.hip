@@ -115,7 +115,7 @@ struct evo_policy {
   };
   std::vector<TeamCfg> teams;
   unsigned team_spin_limit = 1u << 20;  // EVO_TEAM_SPIN_LIMIT
-  int team_withhold = 0;                // EVO_TEAM_TEST_WITHHOLD (test hook)
+  int team_withhold = 0;                // evo_debug_team_withhold (test hook)
   float* d_xchg = nullptr;
   unsigned* d_tctr = nullptr;
   unsigned* d_derr = nullptr;
@@ -389,7 +389,6 @@ int evo_create_policy(const evo_policy_desc* desc, const float* host_weights, si
       const int team_only = env ? std::atoi(env) : -1;
       if (const char* e = std::getenv("EVO_TEAM_SPIN_LIMIT"))
         p->team_spin_limit = (unsigned)std::min(std::strtoul(e, nullptr, 10), 1ul << 28);
-      if (const char* e = std::getenv("EVO_TEAM_TEST_WITHHOLD")) p->team_withhold = e[0] == '1';
       int sizes[4];
       int nsz = kernel_team_sizes(KernelKey{s.d, s.dh(), s.H, s.dff, s.dtype, 1, 0}, sizes);
       if (team_only >= 0) {
@@ -892,6 +891,13 @@ int evo_schedule_codes(const evo_policy_desc* desc, const uint8_t* lattice, int3
     std::memcpy(out, sc.codes.data(), sc.codes.size());
     return EVO_OK;
   });
+}
+
+int evo_debug_team_withhold(evo_policy* p, int32_t enable) {
+  clear_error();
+  if (!p) return fail(EVO_E_INVALID, "policy is NULL");
+  p->team_withhold = enable != 0;
+  return (int)EVO_OK;
 }
 
 int evo_debug_read_cache(evo_policy* p, int32_t unit, int32_t sample, float* host_dst) {

@@ -23,7 +23,7 @@ CODE_EVAL, CODE_STORE, CODE_REUSE, CODE_MERGED = 1, 2, 4, 8
 
 EXPORTED = ("evo_weight_count", "evo_check_desc", "evo_create_policy", "evo_set_schedule",
             "evo_set_schedule_pairs", "evo_denoise", "evo_get_stats", "evo_schedule_stats",
-            "evo_schedule_codes", "evo_debug_read_cache", "evo_synchronize", "evo_destroy_policy",
+            "evo_schedule_codes", "evo_debug_read_cache", "evo_debug_team_withhold", "evo_synchronize", "evo_destroy_policy",
             "evo_last_error", "evo_collect_activations", "evo_redundancy_scores", "evo_guided_probabilities",
             "evo_guided_sample", "evo_ga_initial_population", "evo_ga_next_generation", "evo_ga_search",
             "evo_search", "evo_encoder_weight_count", "evo_create_encoder", "evo_encode", "evo_encoder_flops",
@@ -222,6 +222,8 @@ def lib() -> ctypes.CDLL:
         L.evo_schedule_codes.restype = ctypes.c_int
         L.evo_debug_read_cache.argtypes = [P, I32, I32, P]
         L.evo_debug_read_cache.restype = ctypes.c_int
+        L.evo_debug_team_withhold.argtypes = [P, I32]
+        L.evo_debug_team_withhold.restype = ctypes.c_int
         L.evo_collect_activations.argtypes = [P, I32, P, P, P, P, P, P]
         L.evo_collect_activations.restype = ctypes.c_int
         L.evo_redundancy_scores.argtypes = [P, I32, P, P, P]
@@ -483,6 +485,11 @@ class Policy:
         st = Stats()
         _check(lib().evo_get_stats(self._h, ctypes.byref(st)))
         return st.as_dict()
+
+    def debug_team_withhold(self, enable: bool) -> None:
+        """Test hook: team member 0 of later calls withholds its partials
+        (their waits time out; outputs invalid)."""
+        _check(lib().evo_debug_team_withhold(self._h, 1 if enable else 0))
 
     def read_cache(self, unit: int, sample: int) -> np.ndarray:
         buf = np.zeros((self.shape.horizon, self.shape.d_model), np.float32)

@@ -158,8 +158,8 @@ def test_team_wait_timeout_is_reported(size):
     obs, noise = I.make_obs(s, 1, 7), I.make_noise(s, 1, 7)
     lat = I.lattice_bernoulli(3 * s.n_layers, s.n_steps, 0.2, np.random.default_rng(7))
     say(f"[gpu] team of {size}: wait timeout, forced from the host")
-    pol = _policy(s, wts, "bf16", 1, 1, env={"EVO_TEAM_TEST_WITHHOLD": "1", "EVO_TEAM_SPIN_LIMIT": "64",
-                                             "EVO_TEAM": str(size)})
+    pol = _policy(s, wts, "bf16", 1, 1, env={"EVO_TEAM_SPIN_LIMIT": "64", "EVO_TEAM": str(size)})
+    pol.debug_team_withhold(True)
     pol.set_schedule(0, lat, O.GRAN_UNIT)
     dev = device()
     pol.denoise(torch.from_numpy(obs).to(dev), torch.from_numpy(noise).to(dev), None)
