@@ -217,9 +217,10 @@ def test_image_b256_every_sample():
 
 
 @pytest.mark.parametrize("name", ["bimanual_bf16_b128_d20", "bimanual_bf16_b128_all"])
-def test_bimanual_b128_spread_samples(name):
-    """32 (20% lattice) and 16 (all-refresh) samples spread over the batch:
-    every XCD's tile range and every residue of the sample index mod 8."""
+def test_bimanual_b128_samples(name):
+    """Every sample of the 20% lattice; 32 all-refresh samples spread over
+    the batch (every XCD's tile range, every residue of the sample index
+    mod 8)."""
     _case_stored(name)
 
 
