@@ -13,11 +13,14 @@
 // workgroups into partial outputs that the GroupNorm statistics pass sums
 // in a fixed order.
 //
-// GroupNorm is two passes per layer: partial statistics over pixel chunks
-// (shifted sums, fp64 across threads and chunks), then an apply pass that
-// adds the residual and ReLU and, where the network pools next, does the
-// pooling itself: 3x3/2 max pooling after the stem, global average pooling
-// after the last block (the last block's output is never stored).
+// GroupNorm statistics are shifted sums (x - x0, x0 the group's first
+// element), fp32 per thread and fp64 across threads.  Where there are many
+// (image, channel chunk) workgroups or the map is small, one kernel per
+// GroupNorm takes an image's groups whole (statistics, then apply);
+// otherwise two passes: partial statistics over pixel chunks, then apply.
+// The apply adds the residual and ReLU and, where the network pools next,
+// does the pooling itself: 3x3/2 max pooling after the stem, global average
+// pooling after the last block (the last block's output is never stored).
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -50,6 +53,17 @@ constexpr long long kWsFloats = 1024ll * 4096;  // split-K partials (>= splits *
 // chunking follows the call's batch.  (Fixed chunks of 64 or 128 pixels
 // measured 3-8% slower.)
 constexpr int kGnTarget = 1024;
+// One GroupNorm kernel instead of two for maps of at most kFusedPixels
+// pixels, and for maps of at most kFusedPixelsWide pixels where the
+// max_batch plan has at least kFusedWG (image, channel chunk) workgroups;
+// with fewer workgroups than kFusedWG it takes one group per workgroup.
+// (Measured on 84x84 frames: 2 frames 0.290 -> 0.279 ms; one kernel for
+// every map at 2 frames 0.50 ms; at 512 frames the stem's 1764-pixel maps
+// took 165 us in one kernel against 126 us in two, the 441-pixel maps 10%
+// less in one.)
+constexpr int kFusedWG = 256;
+constexpr int kFusedPixels = 128;
+constexpr int kFusedPixelsWide = 1024;
 
 template <class AT> struct ConvStep;
 template <> struct ConvStep<__bf16> {
@@ -493,6 +507,144 @@ __global__ void __launch_bounds__(kThreads) gn_apply_kernel(const GnArgs a) {
   }
 }
 
+// One kernel per GroupNorm: workgroup (image n, channel chunk of gpw
+// groups) computes the statistics of its groups over the whole image, then
+// applies them (the apply reads what the first sweep just touched, mostly
+// from L2).  Thread t reads float4 column t % Q of pixel rows t / Q + i *
+// RP, as the two-pass kernels do.
+__global__ void __launch_bounds__(kThreads) gn_fused_kernel(const GnArgs a) {
+  const int HW = a.H * a.W, CW = a.G * a.gpw, Q = CW >> 2, RP = kThreads / Q;
+  const int chunks = a.C / CW;
+  const int ch = blockIdx.x % chunks, n = blockIdx.x / chunks;
+  const int tid = threadIdx.x, col = tid % Q, prow = tid / Q;
+  const int c = ch * CW + col * 4, j = (col * 4) / a.G;
+  const size_t base = (size_t)n * HW * a.C;
+  const bool split = a.splits > 1;
+  __shared__ float sx0[16];
+  __shared__ float2 st[16];
+  __shared__ double sd[kThreads], qd[kThreads];
+  // the conv output at i: the sum of the split partials in split order (all
+  // requested before the first is added), or x itself
+  const auto value = [&](size_t i) -> f32x4 {
+    if (!split) return *reinterpret_cast<const f32x4*>(a.x + i);
+    f32x4 t[kMaxSplit];
+#pragma unroll
+    for (int z = 0; z < kMaxSplit; ++z)
+      t[z] = z < a.splits ? *reinterpret_cast<const f32x4*>(a.ws + (long long)z * a.split_stride + i)
+                          : f32x4{0.f, 0.f, 0.f, 0.f};
+    f32x4 v = t[0];
+#pragma unroll
+    for (int z = 1; z < kMaxSplit; ++z)
+      if (z < a.splits) v += t[z];
+    return v;
+  };
+  // shift: the group's first element (pixel 0, first channel of the group;
+  // a multiple of four channels, so the float4 load is aligned)
+  const float x0 = value(base + ch * CW + j * a.G)[0];
+  float s = 0.f, q = 0.f;
+  const auto add = [&](f32x4 v, size_t i) {
+    if (split) *reinterpret_cast<f32x4*>(a.x + i) = v;
+    const f32x4 d = v - x0;
+    s += (d[0] + d[1]) + (d[2] + d[3]);
+    q += (d[0] * d[0] + d[1] * d[1]) + (d[2] * d[2] + d[3] * d[3]);
+  };
+  {
+    constexpr int U = 4;  // pixel rows requested together
+    int p = prow;
+    for (; p + (U - 1) * RP < HW; p += U * RP) {
+      f32x4 v[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) v[u] = value(base + (size_t)(p + u * RP) * a.C + c);
+#pragma unroll
+      for (int u = 0; u < U; ++u) add(v[u], base + (size_t)(p + u * RP) * a.C + c);
+    }
+    for (; p < HW; p += RP) add(value(base + (size_t)p * a.C + c), base + (size_t)p * a.C + c);
+  }
+  sd[tid] = s;
+  qd[tid] = q;
+  if (prow == 0 && col * 4 % a.G == 0) sx0[j] = x0;
+  __syncthreads();
+  for (int h = RP >> 1; h > 0; h >>= 1) {
+    if (prow < h) {
+      sd[tid] += sd[tid + h * Q];
+      qd[tid] += qd[tid + h * Q];
+    }
+    __syncthreads();
+  }
+  if (tid < a.gpw) {
+    const int cols = a.G >> 2;
+    double S = 0.0, Qs = 0.0;
+    for (int k = 0; k < cols; ++k) {
+      S += sd[tid * cols + k];
+      Qs += qd[tid * cols + k];
+    }
+    const double cnt = (double)HW * a.G, m = S / cnt;
+    const double var = std::max(Qs / cnt - m * m, 0.0);
+    st[tid] = make_float2((float)((double)sx0[tid] + m), (float)(1.0 / std::sqrt(var + (double)a.eps)));
+  }
+  __syncthreads();  // also orders the split sums stored above before the reads below
+  const float2 ms = st[j];
+  const f32x4 gm = *reinterpret_cast<const f32x4*>(a.gamma + c);
+  const f32x4 bt = *reinterpret_cast<const f32x4*>(a.beta + c);
+  auto f = [&](f32x4 v, size_t i) -> f32x4 {
+    f32x4 r;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) r[k] = (v[k] - ms.x) * ms.y * gm[k] + bt[k];
+    if (a.res) r += *reinterpret_cast<const f32x4*>(a.res + i);
+    if (a.relu) {
+#pragma unroll
+      for (int k = 0; k < 4; ++k) r[k] = fmaxf(r[k], 0.f);
+    }
+    return r;
+  };
+  if (a.mode == GN_PLAIN) {
+    for (int p = prow; p < HW; p += RP) {
+      const size_t i = base + (size_t)p * a.C + c;
+      *reinterpret_cast<f32x4*>(a.y + i) = f(*reinterpret_cast<const f32x4*>(a.x + i), i);
+    }
+  } else if (a.mode == GN_MAXPOOL) {
+    const int HWp = a.Hp * a.Wp;
+    for (int p = prow; p < HWp; p += RP) {
+      const int oh = p / a.Wp, ow = p - oh * a.Wp;
+      f32x4 m = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+      for (int u = 0; u < 3; ++u) {
+        const int ih = oh * 2 - 1 + u;
+        if (ih < 0 || ih >= a.H) continue;
+        for (int v = 0; v < 3; ++v) {
+          const int iw = ow * 2 - 1 + v;
+          if (iw < 0 || iw >= a.W) continue;
+          const size_t i = base + ((size_t)ih * a.W + iw) * a.C + c;
+          const f32x4 r = f(*reinterpret_cast<const f32x4*>(a.x + i), i);
+#pragma unroll
+          for (int k = 0; k < 4; ++k) m[k] = fmaxf(m[k], r[k]);
+        }
+      }
+      *reinterpret_cast<f32x4*>(a.y + (size_t)n * HWp * a.C + (size_t)p * a.C + c) = m;
+    }
+  } else {
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int p = prow; p < HW; p += RP) {
+      const size_t i = base + (size_t)p * a.C + c;
+      acc += f(*reinterpret_cast<const f32x4*>(a.x + i), i);
+    }
+    __shared__ f32x4 red[kThreads];
+    red[tid] = acc;
+    __syncthreads();
+    for (int h = RP >> 1; h > 0; h >>= 1) {
+      if (prow < h) red[tid] += red[tid + h * Q];
+      __syncthreads();
+    }
+    if (prow == 0) {
+      const f32x4 m = red[tid] / (float)HW;
+      float* o = a.y + (size_t)n * a.out_stride + c;
+      o[0] = m[0];
+      o[1] = m[1];
+      o[2] = m[2];
+      o[3] = m[3];
+    }
+  }
+}
+
 // weights [Cout][K] fp32 -> [Cout][Kp] operand type, zero padded
 __global__ void pack_conv_kernel(const float* __restrict__ w, int Cout, int K, int Kp, int bf, void* dst) {
   const long long total = (long long)Cout * Kp;
@@ -640,13 +792,27 @@ hipError_t launch_conv(const evo_encoder* e, const ConvLayer& L, const float* x,
   return hipGetLastError();
 }
 
+// One GroupNorm pass (gn_fused_kernel) or two (statistics over pixel
+// chunks, then apply).  Chosen from the encoder's max_batch and the map
+// size, never from a call's batch, so an image's statistics are summed in
+// the same order at every batch size.
+bool fused_gn(const evo_encoder* e, int HW, int chunks) {
+  return HW <= kFusedPixels || ((long long)e->desc.max_batch * chunks >= kFusedWG && HW <= kFusedPixelsWide);
+}
+
 // GroupNorm of layer L's conv output (g.ws / splits / x set by launch_conv).
 hipError_t launch_gn(const evo_encoder* e, const ConvLayer& L, GnArgs g, int N, int H, int W, const float* res,
                      int relu, int mode, float* y, int out_stride, hipStream_t st) {
   const int C = L.cout, G = e->desc.gn_group, groups = C / G;
   int gpw = 1;  // groups per workgroup: up to 64 channels, a power of two dividing the group count
   while (gpw * 2 * G <= 64 && groups % (gpw * 2) == 0) gpw *= 2;
-  const int chunks = groups / gpw, HW = H * W;
+  int chunks = groups / gpw;
+  const int HW = H * W;
+  const bool fused = fused_gn(e, HW, chunks);
+  if (fused && (long long)e->desc.max_batch * chunks < kFusedWG) {
+    gpw = 1;  // few images: one group per workgroup, for more workgroups
+    chunks = groups;
+  }
   const int base = N * chunks;
   // statistics chunks of the max_batch plan (see kGnTarget)
   const int ps = std::max(1, std::min(cdiv(kGnTarget, e->desc.max_batch * chunks), cdiv(HW, 16)));
@@ -671,8 +837,12 @@ hipError_t launch_gn(const evo_encoder* e, const ConvLayer& L, GnArgs g, int N, 
   g.eps = 1e-5f;
   const int out_px = mode == GN_MAXPOOL ? g.Hp * g.Wp : HW;
   g.ps_apply = mode == GN_AVGPOOL ? 1 : std::max(1, std::min(cdiv(kGnTarget, base), cdiv(out_px, 16)));
-  hipLaunchKernelGGL(gn_stats_kernel, dim3((unsigned)(base * ps)), dim3(kThreads), 0, st, g);
-  hipLaunchKernelGGL(gn_apply_kernel, dim3((unsigned)(base * g.ps_apply)), dim3(kThreads), 0, st, g);
+  if (fused) {
+    hipLaunchKernelGGL(gn_fused_kernel, dim3((unsigned)base), dim3(kThreads), 0, st, g);
+  } else {
+    hipLaunchKernelGGL(gn_stats_kernel, dim3((unsigned)(base * ps)), dim3(kThreads), 0, st, g);
+    hipLaunchKernelGGL(gn_apply_kernel, dim3((unsigned)(base * g.ps_apply)), dim3(kThreads), 0, st, g);
+  }
   return hipGetLastError();
 }
 
