@@ -8,7 +8,11 @@
 // padded to the K step).  The A tile is gathered from the input with the
 // convolution's padding on the fly (no im2col buffer), converted to the
 // operand type and double-buffered in LDS with the next step's global loads
-// in flight during the current step's MFMAs, in 64 x 64 output tiles.
+// in flight during the current step's MFMAs, in 64 x 64 output tiles.  The
+// gather keeps its K position (kernel tap and channel) from step to step
+// instead of dividing, and every lane loads: positions outside the input
+// (padding, rows beyond the output, K beyond the kernel) read a small block
+// of zero bytes, so no branch surrounds the loads.
 // Layers with few output tiles (small batches, late stages) split K over
 // workgroups into partial outputs that the GroupNorm statistics pass sums
 // in a fixed order.
@@ -77,6 +81,7 @@ struct ConvArgs {
   const float* x;    // [N][H][W][Cin]
   const void* w;     // [Cout][Kp] operand type
   float* y;          // [N][Ho][Wo][Cout], or split z at y + z * split_stride
+  const float* zeros;  // 64 zero bytes (16-byte aligned): the source of loads outside the input
   int H, W, Cin, Ho, Wo, Cout, kw, stride, pad, K, Kp;
   int M, mt, nt, splits, spp;  // pixels, tile counts, K splits, K steps per split
   long long split_stride;
@@ -114,8 +119,11 @@ __global__ void __launch_bounds__(kThreads) conv_kernel(const ConvArgs a) {
   // the A rows this thread stages: output pixel -> image base and window origin
   // (rlo, rhi: the part of a kernel row of kw * Cin contiguous K elements
   // that falls inside the image horizontally)
+  // (wo0: element offset of the window origin within the image, negative
+  // where the window starts in the padding; an image has fewer than 2^31
+  // elements, checked at creation)
   const float* xb[PA];
-  int ih0[PA], iw0[PA], rlo[PA], rhi[PA];
+  int ih0[PA], iw0[PA], wo0[PA], rlo[PA], rhi[PA];
   bool pv[PA];
 #pragma unroll
   for (int p = 0; p < PA; ++p) {
@@ -128,9 +136,12 @@ __global__ void __launch_bounds__(kThreads) conv_kernel(const ConvArgs a) {
     xb[p] = a.x + (size_t)pn * a.H * a.W * a.Cin;
     ih0[p] = oh * a.stride - a.pad;
     iw0[p] = ow * a.stride - a.pad;
+    wo0[p] = (ih0[p] * a.W + iw0[p]) * a.Cin;
     rlo[p] = max(0, -iw0[p]) * a.Cin;
     rhi[p] = min(a.kw, a.W - iw0[p]) * a.Cin;
   }
+  // weight rows beyond Cout read the zero bytes (their B step is SEG
+  // operands, at most 64 bytes)
   const AT* wb[PB];
   bool bv[PB];
 #pragma unroll
@@ -147,42 +158,72 @@ __global__ void __launch_bounds__(kThreads) conv_kernel(const ConvArgs a) {
     uint4 b[PB][BV];
   };
 
+  // the K position of this thread's chunk, advanced by KS per step (loads
+  // are requested for consecutive steps): vec: tap (ka, kb) and channel c;
+  // otherwise kernel row ka0 and offset r0 within it
+  int kc = 0, kka = 0, kkb = 0;
+  const int rowlen = a.kw * a.Cin;
+  {
+    const int kk0 = s_begin * KS + chunk * SEG;
+    if (vec) {
+      const int pix = kk0 / a.Cin;
+      kc = kk0 - pix * a.Cin;
+      kka = pix / a.kw;
+      kkb = pix - kka * a.kw;
+    } else {
+      kka = kk0 / rowlen;
+      kc = kk0 - kka * rowlen;
+    }
+  }
+  const auto advance = [&]() {
+    kc += KS;
+    if (vec) {
+      while (kc >= a.Cin) {
+        kc -= a.Cin;
+        if (++kkb == a.kw) {
+          kkb = 0;
+          ++kka;
+        }
+      }
+    } else {
+      while (kc >= rowlen) {
+        kc -= rowlen;
+        ++kka;
+      }
+    }
+  };
   auto load = [&](Regs& rg, int s) {
     const int kk = s * KS + chunk * SEG;
     if (vec) {
-      const int c = kk % a.Cin, pix = kk / a.Cin, ka = pix / a.kw, kb = pix - ka * a.kw;
+      // every lane loads: from the input inside the image, from the zero
+      // bytes outside it (no branch around the loads)
+      const int ka = kka, kb = kkb, toff = (ka * a.W + kb) * a.Cin + kc;
 #pragma unroll
       for (int p = 0; p < PA; ++p) {
         const int ih = ih0[p] + ka, iw = iw0[p] + kb;
-        if (pv[p] && kk < a.K && ih >= 0 && ih < a.H && iw >= 0 && iw < a.W) {
-          const f32x4* src = reinterpret_cast<const f32x4*>(xb[p] + ((size_t)ih * a.W + iw) * a.Cin + c);
+        const bool in = pv[p] && kk < a.K && ih >= 0 && ih < a.H && iw >= 0 && iw < a.W;
+        const f32x4* src = reinterpret_cast<const f32x4*>(in ? xb[p] + (wo0[p] + toff) : a.zeros);
 #pragma unroll
-          for (int q = 0; q < SEG / 4; ++q) {
-            const f32x4 t = src[q];
-            rg.a[p][4 * q] = t[0];
-            rg.a[p][4 * q + 1] = t[1];
-            rg.a[p][4 * q + 2] = t[2];
-            rg.a[p][4 * q + 3] = t[3];
-          }
-        } else {
-#pragma unroll
-          for (int q = 0; q < SEG; ++q) rg.a[p][q] = 0.f;
+        for (int q = 0; q < SEG / 4; ++q) {
+          const f32x4 t = src[q];
+          rg.a[p][4 * q] = t[0];
+          rg.a[p][4 * q + 1] = t[1];
+          rg.a[p][4 * q + 2] = t[2];
+          rg.a[p][4 * q + 3] = t[3];
         }
       }
     } else {
       // walk the chunk along kernel rows: K element (ka, r) sits at input
       // row ih0 + ka, offset iw0 * Cin + r of that row
-      const int rowlen = a.kw * a.Cin, ka0 = kk / rowlen, r0 = kk - ka0 * rowlen;
+      const int ka0 = kka, r0 = kc;
 #pragma unroll
       for (int p = 0; p < PA; ++p) {
         int ka = ka0, r = r0;
 #pragma unroll
         for (int q = 0; q < SEG; ++q) {
           const int ih = ih0[p] + ka;
-          float v = 0.f;
-          if (pv[p] && kk + q < a.K && ih >= 0 && ih < a.H && r >= rlo[p] && r < rhi[p])
-            v = xb[p][((long long)ih * a.W + iw0[p]) * a.Cin + r];
-          rg.a[p][q] = v;
+          const bool in = pv[p] && kk + q < a.K && ih >= 0 && ih < a.H && r >= rlo[p] && r < rhi[p];
+          rg.a[p][q] = *(in ? xb[p] + ((ih * a.W + iw0[p]) * a.Cin + r) : a.zeros);
           if (++r == rowlen) {
             r = 0;
             ++ka;
@@ -192,10 +233,12 @@ __global__ void __launch_bounds__(kThreads) conv_kernel(const ConvArgs a) {
     }
 #pragma unroll
     for (int p = 0; p < PB; ++p) {
-      const uint4* src = reinterpret_cast<const uint4*>(wb[p] + (size_t)s * KS);
+      const uint4* src = bv[p] ? reinterpret_cast<const uint4*>(wb[p] + (size_t)s * KS)
+                               : reinterpret_cast<const uint4*>(a.zeros);
 #pragma unroll
-      for (int q = 0; q < BV; ++q) rg.b[p][q] = bv[p] ? src[q] : uint4{0u, 0u, 0u, 0u};
+      for (int q = 0; q < BV; ++q) rg.b[p][q] = src[q];
     }
+    advance();
   };
   auto store = [&](const Regs& rg, int buf) {
 #pragma unroll
@@ -675,6 +718,7 @@ struct evo_encoder {
   std::vector<ConvLayer> convs;  // stem, then per block a, b[, d]
   float* buf[4] = {nullptr, nullptr, nullptr, nullptr};
   size_t buf_floats = 0;
+  float* zeros = nullptr;        // 256 zero bytes: the convolutions' loads outside their inputs
   float* ws = nullptr;           // split-K partials, kWsFloats
   double2* part = nullptr;       // GroupNorm partial statistics
   size_t part_cap = 0;
@@ -782,6 +826,7 @@ hipError_t launch_conv(const evo_encoder* e, const ConvLayer& L, const float* x,
   // splits * tiles * 64 * 64 bounds the partials, below the workspace by construction
   if (pl.splits > 1 && (long long)pl.splits * a.split_stride > kWsFloats) return hipErrorInvalidValue;
   a.y = pl.splits > 1 ? e->ws : y;
+  a.zeros = e->zeros;
   gn->ws = e->ws;
   gn->splits = pl.splits;
   gn->split_stride = a.split_stride;
@@ -934,6 +979,8 @@ int evo_create_encoder(const evo_encoder_desc* desc, const float* host_weights, 
     }
     for (int i = 0; i < 4; ++i) ENC_TRY(hipMalloc(&e->buf[i], e->buf_floats * sizeof(float)));
     ENC_TRY(hipMalloc(&e->ws, (size_t)kWsFloats * sizeof(float)));
+    ENC_TRY(hipMalloc(&e->zeros, 256));
+    ENC_TRY(hipMemset(e->zeros, 0, 256));
     ENC_TRY(hipMalloc(&e->part, e->part_cap * sizeof(double2)));
     ENC_TRY(hipMalloc(&e->shift, e->shift_cap * sizeof(float)));
     ENC_TRY(hipEventCreateWithFlags(&e->ev_done, hipEventDisableTiming));
@@ -1028,6 +1075,7 @@ void evo_destroy_encoder(evo_encoder* e) {
   for (ConvLayer& L : e->convs) (void)hipFree(L.w);
   for (int i = 0; i < 4; ++i) (void)hipFree(e->buf[i]);
   (void)hipFree(e->ws);
+  (void)hipFree(e->zeros);
   (void)hipFree(e->part);
   (void)hipFree(e->shift);
   (void)hipFree(e->d_raw);
