@@ -231,3 +231,28 @@ def test_image_policy_query_matches_oracle_chain():
     ref, _ = O.denoise(s, I.split_weights(s, pw), obs_ref, noise, lats, ids, granularity=O.GRAN_LAYER,
                        cold_policy=O.COLD_COMPUTE, clip=True, dtype="bf16")
     compare(got, ref, "bf16", "image policy query bf16")
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_encoder_bench_batch_sampled_frames(dtype):
+    """The benchmark's encode: 512 frames of 84x84 (the image policy's 256
+    chunks x 2 observation steps) on an encoder planned for 512 frames, which
+    runs the stem's GroupNorm in two passes and every other GroupNorm as one
+    kernel over several groups per workgroup; frames spread over the batch
+    against the oracle on those frames alone."""
+    torch = _torch()
+    from paper_2607_20293_amd import evo
+    e = I.ENC_ROBOMIMIC
+    B, pick = 512, [0, 200, 511]
+    w = I.make_encoder_weights(e, 33, "perturbed")
+    imgs = I.make_images(e, B, 33)
+    enc = evo.Encoder(e, w, dtype, max_batch=B)
+    got = enc.encode(torch.from_numpy(imgs).cuda()).cpu().numpy().astype(np.float64)[pick]
+    enc.close()
+    want = E.encode(e, I.split_encoder_weights(e, w), imgs[pick], dtype)
+    if dtype == "fp32":
+        print("bench batch fp32 max-abs", np.max(np.abs(got - want)))
+        assert np.max(np.abs(got - want)) <= 1e-4
+    else:
+        print("bench batch bf16 rel", _rel(got, want))
+        assert _rel(got, want) <= 3e-2
