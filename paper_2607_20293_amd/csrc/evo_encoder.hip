@@ -196,12 +196,13 @@ __global__ void __launch_bounds__(kThreads) conv_kernel(const ConvArgs a) {
     const int kk = s * KS + chunk * SEG;
     if (vec) {
       // every lane loads: from the input inside the image, from the zero
-      // bytes outside it (no branch around the loads)
+      // bytes outside it (no branch around the loads; the tests are combined
+      // with & so that they compile to compares and selects)
       const int ka = kka, kb = kkb, toff = (ka * a.W + kb) * a.Cin + kc;
 #pragma unroll
       for (int p = 0; p < PA; ++p) {
         const int ih = ih0[p] + ka, iw = iw0[p] + kb;
-        const bool in = pv[p] && kk < a.K && ih >= 0 && ih < a.H && iw >= 0 && iw < a.W;
+        const bool in = pv[p] & (kk < a.K) & (ih >= 0) & (ih < a.H) & (iw >= 0) & (iw < a.W);
         const f32x4* src = reinterpret_cast<const f32x4*>(in ? xb[p] + (wo0[p] + toff) : a.zeros);
 #pragma unroll
         for (int q = 0; q < SEG / 4; ++q) {
@@ -222,7 +223,7 @@ __global__ void __launch_bounds__(kThreads) conv_kernel(const ConvArgs a) {
 #pragma unroll
         for (int q = 0; q < SEG; ++q) {
           const int ih = ih0[p] + ka;
-          const bool in = pv[p] && kk + q < a.K && ih >= 0 && ih < a.H && r >= rlo[p] && r < rhi[p];
+          const bool in = pv[p] & (kk + q < a.K) & (ih >= 0) & (ih < a.H) & (r >= rlo[p]) & (r < rhi[p]);
           rg.a[p][q] = *(in ? xb[p] + ((ih * a.W + iw0[p]) * a.Cin + r) : a.zeros);
           if (++r == rowlen) {
             r = 0;
