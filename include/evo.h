@@ -188,8 +188,14 @@ int evo_denoise(evo_policy* p, int32_t batch, const float* obs_cond, const float
  * contents (each call clears what must start at zero): calls that overlap
  * on one device race (different policies, or different threads); calls of
  * one policy on different streams are ordered as for evo_denoise.
- * evo_debug_read_cache refers to evo_denoise calls only (EVO_E_STATE after
- * this call). */
+ * Enqueued on a stream that is being captured into a HIP graph, the call is
+ * recorded (kernels, a fill kernel for the counters, and the copy of the
+ * plan from the policy's pinned staging buffer); each replay reads the plan
+ * that buffer holds when it runs, so replays stay valid while the policy's
+ * calls after the capture use the same batch and schedule ids (they stage
+ * the same bytes), and a replay is a call on the device's array like any
+ * other.  evo_debug_read_cache refers to evo_denoise calls only
+ * (EVO_E_STATE after this call). */
 int evo_denoise_noalloc(evo_policy* p, int32_t batch, const float* obs_cond, const float* noise,
                         const int32_t* schedule_ids, float* actions_out, void* hip_stream);
 

@@ -1,8 +1,9 @@
 """evo_denoise_noalloc (working data in the device's fixed scratch array)
 against evo_denoise on the same policy and inputs, through the C ABI: two
 calls in a row, the second with a smaller batch, on the team variant, on
-one-workgroup tiles and on two-sample tiles; bookkeeping equal; a batch
-too large for the array refused before anything runs."""
+one-workgroup tiles and on two-sample tiles; bookkeeping equal; the call
+captured into a HIP graph and replayed; a batch too large for the array
+refused before anything runs."""
 import numpy as np
 import pytest
 
@@ -73,6 +74,54 @@ def test_noalloc_matches_denoise_twice(case):
         with pytest.raises(evo.EvoError) as e:
             pol.read_cache(0, 0)
         assert e.value.code == -2   # EVO_E_STATE: the cache lives in the scratch array
+    pol.close()
+
+
+@pytest.mark.parametrize("case", ["team", "two_sample"])
+def test_noalloc_captured_in_a_graph_replays(case):
+    """evo_denoise_noalloc enqueued while a stream is captured into a HIP
+    graph: three replays, with eager calls of the same policy and
+    synchronisations between them, each bitwise equal to the eager result
+    (the replays read the plan that the policy's pinned staging buffers hold
+    when they run; the eager calls in between restage the same bytes)."""
+    import torch
+    if case == "team":
+        s, dtype, B = I.PUSHT, "bf16", 2
+    else:
+        s, dtype, B = I.TINY, "fp32", 9
+    wts = I.make_weights(s, 6, "perturbed")
+    rng = np.random.default_rng([6, 3])
+    lats = [I.lattice_bernoulli(s.n_layers, s.n_steps, p, rng) for p in (0.2, 0.5)]
+    pol = _policy(s, wts, dtype, B, 2)
+    for j, lt in enumerate(lats):
+        pol.set_schedule(j, lt, O.GRAN_LAYER)
+    dev = device()
+    obs = torch.from_numpy(np.ascontiguousarray(I.make_obs(s, B, 21))).to(dev)
+    noise = torch.from_numpy(np.ascontiguousarray(I.make_noise(s, B, 21))).to(dev)
+    ids = rng.integers(0, 2, B).astype(np.int32)
+    shape = (B, s.horizon, s.action_dim)
+    ref = torch.zeros(shape, device=dev)
+    pol.denoise_noalloc(obs, noise, ids, ref)
+    pol.synchronize()
+    torch.cuda.synchronize()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    out = torch.zeros(shape, device=dev)
+    g = torch.cuda.CUDAGraph()
+    say(f"[gpu] noalloc graph capture ({case}, batch {B})")
+    with torch.cuda.graph(g, stream=side):
+        pol.denoise_noalloc(obs, noise, ids, out, stream=side)
+    for rep in range(3):
+        out.fill_(float("nan"))
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(out, ref), f"replay {rep}"
+        eager = torch.zeros(shape, device=dev)
+        pol.denoise_noalloc(obs, noise, ids, eager)
+        pol.synchronize()
+        torch.cuda.synchronize()
+        assert torch.equal(eager, ref), f"eager call after replay {rep}"
+    del g
     pol.close()
 
 
