@@ -87,8 +87,8 @@ typedef struct {
  * and an evaluation multiplies only against the S x n_heads folded
  * columns, so there F_CA counts 2(2 H S n_heads d) per evaluation and the
  * query adds 4 n_obs d^2 per layer for the fold.  The byte counters are this implementation's algorithmic
- * traffic: cache reads/writes of reused/refreshed residuals (fp32 values,
- * bf16 for policies of width above 256 with bf16 operands), and weight
+ * traffic: cache reads/writes of reused/refreshed residuals (fp16 values
+ * with bf16 operands, fp32 with fp32 operands), and weight
  * bytes of evaluated units summed over workgroups.  n_tiles counts the
  * sample tiles, n_workgroups the workgroups launched (small batches run
  * several workgroups per one-sample tile; each keeps its own caches, so the
@@ -183,7 +183,8 @@ int evo_denoise(evo_policy* p, int32_t batch, const float* obs_cond, const float
  * host heap memory): the plan is built in arrays sized at evo_create_policy
  * and staged through the policy's pinned buffers.  A batch whose working
  * data does not fit the array is refused with EVO_E_UNSUPPORTED before
- * anything is enqueued (Push-T-shaped policies: about 120 samples).  Every
+ * anything is enqueued (Push-T-shaped policies: about 200 samples with bf16
+ * operands, about 120 with fp32).  Every
  * call on a device shares that device's array, which keeps the last call's
  * contents (each call clears what must start at zero): calls that overlap
  * on one device race (different policies, or different threads); calls of
@@ -433,7 +434,8 @@ int evo_debug_team_withhold(evo_policy* p, int32_t enable);
 
 /* Test hook: synchronise the policy's device and copy the cached residual
  * of `unit` for `sample` of the last evo_denoise into host float[H][d]
- * (for a layer-granular schedule, unit 3l+2 holds the layer's merged sum). */
+ * (for a layer-granular schedule, unit 3l+2 holds the layer's merged sum;
+ * with bf16 operands the caches hold fp16 values, clamped to +-65504). */
 int evo_debug_read_cache(evo_policy* p, int32_t unit, int32_t sample, float* host_dst);
 
 /* Release all device and host resources (NULL is a no-op).  Synchronises

@@ -3,6 +3,7 @@
 
 #include <algorithm>
 #include <cstdlib>
+#include <cmath>
 #include <cstring>
 #include <mutex>
 #include <new>
@@ -18,6 +19,24 @@ const char* last_error();
 using namespace evo;
 
 namespace {
+
+// cached values read back to the host: IEEE binary16 to fp32
+float half_to_float(uint16_t h) {
+  const uint32_t sign = (uint32_t)(h & 0x8000u) << 16, e = (h >> 10) & 0x1Fu, m = h & 0x3FFu;
+  uint32_t u;
+  if (e == 0) {  // zero or subnormal: m * 2^-24
+    const float f = std::ldexp((float)m, -24);
+    std::memcpy(&u, &f, 4);
+    u |= sign;
+  } else if (e == 31) {
+    u = sign | 0x7F800000u | (m << 13);
+  } else {
+    u = sign | ((e + 112u) << 23) | (m << 13);
+  }
+  float f;
+  std::memcpy(&f, &u, 4);
+  return f;
+}
 
 #define HIP_TRY(expr)                                                                        \
   do {                                                                                       \
@@ -928,8 +947,7 @@ int evo_debug_read_cache(evo_policy* p, int32_t unit, int32_t sample, float* hos
       if (elt == 2) {
         uint16_t h;
         std::memcpy(&h, raw.data() + 2 * i, 2);
-        const uint32_t u = (uint32_t)h << 16;
-        std::memcpy(&buf[i], &u, 4);
+        buf[i] = half_to_float(h);
       } else {
         std::memcpy(&buf[i], raw.data() + 4 * i, 4);
       }

@@ -37,9 +37,9 @@ struct Shape {
   int dh() const { return d / nh; }
   int S() const { return 1 + n_obs; }
   int elt() const { return dtype == EVO_BF16 ? 2 : 4; }
-  // bytes per cached residual value: bf16 for the width-768 policy with
-  // bf16 operands, fp32 otherwise (the kernels' cache layout)
-  int cache_elt() const { return dtype == EVO_BF16 && d > 256 ? 2 : 4; }
+  // bytes per cached residual value (the kernels' cache layout): fp16 with
+  // bf16 operands, fp32 otherwise, at every tile size
+  int cache_elt() const { return dtype == EVO_BF16 ? 2 : 4; }
   // Cross-attention folded into per-token fold records (the kernels of
   // width 256 compile the folded unit; its n_heads x S score columns must
   // fit one 16-wide tile).

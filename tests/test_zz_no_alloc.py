@@ -128,7 +128,7 @@ def test_noalloc_captured_in_a_graph_replays(case):
 def test_noalloc_refuses_a_batch_beyond_the_scratch():
     import torch
     s = I.PUSHT
-    B = 200
+    B = 240   # one-sample tiles, fp16 caches: about 200 samples of this policy fit
     pol = _policy(s, I.make_weights(s, 0), "bf16", B, 1, {"EVO_TEAM": "0"})
     pol.set_schedule(0, I.make_lattice("dirichlet", s.n_layers, s.n_steps, 0.25, 0), O.GRAN_LAYER)
     dev = device()
