@@ -307,6 +307,50 @@ def test_step0_only_cache_holds_step0_residuals(dtype):
     pol.close()
 
 
+@pytest.mark.parametrize("gran", [O.GRAN_UNIT, O.GRAN_LAYER])
+def test_fp16_cache_saturates(gran):
+    """With bf16 operands the residual caches hold fp16: a cached residual
+    beyond the fp16 range reads back as +-65504 (a saturating store, never
+    an infinity) and values inside it to fp16 rounding.  Only step 0 is
+    refreshed, so the caches hold step-0 residuals; the first layer's
+    self-attention output bias puts three columns at 1e5, -2e5 and 3e4.
+    Layer-granular schedules cache the layer's summed residual in unit 2."""
+    s = I.PUSHT
+    wts = I.make_weights(s, 5, "perturbed")
+    I.split_weights(s, wts)["l0.b_o"][[3, 7, 11]] = [1e5, -2e5, 3e4]
+    obs, noise = I.make_obs(s, 1, 5), I.make_noise(s, 1, 5)
+    rows = 3 * s.n_layers if gran == O.GRAN_UNIT else s.n_layers
+    lat = np.zeros((rows, s.n_steps), np.uint8)
+    lat[:, 0] = 1
+    say(f"[gpu] fp16 cache saturation, granularity {gran}")
+    pol = _policy(s, wts, "bf16", 1, 1)
+    pol.set_schedule(0, lat, gran)
+    got, _ = run_gpu(pol, obs, noise, np.zeros(1, np.int32))
+    assert np.all(np.isfinite(got))
+    P = O.prepare_params(I.split_weights(s, wts), "bf16")
+    eff = O.effective_lattice(O.expand_lattice(lat, gran, s.n_layers), O.COLD_COMPUTE)
+    tr = {}
+    O.denoise_group(s, P, obs, noise, eff, trace=tr)
+    if gran == O.GRAN_UNIT:
+        unit, ref = 0, tr["r"][0, 0, 0]
+    else:
+        unit, ref = 2, tr["r"][0, 0, 0] + tr["r"][0, 1, 0] + tr["r"][0, 2, 0]
+    c = pol.read_cache(unit, 0).astype(np.float64)
+    pol.close()
+    assert np.all(np.isfinite(c))
+    big = np.abs(ref) > 65504.0
+    assert big[:, 3].all() and big[:, 7].all() and big.sum() == 2 * s.horizon
+    assert np.array_equal(c[big], np.sign(ref[big]) * 65504.0)
+    large = (np.abs(ref) > 1000.0) & ~big   # the 3e4 column: fp16 spacing 16 there
+    assert large[:, 11].all()
+    assert np.max(np.abs(c[large] - ref[large]) / np.abs(ref[large])) <= 3e-2
+    rest = ~big & ~large
+    scale = float(np.max(np.abs(ref[rest])))
+    err = float(np.max(np.abs(c[rest] - ref[rest])))
+    say(f"  saturated {int(big.sum())} values; other columns relative error {err / scale:.2e}")
+    assert err <= 3e-2 * scale
+
+
 @pytest.mark.parametrize("cold", [O.COLD_COMPUTE, O.COLD_ZERO])
 def test_printed_schedules(cold):
     """The paper's printed 24 x 100 unit schedules (three tasks, BAC and
