@@ -471,8 +471,9 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
   // layer-merged residual sum accumulated in registers, else in its cache slot
   constexpr bool MAC_REG = CBW * RB <= 4;
   static_assert(MAC_REG || SPT == 1 || sizeof(AT) == 4, "bf16 layer sums in memory need one sample per tile");
-  // weight fragments in flight per wave in the unit products
-  constexpr int INFL = (TEAM > 1 && RB == 1) ? 16 : (RB == 1 && CBW <= 2 ? 12 : 6);
+  // weight fragments in flight per wave in the unit products (at width 768
+  // the residual stream and the unit output leave room for 8)
+  constexpr int INFL = D > 256 ? 8 : (TEAM > 1 && RB == 1) ? 16 : (RB == 1 && CBW <= 2 ? 12 : 6);
   constexpr float kScale = (DH == 64) ? 0.125f : (DH == 32 ? 0.17677669529663688f : 0.0f);
   static_assert(DH == 64 || DH == 32, "head dim");
 
@@ -657,19 +658,31 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
   const auto cidx = [&](int unit, int c, int rb) {
     return (size_t)unit * (R * D) + ((size_t)((w * RB + rb) * CBW + c) * 64 + lane) * 4;
   };
+  // Cache-policy bits of the residual-cache accesses.  At width 768 a
+  // unit's weights exceed an XCD's L2 and a cached residual is 48 KiB, so
+  // cache reads and writes are non-temporal (evicted first) and leave the
+  // L2 to the weights; at width 256 the default policy measured faster.
+  constexpr int CPOL = D > 256 ? 2 : 0;
   const auto cload = [&](int unit, int c, int rb) -> f32x4 {
     if constexpr (CE == 2) {
-      const uint2 x = *reinterpret_cast<const uint2*>(cbase + cidx(unit, c, rb) * 2);
-      return f16x4_to_f32(x.x, x.y);
+      const u32x2* q = reinterpret_cast<const u32x2*>(cbase + cidx(unit, c, rb) * 2);
+      const u32x2 x = CPOL ? __builtin_nontemporal_load(q) : *q;
+      return f16x4_to_f32(x[0], x[1]);
     } else {
-      return *reinterpret_cast<const f32x4*>(cbase + cidx(unit, c, rb) * 4);
+      const f32x4* q = reinterpret_cast<const f32x4*>(cbase + cidx(unit, c, rb) * 4);
+      return CPOL ? __builtin_nontemporal_load(q) : *q;
     }
   };
   const auto cstore = [&](int unit, int c, int rb, f32x4 v) {
     if constexpr (CE == 2) {
-      *reinterpret_cast<uint2*>(cbase + cidx(unit, c, rb) * 2) = make_uint2(f16x2_sat(v[0], v[1]), f16x2_sat(v[2], v[3]));
+      u32x2* q = reinterpret_cast<u32x2*>(cbase + cidx(unit, c, rb) * 2);
+      const u32x2 x = {f16x2_sat(v[0], v[1]), f16x2_sat(v[2], v[3])};
+      if (CPOL) __builtin_nontemporal_store(x, q);
+      else *q = x;
     } else {
-      *reinterpret_cast<f32x4*>(cbase + cidx(unit, c, rb) * 4) = v;
+      f32x4* q = reinterpret_cast<f32x4*>(cbase + cidx(unit, c, rb) * 4);
+      if (CPOL) __builtin_nontemporal_store(v, q);
+      else *q = v;
     }
   };
   const uint4* pk = p.pk;
@@ -785,10 +798,10 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
           const int off = use ? (ub[q] * (R * D) + (w * RB * CBW * 64 + lane) * 4) * CE : 0x7FFFFFF0;
           const int cst = (rb * CBW + c) * 256 * CE;
           if constexpr (CE == 2) {
-            const auto x = __builtin_amdgcn_raw_buffer_load_b64(crs, off, cst, 0);
+            const auto x = __builtin_amdgcn_raw_buffer_load_b64(crs, off, cst, CPOL);
             v[q][c][rb] = f16x4_to_f32(x[0], x[1]);
           } else {
-            v[q][c][rb] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(crs, off, cst, 0));
+            v[q][c][rb] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(crs, off, cst, CPOL));
           }
         }
   };
@@ -1525,7 +1538,7 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
               } else if (pick(mst, j) & bit) {
                 if constexpr (CE == 2)
                   __builtin_amdgcn_raw_buffer_store_b64(u32x2{f16x2_sat(sum[0], sum[1]), f16x2_sat(sum[2], sum[3])}, crs,
-                                                        (int)(cidx(e, 0, 0) * 2), (rb * CBW + c) * 512, 0);
+                                                        (int)(cidx(e, 0, 0) * 2), (rb * CBW + c) * 512, CPOL);
                 else
                   cstore(e, c, rb, sum);
               }
