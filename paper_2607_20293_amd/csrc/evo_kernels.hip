@@ -658,10 +658,11 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
   const auto cidx = [&](int unit, int c, int rb) {
     return (size_t)unit * (R * D) + ((size_t)((w * RB + rb) * CBW + c) * 64 + lane) * 4;
   };
-  // Cache-policy bits of the residual-cache accesses.  At width 768 a
-  // unit's weights exceed an XCD's L2 and a cached residual is 48 KiB, so
-  // cache reads and writes are non-temporal (evicted first) and leave the
-  // L2 to the weights; at width 256 the default policy measured faster.
+  // Cache-policy bits of the residual-cache accesses (and of the layer
+  // sums kept in cache slots).  At width 768 a unit's weights exceed an
+  // XCD's L2 and a cached residual is 48 KiB, so these reads and writes are
+  // non-temporal (evicted first) and leave the L2 to the weights; at width
+  // 256 the default policy measured faster.
   constexpr int CPOL = D > 256 ? 2 : 0;
   const auto cload = [&](int unit, int c, int rb) -> f32x4 {
     if constexpr (CE == 2) {
@@ -1506,7 +1507,7 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
               if (j == jj) mg = mmg[jj];
             const bool need = u > 0 && mg && ((pick(mev, j) >> e) & 1ull);
             lsum[c][rb] = __builtin_bit_cast(
-                f32x4, __builtin_amdgcn_raw_buffer_load_b128(crs, need ? lacc_base : 0x7FFFFFF0, lacc_cst(c, rb), 0));
+                f32x4, __builtin_amdgcn_raw_buffer_load_b128(crs, need ? lacc_base : 0x7FFFFFF0, lacc_cst(c, rb), CPOL));
           }
       }
       // Eq. 1 per sample at unit e: evaluated residual (and cache refresh) or
@@ -1534,7 +1535,7 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
               // the three residuals is stored at the FFN position
               const f32x4 sum = (u == 0) ? v : lsum[c][rb] + v;
               if (CE == 4 || u < 2) {
-                __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, sum), crs, lacc_base, lacc_cst(c, rb), 0);
+                __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, sum), crs, lacc_base, lacc_cst(c, rb), CPOL);
               } else if (pick(mst, j) & bit) {
                 if constexpr (CE == 2)
                   __builtin_amdgcn_raw_buffer_store_b64(u32x2{f16x2_sat(sum[0], sum[1]), f16x2_sat(sum[2], sum[3])}, crs,
