@@ -659,10 +659,11 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
     return (size_t)unit * (R * D) + ((size_t)((w * RB + rb) * CBW + c) * 64 + lane) * 4;
   };
   // Cache-policy bits of the residual-cache accesses (and of the layer
-  // sums kept in cache slots).  At width 768 a unit's weights exceed an
-  // XCD's L2 and a cached residual is 48 KiB, so these reads and writes are
-  // non-temporal (evicted first) and leave the L2 to the weights; at width
-  // 256 the default policy measured faster.
+  // sums kept in cache slots and the memory tokens' keys and values).  At
+  // width 768 a unit's weights exceed an XCD's L2 and a cached residual is
+  // 48 KiB, so these reads and writes are non-temporal (evicted first) and
+  // leave the L2 to the weights; at width 256 the default policy measured
+  // faster.
   constexpr int CPOL = D > 256 ? 2 : 0;
   const auto cload = [&](int unit, int c, int rb) -> f32x4 {
     if constexpr (CE == 2) {
@@ -1240,7 +1241,8 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
             const bool obs_tok = ok && sm_ > 0;
             // 32-bit offsets: the observation K/V of a member is below 2^31 floats
             const int off = obs_tok ? ((s_ * L + l) * nobs + (sm_ - 1)) * (2 * D) + gcol : gcol;
-            kvv[q] = (obs_tok ? okv : trow)[off];
+            const float* src = &(obs_tok ? okv : trow)[off];
+            kvv[q] = CPOL ? __builtin_nontemporal_load(src) : *src;  // read once per evaluation
             kvok[q] = ok;
           }
         };
