@@ -615,7 +615,10 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
   // the sentinel has not been written yet; every member resets its own slot
   // of unit n-1 once it holds all partials of unit n (then every member has
   // finished reading unit n-1), which is the slot's next use at unit n+2.
-  constexpr int kCoherent = 16;            // SC1 cache-policy bit: device-coherent access
+  // SC1 cache-policy bit: device-coherent access; at width 768 also the
+  // non-temporal bit, so that the exchange traffic (three 96 KiB slots per
+  // member and unit) does not displace the weights from the L2
+  constexpr int kCoherent = D > 256 ? (16 | 2) : 16;
   constexpr unsigned kEmpty = 0xFFFFFFFFu;  // never produced by arithmetic (canonical NaN differs)
   int nbar = 0;                             // evaluated units exchanged so far
   float* const xb = TEAM > 1 ? p.xchg + (size_t)tile * (3 * TEAM) * (R * D) : nullptr;
