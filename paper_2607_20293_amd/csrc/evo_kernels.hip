@@ -472,8 +472,12 @@ __global__ void __launch_bounds__(NW * 64) denoise_kernel(const KParams p) {
   constexpr bool MAC_REG = CBW * RB <= 4;
   static_assert(MAC_REG || SPT == 1 || sizeof(AT) == 4, "bf16 layer sums in memory need one sample per tile");
   // weight fragments in flight per wave in the unit products (at width 768
-  // the residual stream and the unit output leave room for 8)
-  constexpr int INFL = D > 256 ? 8 : (TEAM > 1 && RB == 1) ? 16 : (RB == 1 && CBW <= 2 ? 12 : 6);
+  // and in two-sample bf16 tiles the residual stream and the unit output
+  // leave room for 8)
+  constexpr int INFL = D > 256 ? 8
+                       : (TEAM > 1 && RB == 1) ? 16
+                       : (RB == 1 && CBW <= 2) ? 12
+                       : sizeof(AT) == 2 ? 8 : 6;
   constexpr float kScale = (DH == 64) ? 0.125f : (DH == 32 ? 0.17677669529663688f : 0.0f);
   static_assert(DH == 64 || DH == 32, "head dim");
 
