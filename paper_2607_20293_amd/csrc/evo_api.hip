@@ -399,10 +399,10 @@ int evo_create_policy(const evo_policy_desc* desc, const float* host_weights, si
       // launch.  A team size t serves batches up to n_cu / t, the largest
       // compiled size that fits being chosen.  With bf16 operands the
       // automatic choice keeps only the smallest size: teams of 2 measured
-      // faster than teams of 4 at every batch (Push-T shape, 25% density,
-      // batch 1 to 64: 4.19-4.31 ms against 4.37-4.85 ms), while with fp32
-      // operands teams of 4 are far ahead wherever they fit (6.7-6.8 ms
-      // against 9.3-9.5 ms up to batch 64).
+      // faster than teams of 4 at every batch (Push-T shape, 25% density:
+      // 3.57 and 3.63 ms at batch 1 and 64 against 3.65 and 4.06 ms), while
+      // with fp32 operands teams of 4 are far ahead wherever they fit
+      // (6.7-6.8 ms against 9.3-9.5 ms up to batch 64).
       // EVO_TEAM=0 switches teams off, EVO_TEAM=<size> keeps only that size.
       const char* env = std::getenv("EVO_TEAM");
       const int team_only = env ? std::atoi(env) : -1;
